@@ -1,0 +1,92 @@
+"""Plants plausible mistakes in copies of the oracle (on the CPU) and checks
+that the pins in ``test_oracle_pins.py`` catch every one of them.
+
+Each mutant is a one-line textual edit of ``oracle/avq_oracle.c`` compiled
+into a temporary library; the pins are then run against it and at least one
+must fail. The real oracle is restored afterwards.
+"""
+import contextlib
+import subprocess
+from pathlib import Path
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = Path(oracle.__file__).resolve().parent / "avq_oracle.c"
+
+# (name, original text, mutated text)
+MUTANTS = [
+    ("denominator drops the count weight",
+     "Z += A * (double)n[a];", "Z += A;"),
+    ("child moves on equal distance",
+     "code_idx[t] = (dc < dbest)", "code_idx[t] = (dc <= dbest)"),
+    ("parent ties go to the highest index",
+     "if (dist < dbest) {\n        dsecond = dbest;", "if (dist <= dbest) {\n        dsecond = dbest;"),
+    ("importance drops the count weight",
+     "if (n[a] > 0) wt[a] += (double)n[a] * exp(S[a] - mu) / Z;",
+     "if (n[a] > 0) wt[a] += exp(S[a] - mu) / Z;"),
+    ("top-P takes the smallest importance",
+     "if (best < 0 || wr[a] > wr[best]) best = a;", "if (best < 0 || wr[a] < wr[best]) best = a;"),
+    ("correction sign flipped",
+     "double dA = exp(Tc[k * Ch + c] - mu) - Ap;", "double dA = Ap - exp(Tc[k * Ch + c] - mu);"),
+    ("recovered logit uses the first child only",
+     "R[k] = recovered ? mean / Ch : S[p];", "R[k] = recovered ? Tc[k * Ch] : S[p];"),
+    ("child code index transposed",
+     "(M0 + best * Ch + cbest)", "(M0 + cbest * M0 + best)"),
+    ("parent rows only count keys that stayed",
+     "      n[p] += 1;\n", "      if (code_idx[t] < M0) n[p] += 1;\n"),
+    ("empty children not masked in the correction",
+     "          if (n[code] == 0) continue;\n          double dA", "          double dA"),
+    ("importance uses an unnormalised weight",
+     "wt[a] += (double)n[a] * exp(S[a] - mu) / Z;", "wt[a] += (double)n[a] * exp(S[a] - mu);"),
+    ("child logits against the parent codeword",
+     "double v = dot(q, Cc + (((long long)h * M0 + p) * Ch + c) * d, d);",
+     "double v = dot(q, Cp + ((long long)h * M0 + p) * d, d);"),
+]
+
+PIN_CALLS = [
+    lambda: pins.test_assign_matches_cdist(0),
+    pins.test_assign_exact_ties_lowest_index,
+    pins.test_aggregates_match_add_at_and_invariants,
+    lambda: pins.test_importance_equals_per_key_attention_mass(32),
+    lambda: pins.test_topp_matches_enumeration(3),
+    pins.test_p0_is_vq_attention,
+    lambda: pins.test_refined_direct_equals_per_key_replacement(2, 32),
+    pins.test_refined_recovered_per_key_weights,
+    pins.test_zero_queries_give_mean_value,
+    pins.test_children_equal_parent_reduce_to_vq,
+    pins.test_large_logits_stay_finite,
+    pins.test_empty_far_children_do_not_poison,
+]
+
+
+@contextlib.contextmanager
+def mutant_library(tmp_path, old, new):
+    src = SRC.read_text()
+    assert src.count(old) == 1, f"mutation anchor not unique: {old!r}"
+    mpath = tmp_path / "mutant.c"
+    mpath.write_text(src.replace(old, new))
+    so = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O1", "-std=c99", "-fopenmp", "-fPIC", "-shared", str(mpath),
+                    "-o", str(so), "-lm"], check=True)
+    saved = oracle._load()
+    oracle._lib = oracle.open_library(so)
+    try:
+        yield
+    finally:
+        oracle._lib = saved
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new):
+    caught = []
+    with mutant_library(tmp_path, old, new):
+        for call in PIN_CALLS:
+            try:
+                call()
+            except (AssertionError, ValueError, FloatingPointError):
+                caught.append(call)
+                break
+    assert caught, f"no pin fails for the mutant '{name}'"

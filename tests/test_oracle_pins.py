@@ -1,0 +1,342 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each check goes through a route other than the oracle's own formulas (library
+routines, exhaustive enumeration, closed forms, invariants), so that a dropped
+term, a wrong sign or index, or a transposed operand in the oracle fails at
+least one of them. ``test_oracle_mutants.py`` plants such mistakes in copies
+of the oracle and checks that these pins catch them.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_12789_amd import inputs
+from tests import references as ref
+
+
+def small(**kw):
+    base = dict(name="pin", B=1, H=2, N=100, d=8, M0=6, Ch=4, P=2, block_q=32,
+                dtype="f32", sigma_c=0.3, sigma_k=0.2, q_scale=2.0, seed=3)
+    base.update(kw)
+    return inputs.Workload(**base)
+
+
+def np64(t):
+    return oracle.f64(t)
+
+
+def run(x, w, recovered=True):
+    return oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], w.P, w.block_q,
+                          recovered=recovered)
+
+
+# ---------------------------------------------------------------- assignment
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_assign_matches_cdist(seed):
+    """Sec. 3.2 assignment and Alg. 1 tree refinement against scipy cdist."""
+    w = small(seed=seed)
+    x = inputs.generate(w)
+    o = oracle.assign(x["K"], x["Cp"], x["Cc"])
+    par, code = ref.tree_assign(np64(x["K"]), np64(x["Cp"]), np64(x["Cc"]))
+    np.testing.assert_array_equal(o["parent_idx"], par)
+    np.testing.assert_array_equal(o["code_idx"], code)
+    assert (code >= w.M0).any() and (code < w.M0).any()  # both branches exercised
+
+
+def test_assign_exact_ties_lowest_index():
+    """Dyadic inputs: exact ties between codewords resolve to the lowest index,
+    and equal child/parent distances keep the key on its parent (strict <)."""
+    x = inputs.dyadic_exact(B=1, H=2, N=300, d=4, M0=5, Ch=4, seed=7)
+    Cp = x["Cp"].clone()
+    Cp[0, 3] = Cp[0, 1]  # duplicate parent: index 3 can never win
+    x["Cp"] = Cp
+    o = oracle.assign(x["K"], x["Cp"], x["Cc"])
+    par, code = ref.tree_assign(np64(x["K"]), np64(x["Cp"]), np64(x["Cc"]))
+    np.testing.assert_array_equal(o["parent_idx"], par)
+    np.testing.assert_array_equal(o["code_idx"], code)
+    assert not (o["parent_idx"][0, 0] == 3).any()
+    # some exact parent ties and some exact child/parent ties actually occur
+    ties = o["d_parent2"] == o["d_parent"]
+    assert ties.any()
+    stay_tie = (o["d_child"] == o["d_parent"])
+    assert stay_tie.any()
+    assert (o["code_idx"][stay_tie] < 5).all()
+
+
+def test_assign_codebook_equals_keys():
+    """Codebook made of the keys themselves: every key is its own codeword."""
+    rng = np.random.default_rng(0)
+    K = rng.standard_normal((1, 1, 40, 6))
+    Cp = K[0].copy()
+    Cc = np.repeat(Cp[:, :, None, :], 2, axis=2)
+    o = oracle.assign(K, Cp, Cc)
+    np.testing.assert_array_equal(o["parent_idx"][0, 0], np.arange(40))
+    np.testing.assert_array_equal(o["code_idx"][0, 0], np.arange(40))
+    assert (o["d_parent"] == 0).all()
+
+
+# ---------------------------------------------------------------- aggregates
+
+def test_aggregates_match_add_at_and_invariants():
+    """Eq. (aggregates): bincount/add.at route; sum of parent counts is N per
+    head; parent rows sum to the total value; children never exceed parents."""
+    w = small(B=2, H=3, N=257, sigma_k=0.2)
+    x = inputs.generate(w)
+    o = oracle.assign(x["K"], x["Cp"], x["Cc"])
+    Vbar, n = oracle.aggregate(x["V"], o["parent_idx"], o["code_idx"], w.M0, w.Ch)
+    Vr, nr = ref.aggregates(np64(x["V"]), o["parent_idx"].astype(np.int64),
+                            o["code_idx"].astype(np.int64), w.M0, w.Ch)
+    np.testing.assert_array_equal(n, nr)
+    np.testing.assert_allclose(Vbar, Vr, rtol=0, atol=1e-12)
+    assert (n[..., :w.M0].sum(-1) == w.N).all()
+    np.testing.assert_allclose(Vbar[..., :w.M0, :].sum(-2), np64(x["V"]).sum(-2), atol=1e-10)
+    child = n[..., w.M0:].reshape(w.B, w.H, w.M0, w.Ch).sum(-1)
+    assert (child <= n[..., :w.M0]).all()
+
+
+# ---------------------------------------------------------------- importance
+
+@pytest.mark.parametrize("block_q", [32, 100, 7])
+def test_importance_equals_per_key_attention_mass(block_q):
+    """Eq. (importance) equals the softmax mass that a tile's queries put on
+    the keys of each parent cell (per-key route through torch.softmax), and it
+    sums to the tile size (attention weights sum to 1)."""
+    w = small(block_q=block_q)
+    x = inputs.generate(w)
+    o = run(x, w)
+    Q, Cp = np64(x["Q"]), np64(x["Cp"])
+    T = w.n_tiles
+    for b in range(w.B):
+        for h in range(w.H):
+            for t in range(T):
+                rows = slice(t * block_q, min((t + 1) * block_q, w.N))
+                wr = ref.per_key_importance(Q[b, h, rows], Cp[h], o["parent_idx"][b, h])
+                np.testing.assert_allclose(o["importance"][b, h, t], wr, rtol=1e-10,
+                                           atol=1e-13)
+                n_rows = rows.stop - rows.start
+                assert abs(o["importance"][b, h, t].sum() - n_rows) < 1e-9 * n_rows
+
+
+def test_importance_zero_for_empty_parents():
+    w = small(M0=12, N=40)
+    x = inputs.generate(w)
+    o = run(x, w)
+    empty = o["counts"][..., :w.M0] == 0
+    assert empty.any()
+    wimp = o["importance"]
+    for t in range(w.n_tiles):
+        assert (wimp[:, :, t][empty] == 0).all()
+
+
+# ---------------------------------------------------------------- top-P
+
+@pytest.mark.parametrize("P", [0, 1, 3, 6])
+def test_topp_matches_enumeration(P):
+    rng = np.random.default_rng(P)
+    for trial in range(20):
+        wv = rng.random(6)
+        if trial % 3 == 0:
+            wv = np.round(wv * 3) / 3  # exact ties
+        if trial % 4 == 1:
+            wv[rng.integers(0, 6, 2)] = 0.0
+        sel = oracle.topp(wv[None], P)[0]
+        np.testing.assert_array_equal(sel, ref.topp_by_enumeration(wv, P))
+
+
+# ---------------------------------------------------------------- output
+
+def test_p0_is_vq_attention():
+    """P = 0: plain VQ attention of Sec. 3.2, i.e. per-key softmax attention
+    with each key replaced by its parent codeword (SDPA route)."""
+    w = small(P=0)
+    x = inputs.generate(w)
+    o = run(x, w)
+    Q, V, Cp = np64(x["Q"]), np64(x["V"]), np64(x["Cp"])
+    for b in range(w.B):
+        for h in range(w.H):
+            khat = Cp[h][o["parent_idx"][b, h]]
+            np.testing.assert_allclose(o["Y"][b, h], ref.sdpa(Q[b, h], khat, V[b, h]),
+                                       rtol=1e-10, atol=1e-12)
+
+
+def test_one_codeword_per_key_is_exact_attention():
+    """Codebook = the keys (M0 = N, distinct keys) and P = 0: exact softmax
+    attention, Eq. (standardattention), through torch SDPA."""
+    rng = np.random.default_rng(5)
+    N, d = 48, 8
+    Q = rng.standard_normal((1, 1, N, d)) * 0.7
+    K = rng.standard_normal((1, 1, N, d))
+    V = rng.standard_normal((1, 1, N, d))
+    Cp = K[0].copy()
+    Cc = np.repeat(Cp[:, :, None, :], 2, axis=2)
+    o = oracle.forward(Q, K, V, Cp, Cc, P=0, block_q=16)
+    np.testing.assert_allclose(o["Y"][0, 0], ref.sdpa(Q[0, 0], K[0, 0], V[0, 0]),
+                               rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("P", [1, 2, 6])
+@pytest.mark.parametrize("block_q", [32, 13])
+def test_refined_direct_equals_per_key_replacement(P, block_q):
+    """App. C: updating with the correcting attention equals attention over
+    keys where every key that moved to a child of a selected parent is
+    represented by that child, and all others by their parent. Checked with the
+    direct parent logit (App. C form) against SDPA per tile, using the oracle's
+    own top-P sets, which the enumeration test pins."""
+    w = small(P=P, block_q=block_q)
+    x = inputs.generate(w)
+    o = run(x, w, recovered=False)
+    Q, V, Cp, Cc = np64(x["Q"]), np64(x["V"]), np64(x["Cp"]), np64(x["Cc"])
+    for b in range(w.B):
+        for h in range(w.H):
+            for t in range(w.n_tiles):
+                rows = slice(t * block_q, min((t + 1) * block_q, w.N))
+                khat = ref.quantised_keys(Cp[h], Cc[h], o["parent_idx"][b, h],
+                                          o["code_idx"][b, h], o["selection"][b, h, t])
+                np.testing.assert_allclose(o["Y"][b, h, rows],
+                                           ref.sdpa(Q[b, h, rows], khat, V[b, h]),
+                                           rtol=1e-9, atol=1e-11)
+
+
+def test_refined_recovered_per_key_weights():
+    """Eq. (parent_recovery) form: per key, a moved key of a selected parent
+    carries weight e^{T} + e^{S_p} - e^{mean_c T_c}; every other key e^{S_p}.
+    Evaluated key by key in NumPy (no aggregates) and compared to the oracle."""
+    w = small(P=2, block_q=20, sigma_c=0.5)
+    x = inputs.generate(w)
+    o = run(x, w, recovered=True)
+    Q, V, Cp, Cc = np64(x["Q"]), np64(x["V"]), np64(x["Cp"]), np64(x["Cc"])
+    for b in range(w.B):
+        for h in range(w.H):
+            par, code = o["parent_idx"][b, h], o["code_idx"][b, h]
+            for t in range(w.n_tiles):
+                sel = o["selection"][b, h, t]
+                for i in range(t * w.block_q, min((t + 1) * w.block_q, w.N)):
+                    q = Q[b, h, i]
+                    sp = Cp[h][par] @ q
+                    wgt = np.exp(sp)
+                    for j in range(w.N):
+                        if code[j] >= w.M0 and par[j] in sel:
+                            c = code[j] - w.M0
+                            tc = Cc[h, c // w.Ch, c % w.Ch] @ q
+                            mean_t = (Cc[h, par[j]] @ q).mean()
+                            wgt[j] = np.exp(tc) + np.exp(sp[j]) - np.exp(mean_t)
+                    y = (wgt[:, None] * V[b, h]).sum(0) / wgt.sum()
+                    np.testing.assert_allclose(o["Y"][b, h, i], y, rtol=1e-9, atol=1e-11)
+
+
+def test_recovered_equals_direct_on_exact_constraint():
+    """Eq. (parent_recovery) is exact when the parent is exactly the mean of its
+    children: on dyadic codebooks the two forms agree to rounding."""
+    x = inputs.dyadic_exact(B=1, H=2, N=200, d=8, M0=6, Ch=4, seed=11, dtype="f32")
+    oa = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], 3, 32, recovered=True)
+    ob = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], 3, 32, recovered=False)
+    np.testing.assert_allclose(oa["Y"], ob["Y"], rtol=1e-13, atol=1e-13)
+    assert (oa["code_idx"] >= 6).any()
+
+
+def test_full_p_is_tree_vq_attention():
+    """P = M0: every moved key is represented by its child, every other key by
+    its parent, independent of importance (SDPA route)."""
+    w = small(P=6)
+    x = inputs.generate(w)
+    o = run(x, w, recovered=False)
+    Q, V, Cp, Cc = np64(x["Q"]), np64(x["V"]), np64(x["Cp"]), np64(x["Cc"])
+    for b in range(w.B):
+        for h in range(w.H):
+            khat = ref.quantised_keys(Cp[h], Cc[h], o["parent_idx"][b, h], o["code_idx"][b, h])
+            np.testing.assert_allclose(o["Y"][b, h], ref.sdpa(Q[b, h], khat, V[b, h]),
+                                       rtol=1e-9, atol=1e-11)
+
+
+def test_zero_queries_give_mean_value():
+    """Q = 0: every logit is 0, so each key has weight 1 and Y is the plain mean
+    of V for every P (parents count n, corrections vanish)."""
+    w = small(P=3)
+    x = inputs.generate(w)
+    x["Q"] = torch.zeros_like(x["Q"])
+    o = run(x, w)
+    mean = np64(x["V"]).mean(axis=2, keepdims=True)
+    np.testing.assert_allclose(o["Y"], np.broadcast_to(mean, o["Y"].shape), rtol=1e-12,
+                               atol=1e-13)
+
+
+def test_children_equal_parent_reduce_to_vq():
+    """Children identical to their parent: no key moves (strict <), every child
+    is empty, and the output equals P = 0 VQ attention for every P."""
+    w = small(P=3)
+    x = inputs.generate(w)
+    x["Cc"] = x["Cp"][:, :, None, :].expand(-1, -1, w.Ch, -1).contiguous()
+    o = run(x, w)
+    assert (o["code_idx"] < w.M0).all()
+    assert (o["counts"][..., w.M0:] == 0).all()
+    o0 = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], 0, w.block_q)
+    np.testing.assert_allclose(o["Y"], o0["Y"], rtol=1e-13, atol=1e-14)
+
+
+def test_linearity_in_values():
+    w = small(P=2)
+    x = inputs.generate(w)
+    rng = np.random.default_rng(1)
+    V2 = rng.standard_normal(x["V"].shape)
+    o1 = run(x, w)
+    x2 = dict(x, V=torch.from_numpy(V2))
+    o2 = run(x2, w)
+    x3 = dict(x, V=torch.from_numpy(2.0 * np64(x["V"]) - 3.0 * V2))
+    o3 = run(x3, w)
+    np.testing.assert_allclose(o3["Y"], 2.0 * o1["Y"] - 3.0 * o2["Y"], rtol=1e-10, atol=1e-11)
+    x4 = dict(x, V=torch.full(x["V"].shape, 0.75, dtype=torch.float64))
+    np.testing.assert_allclose(run(x4, w)["Y"], 0.75, rtol=1e-12)
+
+
+def test_key_permutation_invariance_and_query_tile_equivariance():
+    w = small(P=2, block_q=25)
+    x = inputs.generate(w)
+    o = run(x, w)
+    rng = np.random.default_rng(2)
+    perm = rng.permutation(w.N)
+    xk = dict(x, K=x["K"][:, :, perm], V=x["V"][:, :, perm])
+    np.testing.assert_allclose(run(xk, w)["Y"], o["Y"], rtol=1e-11, atol=1e-12)
+    qperm = np.concatenate([t * 25 + rng.permutation(25) for t in range(4)])
+    xq = dict(x, Q=x["Q"][:, :, qperm])
+    np.testing.assert_allclose(run(xq, w)["Y"], o["Y"][:, :, qperm], rtol=1e-11, atol=1e-12)
+
+
+def test_large_logits_stay_finite():
+    """App. D: masked running max and zeroed empty codes keep Q x 20 finite."""
+    w = small(P=3, M0=12, N=60)
+    x = inputs.generate(w)
+    x["Q"] = x["Q"] * 20
+    o = run(x, w)
+    assert np.isfinite(o["Y"]).all()
+    assert (o["zratio"] > 0).all()
+
+
+def test_empty_far_children_do_not_poison():
+    """App. D: a selected parent whose children lie far away on both sides (so
+    they are empty and the parent is still their exact mean) has child logits
+    far above the running max. Their e^{T - m} overflows fp64; the empty-code
+    mask must keep the output finite and equal to per-key attention."""
+    rng = np.random.default_rng(4)
+    d, M0, Ch, N = 4, 3, 2, 60
+    Cp = rng.integers(-4, 5, size=(1, M0, d)).astype(np.float64)
+    Cc = Cp[:, :, None, :] + np.array([0.25, -0.25])[None, None, :, None]
+    far = np.zeros(d)
+    far[0] = 512.0
+    Cc[0, 0, 0] = Cp[0, 0] + far
+    Cc[0, 0, 1] = Cp[0, 0] - far
+    comp = rng.integers(0, M0, size=N)
+    K = (Cp[0, comp] + rng.integers(-1, 2, size=(N, d)) / 8.0)[None, None]
+    Q = np.zeros((1, 1, N, d))
+    Q[0, 0, :, 0] = np.where(np.arange(N) % 2 == 0, 3.0, -3.0)
+    Q[0, 0, :, 1:] = rng.integers(-2, 3, size=(N, d - 1)) / 4.0
+    V = rng.standard_normal((1, 1, N, d))
+    o = oracle.forward(Q, K, V, Cp, Cc, P=M0, block_q=16)
+    assert o["counts"][0, 0, M0:M0 + Ch].sum() == 0  # both far children are empty
+    assert np.isfinite(o["Y"]).all()
+    for t in range(4):
+        rows = slice(16 * t, min(16 * t + 16, N))
+        khat = ref.quantised_keys(Cp[0], Cc[0], o["parent_idx"][0, 0], o["code_idx"][0, 0])
+        np.testing.assert_allclose(o["Y"][0, 0, rows], ref.sdpa(Q[0, 0, rows], khat, V[0, 0]),
+                                   rtol=1e-9, atol=1e-11)
