@@ -1,0 +1,158 @@
+/*
+ * avq.h - C ABI of the MI355X (gfx950) AVQ-Attention forward pass.
+ *
+ * AVQ-Attention (Adaptive Vector-Quantized Attention) replaces keys by
+ * codewords of a two-level codebook: M0 parents per head, each with Ch
+ * children whose mean is the parent (Sec. 4.1, Eq. (parent_constraint)).
+ * The forward pass is split into three calls, in this order:
+ *
+ *   avq_assign         keys -> nearest parent, then nearest child of that
+ *                      parent (Sec. 4.2, Alg. 1)
+ *   avq_aggregate      per-codeword key counts and value sums
+ *                      (Eq. (aggregates), Alg. 1)
+ *   avq_attention_fwd  parent attention, per-query-tile importance, top-P
+ *                      parent selection, child refinement with correcting
+ *                      attention and normalisation (Sec. 4.3,
+ *                      Eq. (vqflashattention), (importance),
+ *                      (parent_recovery), (correcting_attention), Alg. 2)
+ *
+ * Conventions shared by every call:
+ *   - Every array argument is a DEVICE pointer owned by the caller, contiguous,
+ *     row-major and 16-byte aligned. Inputs are never written. Outputs are
+ *     fully overwritten.
+ *   - Tensors: Q, K, V, Y are [B][H][N][d]; the codebook is Cp [H][M0][d]
+ *     (parents) and Cc [H][M0][Ch][d] (children of parent p in rows
+ *     p*Ch .. p*Ch+Ch-1), shared across the batch (one codebook per head).
+ *   - Codes: Mtot = M0*(1+Ch). Code p < M0 is parent p; code M0 + p*Ch + c is
+ *     child c of parent p.
+ *   - dtype selects the element type of Q, K, V, Cp, Cc and Y: AVQ_F32 (fp32)
+ *     or AVQ_BF16 (bfloat16). Aggregated values are always fp32, counts int32.
+ *   - Logits are exactly Q.C (the paper leaves the 1/sqrt(d) scale out of its
+ *     formulas, Eq. (standardattention)); callers fold any scale into Q.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream). No call synchronises the device or allocates device memory.
+ *   - Arguments are validated on the host before anything is launched; a
+ *     non-OK status means nothing was enqueued (AVQ_ERR_DEVICE: a launch was
+ *     rejected). avq_last_error() then returns a message for the calling
+ *     thread. Non-finite inputs are not checked; they propagate.
+ *   - Supported: d in {64, 128}; Ch in {1, 2, 4, 8, 16}; 1 <= M0 <= 512;
+ *     N >= 1, B >= 1, H >= 1 and B*H*N*d < 2^31. Other shapes return
+ *     AVQ_ERR_UNSUPPORTED.
+ */
+#ifndef AVQ_H
+#define AVQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AVQ_OK = 0,
+  AVQ_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, P outside [0, M0], ... */
+  AVQ_ERR_UNSUPPORTED = 2, /* valid, but a shape/dtype this build has no kernel for */
+  AVQ_ERR_DEVICE = 3       /* the HIP runtime rejected a launch */
+} avq_status_t;
+
+typedef enum { AVQ_F32 = 0, AVQ_BF16 = 1 } avq_dtype_t;
+
+/* Version of this ABI (major * 10000 + minor * 100 + patch). */
+int avq_version(void);
+
+/* Message for the last non-OK status returned to the calling thread
+ * ("" if none). The pointer stays valid until the thread's next call. */
+const char* avq_last_error(void);
+
+/*
+ * avq_assign - tree vector quantisation of the keys (Sec. 3.2 assignment with
+ * squared Euclidean distance; Sec. 4.2 and Alg. 1 parent/child loops).
+ *
+ * For every key K[b][h][j]:
+ *   parent_idx = p* = argmin_p ||K_j - Cp[h][p]||^2, lowest p on exact ties;
+ *   c*            = argmin_c ||K_j - Cc[h][p*][c]||^2, lowest c on exact ties;
+ *   code_idx      = M0 + p* * Ch + c* if that child distance is strictly below
+ *                   the parent distance, else p*.
+ * Distances are evaluated in fp32 from the stored inputs.
+ *
+ *   K            [B][H][N][d]   dtype
+ *   Cp           [H][M0][d]     dtype
+ *   Cc           [H][M0][Ch][d] dtype
+ *   parent_idx   [B][H][N]      int32, out
+ *   code_idx     [B][H][N]      int32, out
+ */
+avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                        int32_t M0, int32_t Ch, const void* K, const void* Cp,
+                        const void* Cc, int32_t* parent_idx, int32_t* code_idx,
+                        void* stream);
+
+/*
+ * avq_aggregate - per-codeword counts and value sums (Eq. (aggregates)).
+ *
+ * Parent rows p < M0 cover the whole parent cell (every key whose nearest
+ * parent is p, whether or not it moved to a child: Alg. 1 adds to the parent
+ * unconditionally); child rows M0 + p*Ch + c cover the keys that moved to
+ * that child. The parent of a key is code_idx itself when code_idx < M0 and
+ * (code_idx - M0) / Ch otherwise.
+ *
+ *   V         [B][H][N][d]      dtype
+ *   code_idx  [B][H][N]         int32, values in [0, Mtot) (as avq_assign writes)
+ *   Vbar      [B][H][Mtot][d]   fp32, out
+ *   counts    [B][H][Mtot]      int32, out
+ *
+ * Sums are accumulated in fp32 with atomics, so the rounding of Vbar may vary
+ * between runs; counts are exact.
+ */
+avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                           int32_t M0, int32_t Ch, const void* V, const int32_t* code_idx,
+                           float* Vbar, int32_t* counts, void* stream);
+
+/*
+ * avq_attention_fwd - the fused refined-codebook attention (Alg. 2).
+ *
+ * Queries are taken in tiles of block_q consecutive tokens (the last tile may
+ * be shorter). For each tile I and query i in I:
+ *   parent pass  S_ip = Q_i . Cp_p; running max over non-empty parents
+ *                (App. D); A_ip = exp(S_ip - m_i), zero for empty parents;
+ *                Xbar_i = sum_p A_ip Vbar_p, Zbar_i = sum_p A_ip n_p
+ *                (Eq. (vqflashattention));
+ *   importance   w_p(I) = sum_{i in I} A_ip n_p / Zbar_i (Eq. (importance));
+ *   top-P        the P parents of largest w (lowest index on ties);
+ *   children     for every selected p and child c: T_ic = Q_i . Cc_pc; the
+ *                running max is raised over non-empty children and Xbar, Zbar
+ *                rescaled; the parent logit is recovered as the mean of all Ch
+ *                child logits (Eq. (parent_recovery)); the correcting weight
+ *                dA = exp(T_ic - m) - exp(Srec_ip - m), zero for empty children
+ *                (Eq. (correcting_attention)), adds dA * Vbar_pc to Xbar and
+ *                dA * n_pc to Zbar;
+ *   output       Y_i = Xbar_i / Zbar_i.
+ * P = 0 gives plain VQ attention over the parents (Sec. 3.2).
+ *
+ *   P            0 <= P <= M0
+ *   block_q      query tile size, 1 <= block_q <= 256 (semantic: importance
+ *                and top-P are computed per tile of block_q tokens)
+ *   Q            [B][H][N][d]    dtype
+ *   Cp, Cc       as in avq_assign
+ *   Vbar, counts as written by avq_aggregate
+ *   Y            [B][H][N][d]    dtype, out
+ *   topp_idx     [B][H][T][P]    int32, out, nullable; T = ceil(N / block_q);
+ *                the selected parents in the order importance descending,
+ *                index ascending
+ *   importance   [B][H][T][M0]   fp32, out, nullable; w_p(I) of every parent
+ *
+ * Arithmetic: bf16 inputs use bf16 MFMA with fp32 accumulation (the weights
+ * A and dA and Vbar are rounded to bf16 as MFMA operands; softmax state,
+ * importance and all sums stay fp32); fp32 inputs use fp32 MFMA throughout.
+ */
+avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                               int32_t d, int32_t M0, int32_t Ch, int32_t P,
+                               int32_t block_q, const void* Q, const void* Cp,
+                               const void* Cc, const float* Vbar, const int32_t* counts,
+                               void* Y, int32_t* topp_idx, float* importance,
+                               void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AVQ_H */

@@ -1,0 +1,165 @@
+"""Python binding of ``libavq.so``: argument marshalling only.
+
+Every step of the forward pass runs in the HIP kernels behind the C ABI
+declared in ``include/avq.h``; this module checks tensor shapes, dtypes and
+devices, passes raw device pointers and the current HIP stream, and turns a
+non-OK status into an exception. There is no fallback: if the library is not
+built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+from typing import Optional
+
+import torch
+
+_LIB_PATH = Path(__file__).resolve().parent / "libavq.so"
+_lib = None
+
+AVQ_OK, AVQ_ERR_INVALID_ARG, AVQ_ERR_UNSUPPORTED, AVQ_ERR_DEVICE = 0, 1, 2, 3
+AVQ_F32, AVQ_BF16 = 0, 1
+_DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
+SYMBOLS = ("avq_version", "avq_last_error", "avq_assign", "avq_aggregate", "avq_attention_fwd")
+
+
+class AvqError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+def library_path() -> Path:
+    return _LIB_PATH
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not _LIB_PATH.exists():
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2607_12789_amd.build`")
+        L = ctypes.CDLL(str(_LIB_PATH))
+        i32, vp = ctypes.c_int32, ctypes.c_void_p
+        L.avq_version.restype = ctypes.c_int
+        L.avq_last_error.restype = ctypes.c_char_p
+        L.avq_assign.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.avq_aggregate.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp]
+        L.avq_attention_fwd.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32, i32,
+                                        vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != AVQ_OK:
+        raise AvqError(status, lib().avq_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a tensor on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {t.dtype}: use float32 or bfloat16")
+    return _DTYPES[t.dtype]
+
+
+def assign(K, Cp, Cc, parent_idx=None, code_idx=None, stream=None):
+    """Tree assignment of the keys (``avq_assign``). Returns (parent_idx, code_idx)."""
+    B, H, N, d = K.shape
+    M0, Ch = Cc.shape[1], Cc.shape[2]
+    _dev(K, "K")
+    _dev(Cp, "Cp", K.dtype, (H, M0, d))
+    _dev(Cc, "Cc", K.dtype, (H, M0, Ch, d))
+    if parent_idx is None:
+        parent_idx = torch.empty((B, H, N), dtype=torch.int32, device=K.device)
+    if code_idx is None:
+        code_idx = torch.empty((B, H, N), dtype=torch.int32, device=K.device)
+    _dev(parent_idx, "parent_idx", torch.int32, (B, H, N))
+    _dev(code_idx, "code_idx", torch.int32, (B, H, N))
+    _check(lib().avq_assign(_dtype_code(K), B, H, N, d, M0, Ch, _ptr(K), _ptr(Cp), _ptr(Cc),
+                            _ptr(parent_idx), _ptr(code_idx), _stream(stream)))
+    return parent_idx, code_idx
+
+
+def aggregate(V, code_idx, M0: int, Ch: int, Vbar=None, counts=None, stream=None):
+    """Per-codeword value sums and counts (``avq_aggregate``). Returns (Vbar, counts)."""
+    B, H, N, d = V.shape
+    Mtot = M0 * (1 + Ch)
+    _dev(V, "V")
+    _dev(code_idx, "code_idx", torch.int32, (B, H, N))
+    if Vbar is None:
+        Vbar = torch.empty((B, H, Mtot, d), dtype=torch.float32, device=V.device)
+    if counts is None:
+        counts = torch.empty((B, H, Mtot), dtype=torch.int32, device=V.device)
+    _dev(Vbar, "Vbar", torch.float32, (B, H, Mtot, d))
+    _dev(counts, "counts", torch.int32, (B, H, Mtot))
+    _check(lib().avq_aggregate(_dtype_code(V), B, H, N, d, M0, Ch, _ptr(V), _ptr(code_idx),
+                               _ptr(Vbar), _ptr(counts), _stream(stream)))
+    return Vbar, counts
+
+
+def attention_fwd(Q, Cp, Cc, Vbar, counts, P: int, block_q: int, Y=None, topp_idx=None,
+                  importance=None, debug: bool = False, stream=None):
+    """Refined-codebook attention (``avq_attention_fwd``).
+
+    Returns Y, or (Y, topp_idx, importance) when ``debug`` is set (the two
+    debug outputs are then allocated if not given).
+    """
+    B, H, N, d = Q.shape
+    M0, Ch = Cc.shape[1], Cc.shape[2]
+    Mtot = M0 * (1 + Ch)
+    T = (N + block_q - 1) // block_q if block_q > 0 else 0
+    _dev(Q, "Q")
+    _dev(Cp, "Cp", Q.dtype, (H, M0, d))
+    _dev(Cc, "Cc", Q.dtype, (H, M0, Ch, d))
+    _dev(Vbar, "Vbar", torch.float32, (B, H, Mtot, d))
+    _dev(counts, "counts", torch.int32, (B, H, Mtot))
+    if Y is None:
+        Y = torch.empty_like(Q)
+    _dev(Y, "Y", Q.dtype, Q.shape)
+    if debug:
+        if topp_idx is None:
+            topp_idx = torch.empty((B, H, T, max(P, 0)), dtype=torch.int32, device=Q.device)
+        if importance is None:
+            importance = torch.empty((B, H, T, M0), dtype=torch.float32, device=Q.device)
+    if topp_idx is not None:
+        _dev(topp_idx, "topp_idx", torch.int32, (B, H, T, P))
+    if importance is not None:
+        _dev(importance, "importance", torch.float32, (B, H, T, M0))
+    _check(lib().avq_attention_fwd(_dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(Q),
+                                   _ptr(Cp), _ptr(Cc), _ptr(Vbar), _ptr(counts), _ptr(Y),
+                                   _ptr(topp_idx), _ptr(importance), _stream(stream)))
+    if debug:
+        return Y, topp_idx, importance
+    return Y
+
+
+def forward(Q, K, V, Cp, Cc, P: int, block_q: int, stream=None):
+    """The whole forward pass: assign, aggregate, attention. Returns Y."""
+    M0, Ch = Cc.shape[1], Cc.shape[2]
+    _, code_idx = assign(K, Cp, Cc, stream=stream)
+    Vbar, counts = aggregate(V, code_idx, M0, Ch, stream=stream)
+    return attention_fwd(Q, Cp, Cc, Vbar, counts, P, block_q, stream=stream)

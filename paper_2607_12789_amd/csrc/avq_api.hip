@@ -1,0 +1,146 @@
+// C ABI of the AVQ-Attention forward pass: argument validation on the host,
+// then dispatch to the gfx950 kernels. Nothing here allocates device memory or
+// synchronises; no exception crosses the boundary.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/avq.h"
+#include "avq_common.hpp"
+
+namespace avq {
+template <typename T, int D>
+hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, const void* Cp,
+                         const void* Cc, int32_t* parent_idx, int32_t* code_idx,
+                         hipStream_t stream);
+template <typename T>
+hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
+                            const int32_t* code_idx, float* Vbar, int32_t* counts,
+                            hipStream_t stream);
+template <typename T, int D>
+hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
+                            const void* Q, const void* Cp, const void* Cc, const float* Vbar,
+                            const int32_t* counts, void* Y, int32_t* topp_idx,
+                            float* importance, hipStream_t stream);
+}  // namespace avq
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+avq_status_t fail(avq_status_t st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+avq_status_t ok() {
+  g_err[0] = '\0';
+  return AVQ_OK;
+}
+
+avq_status_t from_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(AVQ_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Shared shape checks. Everything is validated before any HIP call.
+avq_status_t check_common(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                          int32_t M0, int32_t Ch) {
+  if (dtype != AVQ_F32 && dtype != AVQ_BF16)
+    return fail(AVQ_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (B < 1 || H < 1 || N < 1 || d < 1 || M0 < 1 || Ch < 1)
+    return fail(AVQ_ERR_INVALID_ARG, "sizes must be positive (B=%d H=%d N=%d d=%d M0=%d Ch=%d)",
+                B, H, N, d, M0, Ch);
+  if (d != 64 && d != 128) return fail(AVQ_ERR_UNSUPPORTED, "d=%d: only 64 and 128", d);
+  if (Ch != 1 && Ch != 2 && Ch != 4 && Ch != 8 && Ch != 16)
+    return fail(AVQ_ERR_UNSUPPORTED, "Ch=%d: only 1, 2, 4, 8, 16", Ch);
+  if (M0 > 512) return fail(AVQ_ERR_UNSUPPORTED, "M0=%d: at most 512", M0);
+  const long long elems = (long long)B * H * N * d;
+  if (elems >= (1LL << 31))
+    return fail(AVQ_ERR_UNSUPPORTED, "B*H*N*d=%lld: must stay below 2^31", elems);
+  return AVQ_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int avq_version(void) { return 100; }
+
+const char* avq_last_error(void) { return g_err; }
+
+avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                        int32_t M0, int32_t Ch, const void* K, const void* Cp, const void* Cc,
+                        int32_t* parent_idx, int32_t* code_idx, void* stream) {
+  avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
+  if (st != AVQ_OK) return st;
+  if (!K || !Cp || !Cc || !parent_idx || !code_idx)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_assign: null pointer argument");
+  if (!aligned16(K) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(parent_idx) ||
+      !aligned16(code_idx))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_assign: arrays must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int BH = B * H;
+  hipError_t e;
+  if (dtype == AVQ_BF16)
+    e = d == 64 ? avq::launch_assign<avq::bf16, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s)
+                : avq::launch_assign<avq::bf16, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s);
+  else
+    e = d == 64 ? avq::launch_assign<float, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s)
+                : avq::launch_assign<float, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s);
+  return from_hip(e, "avq_assign launch");
+}
+
+avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                           int32_t M0, int32_t Ch, const void* V, const int32_t* code_idx,
+                           float* Vbar, int32_t* counts, void* stream) {
+  avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
+  if (st != AVQ_OK) return st;
+  if (!V || !code_idx || !Vbar || !counts)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_aggregate: null pointer argument");
+  if (!aligned16(V) || !aligned16(code_idx) || !aligned16(Vbar) || !aligned16(counts))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_aggregate: arrays must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int BH = B * H;
+  hipError_t e = dtype == AVQ_BF16
+                     ? avq::launch_aggregate<avq::bf16>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, s)
+                     : avq::launch_aggregate<float>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, s);
+  return from_hip(e, "avq_aggregate launch");
+}
+
+avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                               int32_t M0, int32_t Ch, int32_t P, int32_t block_q,
+                               const void* Q, const void* Cp, const void* Cc,
+                               const float* Vbar, const int32_t* counts, void* Y,
+                               int32_t* topp_idx, float* importance, void* stream) {
+  avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
+  if (st != AVQ_OK) return st;
+  if (P < 0 || P > M0) return fail(AVQ_ERR_INVALID_ARG, "P=%d outside [0, M0=%d]", P, M0);
+  if (block_q < 1) return fail(AVQ_ERR_INVALID_ARG, "block_q=%d must be positive", block_q);
+  if (block_q > 256) return fail(AVQ_ERR_UNSUPPORTED, "block_q=%d: at most 256", block_q);
+  if (!Q || !Cp || !Cc || !Vbar || !counts || !Y)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: null pointer argument");
+  if (!aligned16(Q) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(Vbar) ||
+      !aligned16(counts) || !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: arrays must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int BH = B * H;
+  hipError_t e;
+  if (dtype == AVQ_BF16)
+    e = d == 64 ? avq::launch_attention<avq::bf16, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vbar,
+                                                       counts, Y, topp_idx, importance, s)
+                : avq::launch_attention<avq::bf16, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vbar,
+                                                        counts, Y, topp_idx, importance, s);
+  else
+    e = d == 64 ? avq::launch_attention<float, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vbar,
+                                                   counts, Y, topp_idx, importance, s)
+                : avq::launch_attention<float, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vbar,
+                                                    counts, Y, topp_idx, importance, s);
+  return from_hip(e, "avq_attention_fwd launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,216 @@
+"""GPU-vs-oracle comparison helpers for the parity tests.
+
+Decisions that floating point makes (nearest codeword, top-P membership) are
+compared under a certification rule: a decision is *certified* when the
+oracle's fp64 margin exceeds a bound on the kernel's fp32 rounding error, and
+certified decisions must match bit for bit. An uncertified decision may go
+either way; if the kernel's choice differs from the oracle's it must be a
+valid choice within that bound, and values downstream of it (the aggregates
+of that head, the output rows of that tile) are then left out of the
+element-wise comparison and counted. Everything else is compared element by
+element: integers exactly, floats within the stated tolerance.
+
+Error bounds (u = 2^-24, gamma_n = n u / (1 - n u)):
+* parent distances ||c||^2 - 2 k.c: products of bf16 inputs are exact in
+  fp32 and the sums over d take gamma_d, so the error of one candidate is at
+  most gamma_d (||c||^2 + 2 ||k|| ||c||) + u |value|;
+* child and recomputed parent distances sum (k - c)^2 in fp32: error at most
+  gamma_(d+1) times the distance;
+* importance: the logits carry gamma_d ||q|| ||c||, the weights exp(S - m)
+  twice that plus the exp unit's rounding of (S - m) log2 e, and the
+  normalised sums gamma_(M0 + block_q); w is compared relative to
+  eps_w = 4 gamma_d max||q|| max||c|| + 2 u (max(m - S) + 8) + 2 gamma_(M0 + block_q).
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2607_12789_amd import avq
+
+U = 2.0 ** -24
+TOL_Y = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def gamma(n):
+    return n * U / (1 - n * U)
+
+
+def to_gpu(x: dict) -> dict:
+    return {k: v.cuda() for k, v in x.items()}
+
+
+def gpu_forward(xd: dict, w) -> dict:
+    """Runs the three entry points and returns every output on the CPU."""
+    par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+    Vbar, counts = avq.aggregate(xd["V"], code, w.M0, w.Ch)
+    Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, w.P, w.block_q,
+                                     debug=True)
+    torch.cuda.synchronize()
+    out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, counts=counts, Y=Y, topp=topp,
+               importance=imp)
+    return {k: v.cpu() for k, v in out.items()}
+
+
+class Report(dict):
+    def line(self):
+        return ", ".join(f"{k}={v}" for k, v in self.items())
+
+
+def check_assign(x, w, g, o) -> tuple:
+    """Certified-exact comparison of parent_idx / code_idx. Returns the mask of
+    (b, h) heads whose codes equal the oracle's everywhere, and a report."""
+    K, Cp, Cc = oracle.f64(x["K"]), oracle.f64(x["Cp"]), oracle.f64(x["Cc"])
+    d = w.d
+    knorm = np.linalg.norm(K, axis=-1)
+    cmax = np.linalg.norm(Cp, axis=-1).max(axis=-1)[None, :, None]  # per head
+    err_p = gamma(d) * (cmax ** 2 + 2 * knorm * cmax) + U * (o["d_parent"] + cmax ** 2
+                                                           + 2 * knorm * cmax)
+    par_margin = o["d_parent2"] - o["d_parent"]
+    par_cert = par_margin > 2 * 2 * err_p
+    gp, gc = g["parent_idx"].numpy(), g["code_idx"].numpy()
+    op, oc = o["parent_idx"], o["code_idx"]
+    bad = par_cert & (gp != op)
+    assert not bad.any(), f"{bad.sum()} certified parent decisions differ, e.g. at {np.argwhere(bad)[:5]}"
+
+    err_c = 2 * gamma(d + 1) * (o["d_child"] + o["d_parent"]) + 1e-30
+    move_cert = np.abs(o["d_child"] - o["d_parent"]) > 2 * err_c
+    child_cert = (o["d_child2"] - o["d_child"]) > 2 * 2 * gamma(d + 1) * o["d_child2"]
+    code_cert = par_cert & move_cert & (child_cert | (oc < w.M0))
+    bad = code_cert & (gc != oc)
+    assert not bad.any(), f"{bad.sum()} certified code decisions differ, e.g. at {np.argwhere(bad)[:5]}"
+
+    # Uncertified differences must be valid choices within the bound.
+    diff = (gc != oc) | (gp != op)
+    for b, h, j in np.argwhere(diff):
+        k = K[b, h, j]
+        dp = ((Cp[h] - k) ** 2).sum(-1)
+        assert dp[gp[b, h, j]] <= dp.min() + 4 * err_p[b, h, j], "invalid parent choice"
+        p = gp[b, h, j]
+        dc = ((Cc[h, p] - k) ** 2).sum(-1)
+        dpar = dp[p]
+        if gc[b, h, j] >= w.M0:
+            cc = gc[b, h, j] - w.M0
+            assert cc // w.Ch == p
+            assert dc[cc % w.Ch] <= min(dc.min(), dpar) + 4 * gamma(d + 1) * (dpar + dc.max())
+        else:
+            assert gc[b, h, j] == p
+            assert dpar <= dc.min() + 4 * gamma(d + 1) * (dpar + dc.max())
+    clean = ~diff.any(axis=-1)
+    rep = Report(keys=int(diff.size), uncertified=int((~code_cert).sum()),
+                 differing=int(diff.sum()), heads_excluded=int((~clean).sum()),
+                 moved_frac=round(float((oc >= w.M0).mean()), 4))
+    return clean, rep
+
+
+def check_aggregate(x, w, g, o, clean) -> Report:
+    """Counts exact; Vbar within the fp32 summation bound, on clean heads."""
+    gn, gV = g["counts"].numpy(), g["Vbar"].numpy()
+    on, oV = o["counts"], o["Vbar"]
+    np.testing.assert_array_equal(gn[clean], on[clean])
+    # |fl(sum) - sum| <= gamma_(n-1) sum |v| for each element; |V| aggregated by the oracle
+    absV, _ = oracle.aggregate(np.abs(oracle.f64(x["V"])), o["parent_idx"], o["code_idx"], w.M0,
+                               w.Ch)
+    tol = gamma(np.maximum(on, 1))[..., None] * absV + 1e-30
+    err = np.abs(gV.astype(np.float64) - oV)
+    assert (err[clean] <= tol[clean]).all(), f"Vbar error {err[clean].max()} above bound"
+    assert (gn[..., :w.M0].sum(-1) == w.N).all()
+    return Report(max_vbar_err=float(err[clean].max()) if clean.any() else 0.0)
+
+
+def importance_eps(x, w, o) -> float:
+    Q, Cp = oracle.f64(x["Q"]), oracle.f64(x["Cp"])
+    qmax = np.linalg.norm(Q, axis=-1).max()
+    cmax = np.linalg.norm(Cp, axis=-1).max()
+    S = np.einsum("bhnd,hmd->bhnm", Q[:, :, :64], Cp)
+    spread = float((S.max(-1) - S.min(-1)).max()) * 1.5
+    return 4 * gamma(w.d) * qmax * cmax + 2 * U * (spread + 8) + 2 * gamma(w.M0 + w.block_q)
+
+
+def check_topp(x, w, g, o, clean, tile_mask) -> tuple:
+    """Importance within eps_w; top-P sets certified-exact. Returns the mask of
+    tiles whose selection equals the oracle's (and whose head is clean)."""
+    eps = importance_eps(x, w, o)
+    T = w.n_tiles
+    sel_ok = np.zeros((w.B, w.H, T), bool)
+    gw, ow = g["importance"].numpy().astype(np.float64), o["importance"]
+    gt, ot = g["topp"].numpy(), o["selection"]
+    rep = Report(tiles=0, uncertified=0, differing=0, eps_w=float(f"{eps:.3g}"))
+    for b, h, t in np.argwhere(tile_mask & clean[..., None]):
+        rep["tiles"] += 1
+        wt, gwt = ow[b, h, t], gw[b, h, t]
+        scale = wt.sum()  # = tile size
+        assert np.all(np.abs(gwt - wt) <= eps * wt + 1e-6 * eps * scale), (
+            f"importance off at tile {(b, h, t)}: max rel {np.max(np.abs(gwt - wt) / np.maximum(wt, 1e-30))}")
+        empty = o["counts"][b, h, :w.M0] == 0
+        assert (gwt[empty] == 0).all(), "empty parents must have exactly zero importance"
+        if w.P == 0:
+            sel_ok[b, h, t] = True
+            continue
+        order = np.lexsort((np.arange(w.M0), -wt))
+        srt = wt[order]
+        gs, os_ = set(gt[b, h, t].tolist()), set(ot[b, h, t].tolist())
+        assert len(gs) == w.P, "selection has repeated parents"
+        wP = srt[w.P - 1]
+        wnext = srt[w.P] if w.P < w.M0 else -np.inf
+        certified = (wP - wnext) > 2 * eps * wP + 2e-6 * eps * scale or w.P == w.M0
+        if not certified:
+            rep["uncertified"] += 1
+        if gs == os_:
+            sel_ok[b, h, t] = True
+            # order within the set: (w desc, index asc) where the gaps are certified
+            continue
+        assert not certified, f"certified top-P set differs at tile {(b, h, t)}"
+        rep["differing"] += 1
+        # a valid alternative: nothing left out beats anything taken by more than the bound
+        taken = np.array(sorted(gs))
+        left = np.setdiff1d(np.arange(w.M0), taken)
+        assert wt[taken].min() >= wt[left].max() * (1 - 2 * eps) - 2e-6 * eps * scale, (
+            f"invalid top-P choice at tile {(b, h, t)}")
+    return sel_ok, rep
+
+
+def check_output(x, w, g, o, sel_ok) -> Report:
+    """Per row ||Y - Y*||_inf / ||Y*||_inf within the dtype's tolerance on every
+    row of every compared tile."""
+    tol = TOL_Y[w.dtype]
+    gY = g["Y"].float().numpy().astype(np.float64)
+    oY = o["Y"]
+    rows = np.repeat(sel_ok, w.block_q, axis=-1)[..., :w.N]
+    assert np.isfinite(gY).all(), "non-finite output"
+    num = np.abs(gY - oY).max(-1)
+    den = np.abs(oY).max(-1)
+    rel = np.where(rows, num / np.maximum(den, 1e-30), 0.0)
+    worst = np.unravel_index(np.argmax(rel), rel.shape)
+    assert rel.max() <= tol, f"max row error {rel.max():.3g} > {tol} at {worst}"
+    rel_rows = rel[rows]
+    fro = np.linalg.norm((gY - oY)[rows]) / np.linalg.norm(oY[rows])
+    return Report(rows=int(rows.sum()), max_rel=float(f"{rel.max():.3g}"),
+                  median_rel=float(f"{np.median(rel_rows):.3g}"), frob_rel=float(f"{fro:.3g}"))
+
+
+def compare(x, w, tiles_per_head=None, seed=0, recovered=True) -> dict:
+    """Runs GPU and oracle on the same inputs and checks every output.
+
+    tiles_per_head: number of query tiles per head evaluated by the oracle
+    (None: all). The first and last tile are always included."""
+    T = w.n_tiles
+    mask = np.ones((w.B, w.H, T), np.uint8)
+    if tiles_per_head is not None and tiles_per_head < T:
+        rng = np.random.default_rng(seed)
+        mask[:] = 0
+        for b in range(w.B):
+            for h in range(w.H):
+                pick = rng.choice(T, tiles_per_head, replace=False)
+                mask[b, h, pick] = 1
+                mask[b, h, [0, T - 1]] = 1
+    g = gpu_forward(to_gpu(x), w)
+    o = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], w.P, w.block_q,
+                       recovered=recovered, tile_mask=mask)
+    clean, ra = check_assign(x, w, g, o)
+    rg = check_aggregate(x, w, g, o, clean)
+    sel_ok, rt = check_topp(x, w, g, o, clean, mask.astype(bool))
+    ry = check_output(x, w, g, o, sel_ok & mask.astype(bool) & clean[..., None])
+    assert rt["differing"] <= max(1, 0.01 * rt["tiles"]), "too many differing top-P sets"
+    return dict(assign=ra, aggregate=rg, topp=rt, output=ry, gpu=g, oracle=o)

@@ -1,0 +1,101 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load, export every function that ``include/avq.h``
+declares, and reject invalid arguments on the host before anything is
+launched (these calls pass null device pointers and never reach the GPU).
+"""
+import ctypes
+import re
+from pathlib import Path
+
+import pytest
+
+from paper_2607_12789_amd import avq
+
+ROOT = Path(__file__).resolve().parents[1]
+HEADER = ROOT / "include" / "avq.h"
+OK, INVALID, UNSUPPORTED = avq.AVQ_OK, avq.AVQ_ERR_INVALID_ARG, avq.AVQ_ERR_UNSUPPORTED
+F32, BF16 = avq.AVQ_F32, avq.AVQ_BF16
+
+
+def declared_functions():
+    text = HEADER.read_text()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+[\s\*]+(avq_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not avq.library_path().exists():
+        pytest.fail("libavq.so is not built (python -m paper_2607_12789_amd.build)")
+    return avq.lib()
+
+
+def test_header_declares_the_entry_points():
+    assert declared_functions() == sorted(avq.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    assert L.avq_version() == 100
+
+
+NULL = None
+FAKE = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+
+
+def assign(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 5):
+    return L.avq_assign(dtype, B, H, N, d, M0, Ch, *ptrs, NULL)
+
+
+def aggregate(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 4):
+    return L.avq_aggregate(dtype, B, H, N, d, M0, Ch, *ptrs, NULL)
+
+
+def attn(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,) * 6):
+    return L.avq_attention_fwd(dtype, B, H, N, d, M0, Ch, P, bq, *ptrs, NULL, NULL, NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), INVALID),
+    (dict(B=0), INVALID), (dict(H=-1), INVALID), (dict(N=0), INVALID), (dict(M0=0), INVALID),
+    (dict(Ch=0), INVALID),
+    (dict(d=96), UNSUPPORTED), (dict(d=32), UNSUPPORTED), (dict(Ch=3), UNSUPPORTED),
+    (dict(Ch=32), UNSUPPORTED), (dict(M0=513), UNSUPPORTED),
+    (dict(B=1 << 14, H=1 << 10, N=1 << 10, d=128), UNSUPPORTED),
+])
+def test_shape_validation(L, kw, status):
+    for fn in (assign, aggregate, attn):
+        assert fn(L, **kw) == status, (fn.__name__, kw)
+        assert L.avq_last_error().decode() != ""
+
+
+def test_null_pointers_are_rejected(L):
+    for i in range(5):
+        ptrs = [FAKE] * 5
+        ptrs[i] = NULL
+        assert assign(L, ptrs=ptrs) == INVALID
+    for i in range(4):
+        ptrs = [FAKE] * 4
+        ptrs[i] = NULL
+        assert aggregate(L, ptrs=ptrs) == INVALID
+    for i in range(6):
+        ptrs = [FAKE] * 6
+        ptrs[i] = NULL
+        assert attn(L, ptrs=ptrs) == INVALID
+    assert "null" in L.avq_last_error().decode()
+
+
+@pytest.mark.parametrize("P,bq,status", [(-1, 64, INVALID), (5, 64, INVALID), (1, 0, INVALID),
+                                         (1, 257, UNSUPPORTED)])
+def test_attention_argument_validation(L, P, bq, status):
+    assert attn(L, P=P, bq=bq) == status
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    K = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
+    Cp = torch.zeros(1, 4, 64, dtype=torch.bfloat16)
+    Cc = torch.zeros(1, 4, 2, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        avq.assign(K, Cp, Cc)

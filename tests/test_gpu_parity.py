@@ -1,0 +1,141 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Every case draws seeded inputs, runs avq_assign -> avq_aggregate ->
+avq_attention_fwd on the GPU and the oracle on the CPU, and compares (see
+tests/parity.py): assignments, counts and top-P sets exactly on certified
+decisions, Vbar within the fp32 summation bound, importance within eps_w,
+and Y per row within 1e-4 (fp32) / 2e-2 (bf16) relative to max|Y*|.
+
+The five evaluation workloads run at their full sizes in the same launch
+configuration as the benchmark; for the two largest, the oracle evaluates a
+sample of query tiles per head (plus the first and last), all keys' codes
+and all aggregates.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_12789_amd import inputs
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def banner(name, w):
+    print(f"\n[case] {name}: {w.describe()}", flush=True)
+    sys.stdout.flush()
+
+
+def report(res):
+    for k in ("assign", "aggregate", "topp", "output"):
+        print(f"  {k}: {res[k].line()}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_12789_amd import avq
+    avq.lib()
+
+
+def small(**kw):
+    base = dict(name="edge", B=2, H=3, N=1000, d=64, M0=40, Ch=4, P=5, block_q=128,
+                dtype="bf16", sigma_c=0.1, sigma_k=0.05, q_scale=2.0, seed=1)
+    base.update(kw)
+    return inputs.Workload(**base)
+
+
+EDGE = {
+    "ragged_n": small(),
+    "n_one": small(N=1, B=1, H=1),
+    "n_17_bq16": small(N=17, block_q=16),
+    "p_zero": small(P=0),
+    "p_full": small(P=40),
+    "m0_37_ch16_d128": small(M0=37, Ch=16, d=128, P=7),
+    "ch1": small(Ch=1, P=3),
+    "ch2": small(Ch=2, P=9),
+    "ch8_bq200": small(Ch=8, block_q=200, N=1300, P=11),
+    "keys_stay": small(sigma_k=0.2, Ch=8, P=6),
+    "dirichlet_sparse": small(dirichlet_alpha=0.05, M0=64, Ch=8, P=20, N=2000),
+    "large_logits": small(q_scale=40.0, Ch=8, P=6),
+    "fp32_d128": small(dtype="f32", d=128, Ch=8, P=4, block_q=64),
+    "fp32_ragged": small(dtype="f32", N=777, block_q=100, P=3),
+    "bq1": small(N=50, block_q=1, P=2),
+    "m0_512_bq256": small(M0=512, Ch=8, P=64, block_q=256, N=1536, d=128, B=1, H=2),
+    "m0_300_bq128": small(M0=300, Ch=4, P=30, block_q=128, N=1024, B=1, H=2),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_case(name):
+    w = EDGE[name]
+    banner(name, w)
+    x = inputs.generate(w)
+    res = parity.compare(x, w)
+    report(res)
+
+
+def test_children_equal_parent_gives_vq_attention():
+    """No key may move when the children equal their parent; the refined
+    output then equals P = 0 VQ attention for every P."""
+    w = small(Ch=8, P=6)
+    banner("children_equal_parent", w)
+    x = inputs.generate(w)
+    x["Cc"] = x["Cp"][:, :, None, :].expand(-1, -1, w.Ch, -1).contiguous()
+    res = parity.compare(x, w)
+    report(res)
+    g = res["gpu"]
+    assert (g["code_idx"] < w.M0).all()
+    assert (g["counts"][..., w.M0:] == 0).all()
+    from paper_2607_12789_amd import avq
+    xd = {k: v.cuda() for k, v in x.items()}
+    Vbar, counts = g["Vbar"].cuda(), g["counts"].cuda()
+    y_ref = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, w.P, w.block_q)
+    y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, 0, w.block_q)
+    assert torch.equal(y_ref, y0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_exact_ties_resolve_to_lowest_index(dtype):
+    """Dyadic inputs, exact in every precision: exact distance ties and
+    duplicate codewords must resolve exactly as the oracle does."""
+    w = small(dtype=dtype, M0=12, Ch=4, P=3, N=900)
+    banner(f"exact_ties_{dtype}", w)
+    x = inputs.dyadic_exact(w.B, w.H, w.N, w.d, w.M0, w.Ch, seed=5, dtype=dtype)
+    Cp = x["Cp"].clone()
+    Cp[:, 7] = Cp[:, 2]  # duplicate parent
+    x["Cp"] = Cp
+    Cc = x["Cc"].clone()
+    Cc[:, 4, 3] = Cc[:, 4, 1]  # duplicate child
+    x["Cc"] = Cc
+    res = parity.compare(x, w)
+    report(res)
+    assert res["assign"]["differing"] == 0
+    g = res["gpu"]
+    assert not (g["parent_idx"] == 7).any()
+
+
+def test_repeat_runs_identical_integers():
+    w = small(Ch=8, P=6)
+    x = {k: v.cuda() for k, v in inputs.generate(w).items()}
+    a = parity.gpu_forward(x, w)
+    b = parity.gpu_forward(x, w)
+    for k in ("parent_idx", "code_idx", "counts", "topp"):
+        assert torch.equal(a[k], b[k]), k
+    torch.testing.assert_close(a["Y"], b["Y"], rtol=2e-3, atol=1e-5)
+
+
+SAMPLE = {"c1": None, "c2": None, "c3": None, "c4": 12, "c5": 4}
+
+
+# The five evaluation workloads run last (largest oracle work).
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_workload(name):
+    w = inputs.WORKLOADS[name]
+    banner(name, w)
+    x = inputs.generate(w)
+    res = parity.compare(x, w, tiles_per_head=SAMPLE[name])
+    report(res)
