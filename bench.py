@@ -1,0 +1,179 @@
+"""Throughput of the AVQ-Attention forward pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+One step is the whole forward pass over one batch of synthetic inputs
+already resident in HBM: avq_assign -> avq_aggregate -> avq_attention_fwd.
+The workload is the N = 16384 one (B=2, H=16, d=128, M0=256 parents with 8
+children each, P=32, query block 128, bf16). Prints one JSON line:
+
+* value: query-token*heads per second of the whole step, B*H*N / t_step;
+* roofline: the fused attention kernel (the dominant one) against the bf16
+  MFMA peak, its algorithmic flops 4 d (M0 + P Ch) per query-head divided by
+  its average launch time (HIP events on the launch stream); traffic is the
+  HBM bytes per launch from the committed rocprofv3 counter summary, or null
+  if the kernel source changed since those counters were taken;
+* cpu_baseline: the fp64 oracle timed on the host cores on a bounded sample
+  (a subset of heads of the same workload).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+METRIC = "AVQ attention fwd query-tokens·heads/sec at N=16384; % bf16 MFMA peak"
+UNIT = "query-token*heads/s"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+KERNEL_SRC = ROOT / "paper_2607_12789_amd" / "csrc" / "avq_attention.hip"
+TRAFFIC_SUMMARY = ROOT / "profiles" / "attention_fwd_c4_traffic.md"
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("avq_attention.hip", "avq_common.hpp"):
+        h.update((KERNEL_SRC.parent / name).read_bytes())
+    return h.hexdigest()[:16]
+
+
+def read_traffic():
+    """HBM bytes per launch of the attention kernel from the committed counter
+    summary, if it was taken on the current kernel source."""
+    if not TRAFFIC_SUMMARY.exists():
+        return None
+    text = TRAFFIC_SUMMARY.read_text()
+    m_hash = re.search(r"kernel source hash:\s*`?([0-9a-f]+)`?", text)
+    m_bytes = re.search(r"HBM bytes per launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(x, w, heads: int):
+    import numpy as np
+    import oracle
+    sub = {k: (v[:1, :heads] if k in ("Q", "K", "V") else v[:heads]) for k, v in x.items()}
+    # the codebook is per head: the sample takes heads 0..heads-1 of batch 0
+    t0 = time.perf_counter()
+    oracle.forward(sub["Q"], sub["K"], sub["V"], sub["Cp"], sub["Cc"], w.P, w.block_q)
+    dt = time.perf_counter() - t0
+    return {"value": heads * w.N / dt, "unit": UNIT, "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"batch 0, heads 0-{heads - 1} of the workload ({heads * w.N} queries and "
+                      f"keys, every step of the forward pass) in {dt:.2f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--cpu-heads", type=int, default=8,
+                    help="heads of the workload the oracle baseline runs on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also launch one plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_12789_amd import avq, inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = inputs.WORKLOADS[args.workload]
+    x = inputs.generate(w)
+    dev = torch.device("cuda:0")
+    xd = {k: v.to(dev) for k, v in x.items()}
+    B, H, N, d, M0, Ch, P = w.B, w.H, w.N, w.d, w.M0, w.Ch, w.P
+    par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
+    code = torch.empty_like(par)
+    Vbar = torch.empty((B, H, w.Mtot, d), dtype=torch.float32, device=dev)
+    counts = torch.empty((B, H, w.Mtot), dtype=torch.int32, device=dev)
+    Y = torch.empty_like(xd["Q"])
+
+    def step():
+        avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code)
+        avq.aggregate(xd["V"], code, M0, Ch, Vbar, counts)
+        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, P, w.block_q, Y=Y)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+
+    # per-kernel average launch time, HIP events on the launch stream
+    def timed(fn, reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+        e.synchronize()
+        return s.elapsed_time(e) / reps
+
+    reps = max(args.steps, 1)
+    t_assign = timed(lambda: avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code), reps)
+    t_agg = timed(lambda: avq.aggregate(xd["V"], code, M0, Ch, Vbar, counts), reps)
+    t_attn = timed(lambda: avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, P,
+                                             w.block_q, Y=Y), reps)
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
+    qh = B * H * N
+    flops_attn = 4.0 * d * (M0 + P * Ch) * qh
+    achieved = flops_attn / (t_attn * 1e-3) / 1e12
+    traffic = read_traffic()
+    line = {
+        "metric": METRIC,
+        "value": qh / (ms_per_step * 1e-3),
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.describe()}", "B": B, "H": H, "N": N, "d": d,
+                   "M0": M0, "Ch": Ch, "P": P, "block_q": w.block_q},
+        "kernels_ms": {"assign": t_assign, "aggregate": t_agg, "attention_fwd": t_attn},
+        "roofline": {"kernel": "avq_attention_fwd", "bound": "mfma", "achieved": achieved,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+                     "flops_per_launch": flops_attn},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(x, w, min(args.cpu_heads, H))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
