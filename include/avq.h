@@ -36,7 +36,7 @@
  *     rejected). avq_last_error() then returns a message for the calling
  *     thread. Non-finite inputs are not checked; they propagate.
  *   - Supported: d in {64, 128}; Ch in {1, 2, 4, 8, 16}; 1 <= M0 <= 512;
- *     N >= 1, B >= 1, H >= 1 and B*H*N*d < 2^31. Other shapes return
+ *     1 <= N <= 2^24, B >= 1, H >= 1 and B*H*N*d < 2^31. Other shapes return
  *     AVQ_ERR_UNSUPPORTED.
  */
 #ifndef AVQ_H

@@ -2,102 +2,280 @@
 // convention that a parent row covers its whole cell and a child row the keys
 // that moved to it.
 //
-// One workgroup owns one (batch, head) and a slice of DS value columns. Its
-// fp32 table for all Mtot codes x DS columns lives in LDS, so every atomic add
-// stays on-chip; the table is written to HBM once, each row a contiguous
-// DS-float segment. The workgroup holding slice 0 also counts keys per code
-// in an LDS int table. DS is the widest power of two that divides d and lets
-// both tables fit the 160 KB of LDS of a gfx950 CU.
+// One workgroup owns one (batch, head) and a range of up to 32 parent
+// families (a family = parent p and its Ch children); each quarter wave (16
+// lanes) owns one family and is the only writer of its rows, so no float
+// atomics are needed (LDS float atomics serialise on gfx950; integer ones do
+// not). The workgroup
+//   1. scans the codes of every key of the head (the next round's codes are
+//      prefetched while the current one is queued) and appends the keys whose
+//      parent is in its range to an LDS queue, in key order (wave ballot +
+//      prefix counts);
+//   2. when the queue is full or the codes are exhausted, buckets the queued
+//      keys by their row (stay row of the parent, or one of its children) with
+//      integer LDS atomics: histogram, prefix sum, scatter;
+//   3. lets each quarter wave walk the rows of its family, summing the value
+//      rows of each row's keys in fp32 registers (lane l holds columns
+//      l*CPL .. l*CPL+CPL-1 of the row, up to 16 keys' rows in flight),
+//      and adding every finished row sum into the family's register table.
+// At the end the parent row is the stay row plus the children (the whole
+// cell), every row is written once, and counts come from the histograms.
 #include "avq_common.hpp"
 
 namespace avq {
 
 constexpr int kAggThreads = 512;
-constexpr int kLdsBytes = 160 * 1024;
+constexpr int kAggWaves = kAggThreads / kWave;
+constexpr int kQuarters = kAggThreads / 16;        // families per workgroup at most
+constexpr int kCodesPerThread = 4;                 // codes scanned per thread per round
+constexpr int kRound = kAggThreads * kCodesPerThread;
+constexpr int kQueueCap = 8192;                    // queued keys per flush
+constexpr int kMaxRows = kQuarters * 17;           // families x (1 + Ch), Ch <= 16
+constexpr int kInFlight = 16;                      // value rows loaded ahead per quarter wave (max)
+constexpr int kChMax = 16;
 
-template <typename T>
+struct AggLds {
+  int qkey[kQueueCap];       // queued keys, key order
+  uint16_t qrow[kQueueCap];  // their family-local row
+  int skey[kQueueCap];       // keys bucketed by row
+  int hist[kMaxRows];        // keys per row in this flush
+  int start[kMaxRows + 1];   // bucket starts
+  int cursor[kMaxRows];      // scatter cursors
+  int total[kMaxRows];       // keys per row over all flushes (the counts)
+  int wave_count[kCodesPerThread][kAggWaves];
+};
+
+template <typename T, int D>
 __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restrict__ V,
                                                                 const int32_t* __restrict__ code_idx,
                                                                 float* __restrict__ Vbar,
                                                                 int32_t* __restrict__ counts,
-                                                                int N, int d, int M0, int Ch,
-                                                                int DS, int n_slices) {
-  extern __shared__ __attribute__((aligned(16))) float lds[];
+                                                                int N, int M0, int Ch, int F,
+                                                                int ranges) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
+  AggLds& L = *reinterpret_cast<AggLds*>(lds_raw);
+  constexpr int CPL = D / 16;                      // columns per lane (16 lanes per row)
+  constexpr int VEC = 8 / sizeof(T);               // elements per 8-byte chunk
+  constexpr int LPL = CPL / VEC;                   // 8-byte chunks per lane per row
+  constexpr int INF = 256 / (CPL * sizeof(T)) < kInFlight ? 256 / (CPL * sizeof(T)) : kInFlight;
+  static_assert(LPL >= 1 && CPL % 4 == 0, "lane slice is whole 8-byte chunks and float4s");
+
   const int Mtot = M0 * (1 + Ch);
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int bh = blk / n_slices, slice = blk % n_slices;
-  const bool do_counts = (slice == 0);
-  float* table = lds;                                         // [Mtot][DS]
-  int* cnt = reinterpret_cast<int*>(lds + (size_t)Mtot * DS);  // [Mtot]
+  const int bh = blk / ranges;
+  const int p0 = (blk % ranges) * F;
+  const int nfam = min(F, M0 - p0);
+  const int rows = nfam * (1 + Ch);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int sub = lane % 16, quarter = tid / 16;
 
-  for (int i = threadIdx.x; i < Mtot * DS; i += blockDim.x) table[i] = 0.f;
-  if (do_counts)
-    for (int i = threadIdx.x; i < Mtot; i += blockDim.x) cnt[i] = 0;
-  __syncthreads();
+  for (int r = tid; r < kMaxRows; r += kAggThreads) L.total[r] = 0;
 
-  const int e = threadIdx.x % DS;
-  const int keys_per_iter = blockDim.x / DS;
-  const T* vbase = V + (size_t)bh * N * d + (size_t)slice * DS + e;
-  const int32_t* cbase = code_idx + (size_t)bh * N;
-  for (int j = threadIdx.x / DS; j < N; j += keys_per_iter) {
-    const int code = cbase[j];
-    if (code < 0 || code >= Mtot) continue;  // not a code avq_assign writes
-    const int p = code < M0 ? code : (code - M0) / Ch;
-    const float v = to_f32(vbase[(size_t)j * d]);
-    atomicAdd(&table[p * DS + e], v);
-    if (code >= M0) atomicAdd(&table[code * DS + e], v);
-    if (do_counts && e == 0) {
-      atomicAdd(&cnt[p], 1);
-      if (code >= M0) atomicAdd(&cnt[code], 1);
+  const int32_t* codes = code_idx + (size_t)bh * N;
+  const T* vhead = V + (size_t)bh * N * D;
+
+  // the family table of this quarter wave: row 0 = stay, row 1 + c = child c
+  float acc[1 + kChMax][CPL];
+#pragma unroll
+  for (int r = 0; r <= kChMax; ++r)
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) acc[r][i] = 0.f;
+
+  // 1. scan the head's codes and queue the keys of this range; bucket and
+  //    sum the queue when it would overflow and once the codes are exhausted
+  int qlen = 0;
+  int next[kCodesPerThread];
+#pragma unroll
+  for (int k = 0; k < kCodesPerThread; ++k) {
+    const int j = k * kAggThreads + tid;
+    next[k] = j < N ? codes[j] : -1;
+  }
+  for (int base = 0;; base += kRound) {
+    const bool done = base >= N;
+    int row[kCodesPerThread];
+    unsigned long long mask[kCodesPerThread];
+    int round_total = 0;
+    if (!done) {
+#pragma unroll
+      for (int k = 0; k < kCodesPerThread; ++k) {
+        const int code = next[k];
+        row[k] = -1;
+        if (code >= 0 && code < Mtot) {
+          const int p = code < M0 ? code : (code - M0) / Ch;
+          if (p >= p0 && p < p0 + nfam)
+            row[k] = (p - p0) * (1 + Ch) + (code < M0 ? 0 : 1 + (code - M0) % Ch);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kCodesPerThread; ++k) {  // prefetch the next round
+        const int j = base + kRound + k * kAggThreads + tid;
+        next[k] = j < N ? codes[j] : -1;
+      }
+#pragma unroll
+      for (int k = 0; k < kCodesPerThread; ++k) {
+        mask[k] = __ballot(row[k] >= 0);
+        if (lane == 0) L.wave_count[k][wave] = __popcll(mask[k]);
+      }
+      __syncthreads();
+      for (int k = 0; k < kCodesPerThread; ++k)
+        for (int wv = 0; wv < kAggWaves; ++wv) round_total += L.wave_count[k][wv];
     }
+    // uniform across the workgroup
+    const bool flush = done ? qlen > 0 : qlen + round_total > kQueueCap;
+    if (flush) {
+      for (int r = tid; r < rows; r += kAggThreads) L.hist[r] = 0;
+      __syncthreads();
+      for (int e = tid; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
+      __syncthreads();
+      if (wave == 0) {  // exclusive scan of the row histogram
+        int carry = 0;
+        for (int r0 = 0; r0 < rows; r0 += kWave) {
+          const int r = r0 + lane;
+          const int v = r < rows ? L.hist[r] : 0;
+          int incl = v;
+#pragma unroll
+          for (int off = 1; off < kWave; off <<= 1) {
+            const int y = __shfl_up(incl, off, kWave);
+            if (lane >= off) incl += y;
+          }
+          if (r < rows) {
+            L.start[r] = carry + incl - v;
+            L.cursor[r] = carry + incl - v;
+            L.total[r] += v;
+          }
+          carry += __shfl(incl, kWave - 1, kWave);
+        }
+        if (lane == 0) L.start[rows] = carry;
+      }
+      __syncthreads();
+      for (int e = tid; e < qlen; e += kAggThreads)
+        L.skey[atomicAdd(&L.cursor[L.qrow[e]], 1)] = L.qkey[e];
+      __syncthreads();
+      if (quarter < nfam) {
+        const int r_begin = quarter * (1 + Ch);
+        for (int rr = 0; rr <= Ch; ++rr) {
+          const int b = L.start[r_begin + rr], e = L.start[r_begin + rr + 1];
+          if (b == e) continue;
+          float cur[CPL];
+#pragma unroll
+          for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
+          for (int k0 = b; k0 < e; k0 += INF) {
+            uint2 raw[INF][LPL];
+#pragma unroll
+            for (int u = 0; u < INF; ++u) {
+              const int k = k0 + u;
+              const T* vrow = vhead + (size_t)L.skey[k < e ? k : b] * D + sub * CPL;
+#pragma unroll
+              for (int l = 0; l < LPL; ++l) raw[u][l] = reinterpret_cast<const uint2*>(vrow)[l];
+            }
+#pragma unroll
+            for (int u = 0; u < INF; ++u) {
+              if (k0 + u < e) {
+#pragma unroll
+                for (int l = 0; l < LPL; ++l) {
+                  const T* x = reinterpret_cast<const T*>(&raw[u][l]);
+#pragma unroll
+                  for (int v = 0; v < VEC; ++v) cur[l * VEC + v] += to_f32(x[v]);
+                }
+              }
+            }
+          }
+#pragma unroll
+          for (int r = 0; r <= kChMax; ++r)
+            if (r == rr)
+#pragma unroll
+              for (int i = 0; i < CPL; ++i) acc[r][i] += cur[i];
+        }
+      }
+      __syncthreads();
+      qlen = 0;
+    }
+    if (done) break;
+    int offset = qlen;
+#pragma unroll
+    for (int k = 0; k < kCodesPerThread; ++k) {
+      int before = offset, all = 0;
+      for (int wv = 0; wv < kAggWaves; ++wv) {
+        if (wv < wave) before += L.wave_count[k][wv];
+        all += L.wave_count[k][wv];
+      }
+      if (row[k] >= 0) {
+        const int slot = before + __popcll(mask[k] & ((1ull << lane) - 1ull));
+        L.qkey[slot] = base + k * kAggThreads + tid;
+        L.qrow[slot] = (uint16_t)row[k];
+      }
+      offset += all;
+    }
+    qlen = offset;
+    __syncthreads();
+  }
+
+  // 2. parent row = stay + children; write every row once, and the counts
+  if (quarter < nfam) {
+    const int p = p0 + quarter;
+    float* vb = Vbar + (size_t)bh * Mtot * D;
+    float par[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) par[i] = acc[0][i];
+#pragma unroll
+    for (int r = 1; r <= kChMax; ++r) {
+      if (r <= Ch) {
+        float4* dst =
+            reinterpret_cast<float4*>(vb + (size_t)(M0 + p * Ch + (r - 1)) * D + sub * CPL);
+#pragma unroll
+        for (int i = 0; i < CPL; i += 4)
+          dst[i / 4] = float4{acc[r][i], acc[r][i + 1], acc[r][i + 2], acc[r][i + 3]};
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) par[i] += acc[r][i];
+      }
+    }
+    float4* dst = reinterpret_cast<float4*>(vb + (size_t)p * D + sub * CPL);
+#pragma unroll
+    for (int i = 0; i < CPL; i += 4) dst[i / 4] = float4{par[i], par[i + 1], par[i + 2], par[i + 3]};
   }
   __syncthreads();
-
-  float* out = Vbar + (size_t)bh * Mtot * d + (size_t)slice * DS;
-  for (int i = threadIdx.x; i < Mtot * DS; i += blockDim.x) {
-    const int r = i / DS, col = i % DS;
-    out[(size_t)r * d + col] = table[i];
+  int32_t* nb = counts + (size_t)bh * Mtot;
+  for (int f = tid; f < nfam; f += kAggThreads) {
+    const int* tot = &L.total[f * (1 + Ch)];
+    int cell = 0;
+    for (int c = 0; c <= Ch; ++c) cell += tot[c];
+    nb[p0 + f] = cell;
+    for (int c = 0; c < Ch; ++c) nb[M0 + (p0 + f) * Ch + c] = tot[1 + c];
   }
-  if (do_counts)
-    for (int i = threadIdx.x; i < Mtot; i += blockDim.x) counts[(size_t)bh * Mtot + i] = cnt[i];
 }
 
-// Widest d-slice (power of two dividing d, at most 16) whose tables fit in
-// lds_bytes of LDS.
-int aggregate_slice_width(int d, int M0, int Ch, long long lds_bytes) {
-  const long long Mtot = (long long)M0 * (1 + Ch);
-  for (int ds = 16; ds >= 1; ds >>= 1) {
-    if (d % ds != 0) continue;
-    if (Mtot * (ds + 1) * 4 <= lds_bytes) return ds;
-  }
-  return 0;
+template <typename T, int D>
+hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
+                              const int32_t* code_idx, float* Vbar, int32_t* counts,
+                              hipStream_t stream) {
+  DeviceInfo info;
+  hipError_t e = device_info(&info);
+  if (e != hipSuccess) return e;
+  if (Ch > kChMax) return hipErrorInvalidValue;
+  // families per workgroup: one per quarter wave, fewer while that leaves
+  // fewer workgroups than CUs
+  int F = kQuarters < M0 ? kQuarters : M0;
+  while (F > 8 && (long long)BH * ((M0 + F - 1) / F) < info.cus) F /= 2;
+  const int ranges = (M0 + F - 1) / F;
+  const int lds = (int)sizeof(AggLds);
+  e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D>, lds,
+                         (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0));
+  if (e != hipSuccess) return e;
+  const long long grid = (long long)BH * ranges;
+  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((aggregate_kernel<T, D>), dim3((unsigned)grid), dim3(kAggThreads), lds,
+                     stream, static_cast<const T*>(V), code_idx, Vbar, counts, N, M0, Ch, F,
+                     ranges);
+  return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
                             const int32_t* code_idx, float* Vbar, int32_t* counts,
                             hipStream_t stream) {
-  int dev = 0, lds_max = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-  if (e != hipSuccess) return e;
-  if (lds_max > kLdsBytes) lds_max = kLdsBytes;
-  const int DS = aggregate_slice_width(d, M0, Ch, lds_max);
-  if (DS == 0) return hipErrorInvalidValue;
-  const int n_slices = d / DS;
-  const size_t lds = (size_t)M0 * (1 + Ch) * (DS + 1) * sizeof(float);
-  if (lds > 65536) {
-    e = hipFuncSetAttribute((const void*)aggregate_kernel<T>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  const long long grid = (long long)BH * n_slices;
-  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(aggregate_kernel<T>, dim3((unsigned)grid), dim3(kAggThreads), lds, stream,
-                     static_cast<const T*>(V), code_idx, Vbar, counts, N, d, M0, Ch, DS,
-                     n_slices);
-  return hipGetLastError();
+  if (d == 64) return launch_aggregate_d<T, 64>(BH, N, M0, Ch, V, code_idx, Vbar, counts, stream);
+  if (d == 128) return launch_aggregate_d<T, 128>(BH, N, M0, Ch, V, code_idx, Vbar, counts, stream);
+  return hipErrorInvalidValue;
 }
 
 template hipError_t launch_aggregate<bf16>(int, int, int, int, int, const void*, const int32_t*,

@@ -4,6 +4,8 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
+
 #include "../../include/avq.h"
 #include "avq_common.hpp"
 
@@ -21,6 +23,49 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
                             const void* Q, const void* Cp, const void* Cc, const float* Vbar,
                             const int32_t* counts, void* Y, int32_t* topp_idx,
                             float* importance, hipStream_t stream);
+}  // namespace avq
+
+namespace avq {
+
+constexpr int kMaxDevices = 64;
+constexpr int kMaxSlots = 64;
+
+hipError_t device_info(DeviceInfo* out) {
+  static DeviceInfo cache[kMaxDevices];
+  static std::atomic<int> ready[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (ready[dev].load(std::memory_order_acquire) == 0) {
+    DeviceInfo info;
+    e = hipDeviceGetAttribute(&info.lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&info.cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    cache[dev] = info;
+    ready[dev].store(1, std::memory_order_release);
+  }
+  *out = cache[dev];
+  return hipSuccess;
+}
+
+hipError_t ensure_dynamic_lds(const void* kernel, int bytes, int slot) {
+  // largest limit already set for (device, slot)
+  static std::atomic<int> done[kMaxDevices][kMaxSlots];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices || slot < 0 || slot >= kMaxSlots) return hipErrorInvalidValue;
+  if (done[dev][slot].load(std::memory_order_acquire) >= bytes) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return e;
+  int prev = done[dev][slot].load(std::memory_order_relaxed);
+  while (prev < bytes && !done[dev][slot].compare_exchange_weak(prev, bytes)) {
+  }
+  return hipSuccess;
+}
+
 }  // namespace avq
 
 namespace {
@@ -57,6 +102,7 @@ avq_status_t check_common(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, in
   if (Ch != 1 && Ch != 2 && Ch != 4 && Ch != 8 && Ch != 16)
     return fail(AVQ_ERR_UNSUPPORTED, "Ch=%d: only 1, 2, 4, 8, 16", Ch);
   if (M0 > 512) return fail(AVQ_ERR_UNSUPPORTED, "M0=%d: at most 512", M0);
+  if (N > (1 << 24)) return fail(AVQ_ERR_UNSUPPORTED, "N=%d: at most 2^24 keys per head", N);
   const long long elems = (long long)B * H * N * d;
   if (elems >= (1LL << 31))
     return fail(AVQ_ERR_UNSUPPORTED, "B*H*N*d=%lld: must stay below 2^31", elems);

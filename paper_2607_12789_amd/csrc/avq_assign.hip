@@ -15,12 +15,15 @@
 // identical codewords give identical distances.
 //
 // Child compare: the key is compared with the Ch children of its parent and,
-// with the same routine, with the parent itself: sum over d of (k - c)^2 in
-// fp32, each lane group summing its quarter of d, the quarters combined by the
-// same butterfly for every candidate. A key moves to its nearest child only if
-// that distance is strictly below the recomputed parent distance (equal
-// distances keep the parent, and a child identical to its parent never takes
-// a key).
+// with the same routine, with the parent itself, so that a child identical to
+// its parent gives exactly the parent's distance. For bf16 the routine is
+// ||c||^2 - 2 k.c with both dot products taken by packed bf16 dot2
+// instructions (products exact, fp32 accumulation); for fp32 it is the direct
+// sum of (k - c)^2. Each lane group sums its quarter of d and the quarters are
+// combined by the same butterfly for every candidate. A key moves to its
+// nearest child only if that value is strictly below the parent's (equal
+// values keep the parent). Candidates are gathered four at a time so their
+// loads overlap.
 #include "avq_common.hpp"
 
 namespace avq {
@@ -102,13 +105,20 @@ __global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
       *reinterpret_cast<uint4*>(&lc[r * ROW + col]) = val;
     }
     __syncthreads();
-    if (tid < CW) {
+    {
+      // ||c||^2 of every staged row: four threads per row, each summing a
+      // quarter of d in order, combined in a fixed order (identical codewords
+      // give identical norms).
+      static_assert(CW * 4 == 256, "four threads per staged row");
+      const int r = tid / 4, qd = tid % 4;
       float s2 = 0.f;
-      for (int e = 0; e < D; ++e) {
-        const float x = to_f32(lc[tid * ROW + e]);
+      for (int e = qd * (D / 4); e < (qd + 1) * (D / 4); ++e) {
+        const float x = to_f32(lc[r * ROW + e]);
         s2 = fmaf(x, x, s2);
       }
-      lnorm[tid] = (base + tid < M0) ? s2 : __builtin_inff();
+      s2 += shfl_xor(s2, 1);
+      s2 += shfl_xor(s2, 2);
+      if (qd == 0) lnorm[r] = (base + r < M0) ? s2 : __builtin_inff();
     }
     __syncthreads();
 
@@ -163,39 +173,66 @@ __global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
   }
 
   // Child compare (Alg. 1): the parent and its children through one routine.
+  // Candidate 0 is the parent, candidate 1 + c is child c.
+  constexpr int kBatch = 4;
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     const int j = key0 + 16 * s + c;
     const int p = bidx[s];
-    auto sqdist = [&](const T* code) -> float {
-      float part = 0.f;
+    const T* kids = Cc + ((size_t)h * M0 + p) * Ch * D;
+    float dpar = 0.f, dch = __builtin_inff();
+    int cbest = 0;
+    for (int b0 = 0; b0 <= Ch; b0 += kBatch) {
+      Frag cv[kBatch][KQ];
 #pragma unroll
-      for (int kq = 0; kq < KQ; ++kq) {
-        if constexpr (kB) {
-          const bf16x8 cv = *reinterpret_cast<const bf16x8*>(code + 32 * kq + 8 * g);
+      for (int u = 0; u < kBatch; ++u) {
+        const int cand = min(b0 + u, Ch);  // clamped: slots past Ch are ignored
+        const T* code = cand == 0 ? cp_head + (size_t)p * D : kids + (size_t)(cand - 1) * D;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const float diff = to_f32(kf[s][kq][i]) - to_f32(cv[i]);
-            part = fmaf(diff, diff, part);
-          }
-        } else {
-          const float diff = kf[s][kq] - code[4 * kq + g];
-          part = fmaf(diff, diff, part);
+        for (int kq = 0; kq < KQ; ++kq) {
+          if constexpr (kB)
+            cv[u][kq] = *reinterpret_cast<const bf16x8*>(code + 32 * kq + 8 * g);
+          else
+            cv[u][kq] = code[4 * kq + g];
         }
       }
-      part += shfl_xor(part, 16);
-      part += shfl_xor(part, 32);
-      return part;
-    };
-    const float dpar = sqdist(cp_head + (size_t)p * D);
-    const T* kids = Cc + ((size_t)h * M0 + p) * Ch * D;
-    float dch = __builtin_inff();
-    int cbest = 0;
-    for (int ch = 0; ch < Ch; ++ch) {
-      const float dist = sqdist(kids + (size_t)ch * D);
-      if (dist < dch) {
-        dch = dist;
-        cbest = ch;
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        float part;
+        if constexpr (kB) {
+          float dotkc = 0.f, dotcc = 0.f;
+#pragma unroll
+          for (int kq = 0; kq < KQ; ++kq) {
+#pragma unroll
+            for (int i = 0; i < 8; i += 2) {
+              const bf16x2 kk = {kf[s][kq][i], kf[s][kq][i + 1]};
+              const bf16x2 cc = {cv[u][kq][i], cv[u][kq][i + 1]};
+              dotkc = __builtin_amdgcn_fdot2_f32_bf16(kk, cc, dotkc, false);
+              dotcc = __builtin_amdgcn_fdot2_f32_bf16(cc, cc, dotcc, false);
+            }
+          }
+          dotkc += shfl_xor(dotkc, 16);
+          dotkc += shfl_xor(dotkc, 32);
+          dotcc += shfl_xor(dotcc, 16);
+          dotcc += shfl_xor(dotcc, 32);
+          part = fmaf(-2.f, dotkc, dotcc);
+        } else {
+          part = 0.f;
+#pragma unroll
+          for (int kq = 0; kq < KQ; ++kq) {
+            const float diff = kf[s][kq] - cv[u][kq];
+            part = fmaf(diff, diff, part);
+          }
+          part += shfl_xor(part, 16);
+          part += shfl_xor(part, 32);
+        }
+        const int cand = b0 + u;
+        if (cand == 0) {
+          dpar = part;
+        } else if (cand <= Ch && part < dch) {
+          dch = part;
+          cbest = cand - 1;
+        }
       }
     }
     if (g == 0 && j < N) {

@@ -2,33 +2,43 @@
 //
 // One workgroup processes one query tile (block_q consecutive tokens of one
 // (batch, head)); each wave owns 32 query rows. Everything is computed
-// transposed, codewords x queries: S^T = C . Q^T and Xbar^T = Vbar^T . A^T.
-// With the 16x16 MFMA layouts, a lane then owns one query column and four
-// consecutive codeword rows, which gives:
-//   - the A^T tile that comes out of the exp() is already in the register
-//     layout of the MFMA operand of the next product (no shuffles);
+// transposed, codewords x queries: S^T = C . Q^T and Xbar^T = Vmean^T . A^T.
+// With the 16x16 MFMA layouts a lane owns one query column and four
+// consecutive codeword rows, so
+//   - the weights that come out of exp2() are already in the register layout
+//     of the MFMA operand of the next product (no shuffles);
 //   - the Ch children of one parent sit in one lane's consecutive rows (plus
-//     the partner lane group for Ch = 8, 16), so the recovered parent logit of
+//     the partner lane groups for Ch = 8, 16): the recovered parent logit of
 //     Eq. (parent_recovery) is an in-register sum;
-//   - per-query softmax state (running max, denominator) is per lane.
+//   - per-query softmax state is per lane.
+//
+// Log-count bias (App. D): a codeword's logit enters as
+// t = S log2(e) + log2(n), so the weight exp2(t - m) is n exp(S - m'); empty
+// codewords get t = -inf and drop out of the running max and of every sum
+// without masks. The values are staged as means Vbar/n, which gives
+// sum_j n_j exp(S_j - m') Vbar_j / n_j = sum_j exp(S_j - m') Vbar_j, the
+// numerator of Eq. (vqflashattention). The parent logit recovered from the
+// children uses the unbiased child logits, and the correcting weight of
+// child c is n_c (exp(T_c - m') - exp(Srec - m')), Eq. (correcting_attention)
+// times n_c. The denominator (sum of the weights, n folded in) is produced by
+// the value MFMA itself through one extra d-tile whose first row is all ones,
+// so numerator and denominator use the same rounded weights; the parent-only
+// denominator needed by Eq. (importance) is also summed in fp32.
 //
 // Phases per tile:
 //   1. parent pass over the M0 parents in groups of 16*NT codewords held in
-//      registers: logits, masked running max (App. D), A = exp(S - m) zeroed
-//      for empty parents, Zbar += A n, Xbar += Vbar^T A (Eq. (vqflashattention));
-//   2. importance w_p = n_p sum_i A_ip / Zbar_i (Eq. (importance)) from the
-//      final denominators: straight from the registers when all parents fit in
-//      one group, otherwise from a second sweep that recomputes the logits;
-//   3. top-P: every parent's rank under (w desc, index asc) by counting, in
-//      LDS; parents of rank < P are selected;
-//   4. child pass over the P*Ch gathered children in chunks of 64 rows:
-//      logits, running max raised over non-empty children with Xbar/Zbar
-//      rescaled, recovered parent logit, correcting weights
-//      dA = exp(T - m) - exp(Srec - m) zeroed for empty children
-//      (Eq. (correcting_attention)), Zbar += dA n, Xbar += Vbar^T dA;
-//   5. Y = Xbar / Zbar.
-// Codeword rows and (transposed) aggregated values are staged through LDS in
-// chunks shared by all waves of the workgroup.
+//      registers: logits, running max, weights, Xbar += Vmean^T W;
+//   2. importance w_p = sum_i W_ip / Z_i with the final parent denominators
+//      (Eq. (importance), n_p already inside W): straight from the registers
+//      when all parents fit in one group, else from a second sweep that
+//      recomputes the logits;
+//   3. top-P: histogram of the importance exponents finds the bin holding the
+//      P-th largest value; exact ranks (w desc, index asc) inside that bin
+//      decide the rest; the selected parents are listed in index order;
+//   4. child pass over the selected parents' children in chunks: logits,
+//      running max raised (Xbar rescaled), recovered parent logit, correcting
+//      weights, Xbar += Vmean^T dW;
+//   5. Y = Xbar / Z.
 #include "avq_common.hpp"
 
 namespace avq {
@@ -38,16 +48,32 @@ struct AttnCfg {
   static constexpr bool kB = Elem<T>::kBf16;
   static constexpr int RPW = 32;                  // query rows per wave
   static constexpr int QS = RPW / 16;             // query subtiles per wave
-  static constexpr int CW = kB ? 64 : 32;         // codeword rows per LDS chunk
+  static constexpr int GROUP = 16 * NT;           // parents held in registers
+  static constexpr int CW = kB ? GROUP : 32;      // codeword rows per LDS chunk
   static constexpr int KQ = kB ? D / 32 : D / 4;  // MFMA k-steps over d
   static constexpr int DT = D / 16;               // d tiles of Xbar
+  static constexpr int XT = DT + 1;               // plus the denominator tile
   static constexpr int CPAD = kB ? 8 : 4;         // 16 bytes of row padding
   static constexpr int CROW = D + CPAD;
   static constexpr int VPAD = kB ? 8 : 4;
   static constexpr int VROW = CW + VPAD;
   static constexpr int M0MAX = 512;
-  static constexpr int GROUP = 16 * NT;           // parents held in registers
   static_assert(GROUP % CW == 0, "a register group is a whole number of LDS chunks");
+  using VT = typename std::conditional<kB, bf16, float>::type;
+  // dynamic LDS layout (bytes)
+  static constexpr size_t OFF_C = 0;                                      // [CW][CROW] T
+  static constexpr size_t OFF_V = OFF_C + (size_t)CW * CROW * sizeof(T);   // [D][VROW] VT
+  static constexpr size_t OFF_N = OFF_V + (size_t)D * VROW * sizeof(VT);   // [CW] f32 n
+  static constexpr size_t OFF_L = OFF_N + (size_t)CW * 4;                  // [CW] f32 log2 n
+  static constexpr size_t OFF_LP = OFF_L + (size_t)CW * 4;                 // [M0MAX] parents' log2 n
+  static constexpr size_t OFF_W = OFF_LP + (size_t)M0MAX * 4;              // [MAXW][M0MAX] f32
+  static constexpr size_t OFF_WF = OFF_W + (size_t)MAXW * M0MAX * 4;       // [M0MAX] f32
+  static constexpr size_t OFF_SEL = OFF_WF + (size_t)M0MAX * 4;            // [M0MAX] i32
+  static constexpr size_t OFF_FLAG = OFF_SEL + (size_t)M0MAX * 4;          // [M0MAX] i32
+  static constexpr size_t OFF_HIST = OFF_FLAG + (size_t)M0MAX * 4;         // [256] i32
+  static constexpr size_t OFF_MISC = OFF_HIST + 256 * 4;                   // [4] i32
+  static constexpr size_t LDS_BYTES = OFF_MISC + 16;
+  static_assert(OFF_V % 16 == 0 && OFF_N % 16 == 0 && OFF_W % 16 == 0, "aligned LDS regions");
 };
 
 struct AttnArgs {
@@ -66,18 +92,24 @@ template <typename T, int D, int NT, int MAXW>
 __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
   using Cfg = AttnCfg<T, D, NT, MAXW>;
   constexpr bool kB = Cfg::kB;
-  constexpr int QS = Cfg::QS, CW = Cfg::CW, KQ = Cfg::KQ, DT = Cfg::DT;
+  constexpr int QS = Cfg::QS, CW = Cfg::CW, KQ = Cfg::KQ, DT = Cfg::DT, XT = Cfg::XT;
   constexpr int CROW = Cfg::CROW, VROW = Cfg::VROW, M0MAX = Cfg::M0MAX;
   using QFrag = typename std::conditional<kB, bf16x8, float>::type;
-  using VT = typename std::conditional<kB, bf16, float>::type;
+  using VT = typename Cfg::VT;
+  constexpr float kNegInf = -__builtin_inff();
 
-  __shared__ __attribute__((aligned(16))) T lc[CW * CROW];   // codeword rows
-  __shared__ __attribute__((aligned(16))) VT lv[D * VROW];   // Vbar^T of those rows
-  __shared__ float ln[CW];                                   // their counts
-  __shared__ float lnp[M0MAX];                                     // parent counts
-  __shared__ __attribute__((aligned(16))) float lw[MAXW * M0MAX];  // per-wave importance
-  __shared__ __attribute__((aligned(16))) float lwf[M0MAX];        // importance
-  __shared__ int lsel[M0MAX];                                      // selected parents
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
+  T* lc = reinterpret_cast<T*>(lds_raw + Cfg::OFF_C);          // staged codeword rows
+  VT* lv = reinterpret_cast<VT*>(lds_raw + Cfg::OFF_V);        // their mean values, transposed
+  float* ln = reinterpret_cast<float*>(lds_raw + Cfg::OFF_N);  // their counts
+  float* ll = reinterpret_cast<float*>(lds_raw + Cfg::OFF_L);  // log2 of their counts
+  float* lp = reinterpret_cast<float*>(lds_raw + Cfg::OFF_LP);   // log2 n of all parents
+  float* lw = reinterpret_cast<float*>(lds_raw + Cfg::OFF_W);    // per-wave importance
+  float* lwf = reinterpret_cast<float*>(lds_raw + Cfg::OFF_WF);  // importance
+  int* lsel = reinterpret_cast<int*>(lds_raw + Cfg::OFF_SEL);    // selected, index order
+  int* lflag = reinterpret_cast<int*>(lds_raw + Cfg::OFF_FLAG);  // selected flags
+  int* lhist = reinterpret_cast<int*>(lds_raw + Cfg::OFF_HIST);  // exponent histogram
+  int* lmisc = reinterpret_cast<int*>(lds_raw + Cfg::OFF_MISC);
 
   const T* __restrict__ Q = static_cast<const T*>(args.Q);
   const T* __restrict__ Cp = static_cast<const T*>(args.Cp);
@@ -117,7 +149,7 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
     }
   }
 
-  // ---- LDS staging of a chunk of CW codeword rows -----------------------------
+  // ---- LDS staging of a chunk of CW codeword rows ---------------------------
   // stage_codes: row r of the chunk <- codebook row crow(r) (nullptr: zeros).
   auto stage_codes = [&](auto crow) {
     constexpr int VEC = 16 / sizeof(T);
@@ -130,13 +162,15 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
       *reinterpret_cast<uint4*>(&lc[r * CROW + col]) = val;
     }
   };
-  // stage_values: Vbar^T and counts of aggregate rows vrow(r) (-1: zeros).
+  // stage_values: mean values Vbar/n (transposed), n and log2 n of aggregate
+  // rows vrow(r) (-1: an empty row).
+  const float* vb = Vbar + (size_t)bh * Mtot * D;
+  const int32_t* cb = counts + (size_t)bh * Mtot;
   auto stage_values = [&](auto vrow) {
-    const float* vb = Vbar + (size_t)bh * Mtot * D;
     if constexpr (kB) {
-      // Vbar^T in bf16, codewords of each 32-block permuted so that lane
-      // group g reads its 8 MFMA k-slots {4g..4g+3, 16+4g..16+4g+3} as one
-      // 16-byte word: position 8g' + i holds codeword perm(g', i).
+      // bf16, codewords of each 32-block permuted so that lane group g reads
+      // its 8 MFMA k-slots {4g..4g+3, 16+4g..16+4g+3} as one 16-byte word:
+      // position 8g' + i holds codeword perm(g', i).
       for (int v = tid; v < (CW / 32) * 4 * (D / 4); v += nthr) {
         const int dq = v % (D / 4), gg = (v / (D / 4)) % 4, blk = v / (D / 4) / 4;
         float4 x[8];
@@ -144,8 +178,13 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
         for (int i = 0; i < 8; ++i) {
           const int r = 32 * blk + (i < 4 ? 4 * gg + i : 16 + 4 * gg + (i - 4));
           const int a = vrow(r);
-          x[i] = (a >= 0) ? *reinterpret_cast<const float4*>(vb + (size_t)a * D + 4 * dq)
-                          : float4{0.f, 0.f, 0.f, 0.f};
+          const int n = a >= 0 ? cb[a] : 0;
+          x[i] = float4{0.f, 0.f, 0.f, 0.f};
+          if (n > 0) {
+            const float inv = 1.f / (float)n;
+            const float4 y = *reinterpret_cast<const float4*>(vb + (size_t)a * D + 4 * dq);
+            x[i] = float4{y.x * inv, y.y * inv, y.z * inv, y.w * inv};
+          }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -156,15 +195,20 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
         }
       }
     } else {
-      // Vbar^T in fp32, natural codeword order, written as 4x4 transposes.
+      // fp32, natural codeword order, written as 4x4 transposes.
       for (int v = tid; v < (CW / 4) * (D / 4); v += nthr) {
         const int dq = v % (D / 4), rq = v / (D / 4);
         float4 x[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int a = vrow(4 * rq + i);
-          x[i] = (a >= 0) ? *reinterpret_cast<const float4*>(vb + (size_t)a * D + 4 * dq)
-                          : float4{0.f, 0.f, 0.f, 0.f};
+          const int n = a >= 0 ? cb[a] : 0;
+          x[i] = float4{0.f, 0.f, 0.f, 0.f};
+          if (n > 0) {
+            const float inv = 1.f / (float)n;
+            const float4 y = *reinterpret_cast<const float4*>(vb + (size_t)a * D + 4 * dq);
+            x[i] = float4{y.x * inv, y.y * inv, y.z * inv, y.w * inv};
+          }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -173,10 +217,11 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
         }
       }
     }
-    const int32_t* cb = counts + (size_t)bh * Mtot;
     for (int r = tid; r < CW; r += nthr) {
       const int a = vrow(r);
-      ln[r] = (a >= 0) ? (float)cb[a] : 0.f;
+      const float n = a >= 0 ? (float)cb[a] : 0.f;
+      ln[r] = n;
+      ll[r] = n > 0.f ? log2_hw(n) : kNegInf;
     }
   };
 
@@ -199,68 +244,92 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
     }
   };
 
-  // ---- Xbar^T += Vbar^T . W^T for chunk tiles (tt, tt+1) (bf16) or tt (fp32) --
-  f32x4 X[DT][QS];
+  // ---- Xbar^T += Vmean^T . W^T for chunk tiles (tt, tt+1) (bf16) or tt (fp32);
+  // the extra tile DT has an all-ones first row and accumulates sum W.
+  f32x4 X[XT][QS];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
+  for (int dt = 0; dt < XT; ++dt)
 #pragma unroll
     for (int s = 0; s < QS; ++s) X[dt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto accumulate = [&](int tt, const f32x4 (&w0)[QS], const f32x4 (&w1)[QS]) {
-    if constexpr (kB) {
-      bf16x8 b[QS];
+  // bf16: pack the weights of tiles (tt, tt+1) into the MFMA B operand.
+  auto pack = [&](const f32x4 (&w0)[QS], const f32x4 (&w1)[QS], bf16x8 (&b)[QS]) {
 #pragma unroll
-      for (int s = 0; s < QS; ++s) {
+    for (int s = 0; s < QS; ++s) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          b[s][r] = (bf16)w0[s][r];
-          b[s][4 + r] = (bf16)w1[s][r];
-        }
-      }
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(&lv[(16 * dt + c) * VROW + 16 * tt + 8 * g]);
-#pragma unroll
-        for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(a, b[s], X[dt][s]);
-      }
-    } else {
-      (void)w1;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const float4 a = *reinterpret_cast<const float4*>(&lv[(16 * dt + c) * VROW + 16 * tt + 4 * g]);
-#pragma unroll
-        for (int s = 0; s < QS; ++s) {
-          X[dt][s] = mfma_f32(a.x, w0[s][0], X[dt][s]);
-          X[dt][s] = mfma_f32(a.y, w0[s][1], X[dt][s]);
-          X[dt][s] = mfma_f32(a.z, w0[s][2], X[dt][s]);
-          X[dt][s] = mfma_f32(a.w, w0[s][3], X[dt][s]);
-        }
+      for (int r = 0; r < 4; ++r) {
+        b[s][r] = (bf16)w0[s][r];
+        b[s][4 + r] = (bf16)w1[s][r];
       }
     }
   };
+  auto accumulate_b = [&](int tt, const bf16x8 (&b)[QS]) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16x8 a =
+          *reinterpret_cast<const bf16x8*>(&lv[(16 * dt + c) * VROW + 16 * tt + 8 * g]);
+#pragma unroll
+      for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(a, b[s], X[dt][s]);
+    }
+    const bf16 one = (bf16)(c == 0 ? 1.f : 0.f);
+    const bf16x8 ones = {one, one, one, one, one, one, one, one};
+#pragma unroll
+    for (int s = 0; s < QS; ++s) X[DT][s] = mfma_bf16(ones, b[s], X[DT][s]);
+  };
+  // fp32: weights of tile tt as scalar MFMA operands.
+  auto accumulate_f = [&](int tt, const f32x4 (&w0)[QS]) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const float4 a =
+          *reinterpret_cast<const float4*>(&lv[(16 * dt + c) * VROW + 16 * tt + 4 * g]);
+#pragma unroll
+      for (int s = 0; s < QS; ++s) {
+        X[dt][s] = mfma_f32(a.x, w0[s][0], X[dt][s]);
+        X[dt][s] = mfma_f32(a.y, w0[s][1], X[dt][s]);
+        X[dt][s] = mfma_f32(a.z, w0[s][2], X[dt][s]);
+        X[dt][s] = mfma_f32(a.w, w0[s][3], X[dt][s]);
+      }
+    }
+    const float one = c == 0 ? 1.f : 0.f;
+#pragma unroll
+    for (int s = 0; s < QS; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) X[DT][s] = mfma_f32(one, w0[s][r], X[DT][s]);
+  };
 
-  // Per-lane softmax state for query columns c + 16 s. zp holds this lane
-  // group's partial denominator; the four groups are summed when needed.
+  // Per-lane softmax state for query columns c + 16 s, in log2 units: m is
+  // the running max of t, started at a finite floor so that t - m stays
+  // -inf (weight 0) for empty codewords even before any non-empty one was
+  // seen. zp holds this lane group's partial fp32 sum of the parent weights
+  // (for importance); the four groups are summed when needed.
+  constexpr float kMaxFloor = -1e30f;
   float m[QS], zp[QS];
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
-    m[s] = -__builtin_inff();
+    m[s] = kMaxFloor;
     zp[s] = 0.f;
   }
-  auto full_z = [&](int s) {
+  auto full_zp = [&](int s) {
     float z = zp[s];
     z += shfl_xor(z, 16);
     z += shfl_xor(z, 32);
     return z;
   };
-  auto rescale = [&](const float (&mnew)[QS]) {
+  auto raise_max = [&](float (&mnew)[QS]) {
+    bool moved = false;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
-      const float sc = (mnew[s] == -__builtin_inff()) ? 1.f : exp_neg(m[s] - mnew[s]);
+      mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 16));
+      mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 32));
+      moved |= mnew[s] != m[s];
+    }
+    if (__ballot(moved) == 0) return;  // wave-uniform: nothing to rescale
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      const float sc = exp2_hw(m[s] - mnew[s]);
       zp[s] *= sc;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) X[dt][s] *= sc;
+      for (int dt = 0; dt < XT; ++dt) X[dt][s] *= sc;
       m[s] = mnew[s];
     }
   };
@@ -270,14 +339,27 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
   f32x4 S[NT][QS];
 
   // ---- phase 1: parent pass (online softmax over register groups) -----------
-  const int32_t* nb = counts + (size_t)bh * Mtot;
-  for (int a = tid; a < M0MAX; a += nthr) lnp[a] = a < M0 ? (float)nb[a] : 0.f;
+  for (int a = tid; a < M0MAX; a += nthr) {
+    const int n = a < M0 ? cb[a] : 0;
+    lp[a] = n > 0 ? log2_hw((float)n) : kNegInf;
+  }
   __syncthreads();
-  auto parent_count = [&](int a) -> float { return lnp[a]; };
 
-  for (int grp = 0; grp < n_groups; ++grp) {
-    const int gbase = grp * Cfg::GROUP;
-    // logits for the whole group (chunks staged one after another)
+  // t = S log2(e) + log2 n for the group's logits held in S
+  auto bias_group = [&](int gbase) {
+#pragma unroll
+    for (int ti = 0; ti < NT; ++ti) {
+      const float4 l4 = *reinterpret_cast<const float4*>(&lp[gbase + 16 * ti + 4 * g]);
+#pragma unroll
+      for (int s = 0; s < QS; ++s) {
+        S[ti][s][0] = fmaf(S[ti][s][0], kLog2e, l4.x);
+        S[ti][s][1] = fmaf(S[ti][s][1], kLog2e, l4.y);
+        S[ti][s][2] = fmaf(S[ti][s][2], kLog2e, l4.z);
+        S[ti][s][3] = fmaf(S[ti][s][3], kLog2e, l4.w);
+      }
+    }
+  };
+  auto group_logits = [&](int gbase, bool with_values) {
 #pragma unroll
     for (int k = 0; k < NT * 16 / CW; ++k) {
       const int cbase = gbase + k * CW;
@@ -286,6 +368,8 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
         stage_codes([&](int r) -> const T* {
           return cbase + r < M0 ? cp_head + (size_t)(cbase + r) * D : nullptr;
         });
+        if (with_values)
+          stage_values([&](int r) -> int { return cbase + r < M0 ? cbase + r : -1; });
         __syncthreads();
       }
 #pragma unroll
@@ -299,172 +383,246 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
         }
       }
     }
-    // masked group max and rescale
+    bias_group(gbase);
+  };
+
+  constexpr bool kOneChunk = (CW == Cfg::GROUP);
+  const bool need_importance =
+      (P > 0 && P < M0) || args.importance != nullptr || (P > 0 && args.topp_idx != nullptr);
+  float rz[QS];
+
+  // u_a = sum over this wave's queries of W_ia / Z_i for the group in S: first
+  // over the query subtiles in registers, then over the 16 query columns by a
+  // reduce-scatter butterfly over lane bits 3, 0, 1, 2, which leaves lane c
+  // with the L values of block perm(c) = 8 b3 + 4 b0 + 2 b1 + b2.
+  auto importance_partials = [&](int gbase) {
+    constexpr int NV = NT * 4, L = NT / 4;
+    float u[NV];
+#pragma unroll
+    for (int ti = 0; ti < NT; ++ti)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int s = 0; s < QS; ++s) acc = fmaf(S[ti][s][r], rz[s], acc);
+        u[4 * ti + r] = acc;
+      }
+    auto step = [&](auto mask_tag, int half) {
+      constexpr int MASK = decltype(mask_tag)::value;
+      const bool upper = (c & MASK) != 0;
+#pragma unroll
+      for (int i = 0; i < NV / 2; ++i) {
+        if (i < half) {
+          const float lo = u[i] + xor16<MASK>(u[i]);
+          const float hi = u[i + half] + xor16<MASK>(u[i + half]);
+          u[i] = upper ? hi : lo;
+        }
+      }
+    };
+    step(std::integral_constant<int, 8>{}, NV / 2);
+    step(std::integral_constant<int, 1>{}, NV / 4);
+    step(std::integral_constant<int, 2>{}, NV / 8);
+    step(std::integral_constant<int, 4>{}, NV / 16);
+    const int blk = 8 * ((c >> 3) & 1) + 4 * (c & 1) + 2 * ((c >> 1) & 1) + ((c >> 2) & 1);
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int k = L * blk + i;
+      const int a = gbase + 16 * (k / 4) + 4 * g + (k % 4);
+      if (a < M0MAX) lw[wave * M0MAX + a] = u[i];
+    }
+  };
+  auto set_rz = [&]() {
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      const float z = full_zp(s);
+      rz[s] = qvalid[s] ? 1.f / z : 0.f;
+    }
+  };
+
+  for (int grp = 0; grp < n_groups; ++grp) {
+    const int gbase = grp * Cfg::GROUP;
+    group_logits(gbase, kOneChunk);
     float mnew[QS];
 #pragma unroll
     for (int s = 0; s < QS; ++s) mnew[s] = m[s];
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float n = parent_count(gbase + 16 * ti + 4 * g + r);
+      for (int s = 0; s < QS; ++s)
 #pragma unroll
-        for (int s = 0; s < QS; ++s)
-          if (n > 0.f) mnew[s] = fmaxf(mnew[s], S[ti][s][r]);
-      }
-#pragma unroll
-    for (int s = 0; s < QS; ++s) {
-      mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 16));
-      mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 32));
-    }
-    rescale(mnew);
-    // A = exp(S - m), zero for empty parents; Zbar += A n
+        for (int r = 0; r < 4; ++r) mnew[s] = fmaxf(mnew[s], S[ti][s][r]);
+    raise_max(mnew);
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float n = parent_count(gbase + 16 * ti + 4 * g + r);
+      for (int s = 0; s < QS; ++s)
 #pragma unroll
-        for (int s = 0; s < QS; ++s) {
-          const float a = (n > 0.f) ? exp_neg(S[ti][s][r] - m[s]) : 0.f;
-          S[ti][s][r] = a;
-          zp[s] = fmaf(a, n, zp[s]);
+        for (int r = 0; r < 4; ++r) {
+          const float w = exp2_hw(S[ti][s][r] - m[s]);
+          S[ti][s][r] = w;
+          zp[s] += w;
         }
-      }
-    // Xbar += Vbar^T A, staging the Vbar rows of the group chunk by chunk
+    // one group: its max and denominators are final, so importance comes
+    // straight from these weights before they are consumed
+    if (n_groups == 1 && need_importance) {
+      set_rz();
+      importance_partials(gbase);
+    }
+    if constexpr (kB) {
+      bf16x8 Sb[NT / 2][QS];
 #pragma unroll
-    for (int k = 0; k < NT * 16 / CW; ++k) {
-      const int cbase = gbase + k * CW;
-      if (cbase >= M0) break;
-      __syncthreads();
-      stage_values([&](int r) -> int { return cbase + r < M0 ? cbase + r : -1; });
-      __syncthreads();
-      if constexpr (kB) {
+      for (int ti = 0; ti < NT; ti += 2) pack(S[ti], S[ti + 1], Sb[ti / 2]);
+#pragma unroll
+      for (int k = 0; k < NT * 16 / CW; ++k) {
+        const int cbase = gbase + k * CW;
+        if (cbase >= M0) break;
+        if constexpr (!kOneChunk) {
+          __syncthreads();
+          stage_values([&](int r) -> int { return cbase + r < M0 ? cbase + r : -1; });
+          __syncthreads();
+        }
 #pragma unroll
         for (int tt = 0; tt < CW / 16; tt += 2) {
           const int ti = k * (CW / 16) + tt;
-          accumulate(tt, S[ti], S[ti + 1]);
+          if (cbase + 16 * tt < M0) accumulate_b(tt, Sb[ti / 2]);
         }
-      } else {
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < NT * 16 / CW; ++k) {
+        const int cbase = gbase + k * CW;
+        if (cbase >= M0) break;
+        if constexpr (!kOneChunk) {
+          __syncthreads();
+          stage_values([&](int r) -> int { return cbase + r < M0 ? cbase + r : -1; });
+          __syncthreads();
+        }
 #pragma unroll
         for (int tt = 0; tt < CW / 16; ++tt) {
           const int ti = k * (CW / 16) + tt;
-          accumulate(tt, S[ti], S[ti]);
+          if (cbase + 16 * tt < M0) accumulate_f(tt, S[ti]);
         }
       }
     }
   }
 
   // ---- phase 2: importance with the final denominators -----------------------
-  const bool need_importance = (P > 0) || (args.importance != nullptr);
   if (need_importance) {
-    float rz[QS];
-#pragma unroll
-    for (int s = 0; s < QS; ++s) {
-      const float z = full_z(s);
-      rz[s] = qvalid[s] ? 1.f / z : 0.f;
-    }
-    for (int grp = 0; grp < n_groups; ++grp) {
-      const int gbase = grp * Cfg::GROUP;
-      if (n_groups > 1) {
+    if (n_groups > 1) {
+      set_rz();
+      for (int grp = 0; grp < n_groups; ++grp) {
         // recompute this group's logits and weights with the final max
-#pragma unroll
-        for (int k = 0; k < NT * 16 / CW; ++k) {
-          const int cbase = gbase + k * CW;
-          if (cbase < M0) {
-            __syncthreads();
-            stage_codes([&](int r) -> const T* {
-              return cbase + r < M0 ? cp_head + (size_t)(cbase + r) * D : nullptr;
-            });
-            __syncthreads();
-          }
-#pragma unroll
-          for (int tt = 0; tt < CW / 16; ++tt) {
-            const int ti = k * (CW / 16) + tt;
-            if (cbase + 16 * tt < M0) {
-              logits(tt, S[ti]);
-            } else {
-#pragma unroll
-              for (int s = 0; s < QS; ++s) S[ti][s] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
-          }
-        }
+        const int gbase = grp * Cfg::GROUP;
+        group_logits(gbase, false);
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float n = parent_count(gbase + 16 * ti + 4 * g + r);
+          for (int s = 0; s < QS; ++s)
 #pragma unroll
-            for (int s = 0; s < QS; ++s)
-              S[ti][s][r] = (n > 0.f) ? exp_neg(S[ti][s][r] - m[s]) : 0.f;
-          }
-      }
-      // u_a = sum over this wave's queries of A_ia / Zbar_i: first over the
-      // query subtiles in registers, then over the 16 query columns by a
-      // reduce-scatter butterfly that leaves lane c with values [L c, L c + L).
-      constexpr int NV = NT * 4, L = NT / 4;
-      float u[NV];
-#pragma unroll
-      for (int ti = 0; ti < NT; ++ti)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float acc = 0.f;
-#pragma unroll
-          for (int s = 0; s < QS; ++s) acc = fmaf(S[ti][s][r], rz[s], acc);
-          u[4 * ti + r] = acc;
-        }
-#pragma unroll
-      for (int step = 0; step < 4; ++step) {
-        const int mask = 8 >> step;
-        const int half = NV >> (step + 1);
-        const bool upper = (c & mask) != 0;
-#pragma unroll
-        for (int i = 0; i < half; ++i) {
-          const float lo = u[i], hi = u[i + half];
-          const float send = upper ? lo : hi;
-          const float keep = upper ? hi : lo;
-          u[i] = keep + shfl_xor(send, mask);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < L; ++i) {
-        const int k = L * c + i;
-        const int a = gbase + 16 * (k / 4) + 4 * g + (k % 4);
-        if (a < M0MAX) lw[wave * M0MAX + a] = u[i];
+            for (int r = 0; r < 4; ++r) S[ti][s][r] = exp2_hw(S[ti][s][r] - m[s]);
+        importance_partials(gbase);
       }
     }
     __syncthreads();
-    // sum the wave partials in fixed order, weight by the counts
+    // sum the wave partials in fixed order
     for (int a = tid; a < M0; a += nthr) {
       float acc = 0.f;
       for (int wv = 0; wv < nwaves; ++wv) acc += lw[wv * M0MAX + a];
-      const float w = acc * (float)nb[a];
-      lwf[a] = w;
+      lwf[a] = acc;
       if (args.importance)
-        args.importance[((size_t)bh * args.n_tiles + t) * M0 + a] = w;
+        args.importance[((size_t)bh * args.n_tiles + t) * M0 + a] = acc;
     }
     __syncthreads();
   }
 
-  // ---- phase 3: top-P by rank counting (w desc, index asc) --------------------
+  // ---- phase 3: top-P (w desc, index asc) -------------------------------------
   if (P > 0) {
-    for (int a = tid; a < M0; a += nthr) {
-      const float wa = lwf[a];
-      int rank = 0;
-      for (int k = 0; k < M0; ++k) {
-        const float wk = lwf[k];
-        rank += (wk > wa) || (wk == wa && k < a);
+    if (P < M0) {
+      for (int i = tid; i < 256; i += nthr) lhist[i] = 0;
+      if (tid == 0) lmisc[2] = 0;
+      __syncthreads();
+      for (int a = tid; a < M0; a += nthr) atomicAdd(&lhist[(__float_as_uint(lwf[a]) >> 23) & 255], 1);
+      __syncthreads();
+      if (wave == 0) {
+        // lane l holds bins 255 - 4l - i (i = 0..3): lanes in descending bins
+        int cnt[4], local = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cnt[i] = lhist[255 - 4 * lane - i];
+          local += cnt[i];
+        }
+        int incl = local;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+          const int y = __shfl_up(incl, off, kWave);
+          if (lane >= off) incl += y;
+        }
+        int above = incl - local;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (above < P && P <= above + cnt[i]) {
+            lmisc[0] = 255 - 4 * lane - i;
+            lmisc[1] = above;
+          }
+          above += cnt[i];
+        }
       }
-      if (rank < P) {
-        lsel[rank] = a;
-        if (args.topp_idx) args.topp_idx[((size_t)bh * args.n_tiles + t) * P + rank] = a;
+      __syncthreads();
+      const int bstar = lmisc[0], need = P - lmisc[1];
+      int* bmem = reinterpret_cast<int*>(lw);  // boundary-bin members (lw is free now)
+      for (int a = tid; a < M0; a += nthr) {
+        const int bin = (int)((__float_as_uint(lwf[a]) >> 23) & 255);
+        lflag[a] = bin > bstar ? 1 : 0;
+        if (bin == bstar) bmem[atomicAdd(&lmisc[2], 1)] = a;
+      }
+      __syncthreads();
+      const int nbm = lmisc[2];
+      for (int q = tid; q < nbm; q += nthr) {
+        const int a = bmem[q];
+        const float wa = lwf[a];
+        int rank = 0;
+        for (int k = 0; k < nbm; ++k) {
+          const int b = bmem[k];
+          const float wb = lwf[b];
+          rank += (wb > wa) || (wb == wa && b < a);
+        }
+        if (rank < need) lflag[a] = 1;
+      }
+    } else {
+      for (int a = tid; a < M0; a += nthr) lflag[a] = 1;
+    }
+    __syncthreads();
+    if (wave == 0) {  // selected parents in ascending index order
+      int filled = 0;
+      for (int a0 = 0; a0 < M0; a0 += kWave) {
+        const int a = a0 + lane;
+        const bool f = a < M0 && lflag[a] != 0;
+        const unsigned long long mask = __ballot(f);
+        if (f) lsel[filled + __popcll(mask & ((1ull << lane) - 1ull))] = a;
+        filled += __popcll(mask);
       }
     }
     __syncthreads();
+    if (args.topp_idx) {  // canonical order (w desc, index asc) for the caller
+      const bool have_w = need_importance;
+      for (int q = tid; q < P; q += nthr) {
+        const int a = lsel[q];
+        const float wa = have_w ? lwf[a] : 0.f;
+        int rank = 0;
+        for (int k = 0; k < P; ++k) {
+          const int b = lsel[k];
+          const float wb = have_w ? lwf[b] : 0.f;
+          rank += (wb > wa) || (wb == wa && b < a);
+        }
+        args.topp_idx[((size_t)bh * args.n_tiles + t) * P + rank] = a;
+      }
+    }
 
     // ---- phase 4: child refinement ------------------------------------------
+    // With one child the recovered parent logit is that child's own logit, so
+    // every correcting weight is exactly zero: nothing to do.
     const T* cc_head = Cc + (size_t)h * M0 * Ch * D;
-    const int rows = P * Ch;
+    const int rows = Ch > 1 ? P * Ch : 0;
     for (int cbase = 0; cbase < rows; cbase += CW) {
       __syncthreads();
       stage_codes([&](int r) -> const T* {
@@ -477,70 +635,84 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
         return q < rows ? M0 + lsel[q / Ch] * Ch + (q % Ch) : -1;
       });
       __syncthreads();
-      f32x4 Sc[CW / 16][QS];
+      // tiles in halves of HT so that logits and weights of a half stay in
+      // registers next to the accumulators
+      constexpr int HT = (CW / 16) < (NT / 2) ? (CW / 16) : (NT / 2);
 #pragma unroll
-      for (int tt = 0; tt < CW / 16; ++tt) logits(tt, Sc[tt]);
-      // running max over the non-empty children of the chunk
-      float mnew[QS];
+      for (int h0 = 0; h0 < CW / 16; h0 += HT) {
+        if (cbase + 16 * h0 >= rows) break;
+        f32x4 Sc[HT][QS];
+        float sp[HT][QS][2];  // recovered parent logits (rows 0-1 / 2-3 for Ch = 2)
 #pragma unroll
-      for (int s = 0; s < QS; ++s) mnew[s] = m[s];
+        for (int tt = 0; tt < HT; ++tt) {
+          logits(h0 + tt, Sc[tt]);
 #pragma unroll
-      for (int tt = 0; tt < CW / 16; ++tt)
+          for (int s = 0; s < QS; ++s) {
+            const f32x4 v = Sc[tt][s];
+            if (Ch == 2) {
+              sp[tt][s][0] = (v[0] + v[1]) * 0.5f;
+              sp[tt][s][1] = (v[2] + v[3]) * 0.5f;
+            } else {
+              float sum = (v[0] + v[1]) + (v[2] + v[3]);
+              if (Ch >= 8) sum += shfl_xor(sum, 16);
+              if (Ch >= 16) sum += shfl_xor(sum, 32);
+              sp[tt][s][0] = sum * (1.f / (float)Ch);
+              sp[tt][s][1] = sp[tt][s][0];
+            }
+          }
+          const float4 l4 = *reinterpret_cast<const float4*>(&ll[16 * (h0 + tt) + 4 * g]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float n = ln[16 * tt + 4 * g + r];
+          for (int s = 0; s < QS; ++s) {
+            Sc[tt][s][0] = fmaf(Sc[tt][s][0], kLog2e, l4.x);
+            Sc[tt][s][1] = fmaf(Sc[tt][s][1], kLog2e, l4.y);
+            Sc[tt][s][2] = fmaf(Sc[tt][s][2], kLog2e, l4.z);
+            Sc[tt][s][3] = fmaf(Sc[tt][s][3], kLog2e, l4.w);
+          }
+        }
+        float mnew[QS];
+#pragma unroll
+        for (int s = 0; s < QS; ++s) mnew[s] = m[s];
+#pragma unroll
+        for (int tt = 0; tt < HT; ++tt)
 #pragma unroll
           for (int s = 0; s < QS; ++s)
-            if (n > 0.f) mnew[s] = fmaxf(mnew[s], Sc[tt][s][r]);
-        }
 #pragma unroll
-      for (int s = 0; s < QS; ++s) {
-        mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 16));
-        mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 32));
-      }
-      rescale(mnew);
-      // recovered parent logit = mean of the Ch child logits of each parent
+            for (int r = 0; r < 4; ++r) mnew[s] = fmaxf(mnew[s], Sc[tt][s][r]);
+        raise_max(mnew);
+        // dW = n_c (exp(T_c - m) - exp(Srec - m)); empty rows have n = 0 and
+        // t = -inf, so dW = 0 (the recovered term is clamped to stay finite)
 #pragma unroll
-      for (int tt = 0; tt < CW / 16; ++tt) {
+        for (int tt = 0; tt < HT; ++tt) {
+          const float4 n4 = *reinterpret_cast<const float4*>(&ln[16 * (h0 + tt) + 4 * g]);
 #pragma unroll
-        for (int s = 0; s < QS; ++s) {
-          f32x4 sp;
-          if (Ch == 1) {
-            sp = Sc[tt][s];
-          } else if (Ch == 2) {
-            const float a = Sc[tt][s][0] + Sc[tt][s][1], b = Sc[tt][s][2] + Sc[tt][s][3];
-            sp = f32x4{a, a, b, b} * 0.5f;
-          } else {
-            float sum = (Sc[tt][s][0] + Sc[tt][s][1]) + (Sc[tt][s][2] + Sc[tt][s][3]);
-            if (Ch >= 8) sum += shfl_xor(sum, 16);
-            if (Ch >= 16) sum += shfl_xor(sum, 32);
-            const float mean = sum * (1.f / (float)Ch);
-            sp = f32x4{mean, mean, mean, mean};
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float n = ln[16 * tt + 4 * g + r];
-            const float da = exp_neg(Sc[tt][s][r] - m[s]) - exp_neg(sp[r] - m[s]);
-            const float dA = (n > 0.f) ? da : 0.f;
-            Sc[tt][s][r] = dA;
-            zp[s] = fmaf(dA, n, zp[s]);
+          for (int s = 0; s < QS; ++s) {
+            const float e0 = exp2_hw(fminf(fmaf(sp[tt][s][0], kLog2e, -m[s]), 64.f));
+            const float e1 = Ch == 2 ? exp2_hw(fminf(fmaf(sp[tt][s][1], kLog2e, -m[s]), 64.f)) : e0;
+            Sc[tt][s][0] = fmaf(-n4.x, e0, exp2_hw(Sc[tt][s][0] - m[s]));
+            Sc[tt][s][1] = fmaf(-n4.y, e0, exp2_hw(Sc[tt][s][1] - m[s]));
+            Sc[tt][s][2] = fmaf(-n4.z, e1, exp2_hw(Sc[tt][s][2] - m[s]));
+            Sc[tt][s][3] = fmaf(-n4.w, e1, exp2_hw(Sc[tt][s][3] - m[s]));
           }
         }
-      }
-      if constexpr (kB) {
+        if constexpr (kB) {
 #pragma unroll
-        for (int tt = 0; tt < CW / 16; tt += 2) accumulate(tt, Sc[tt], Sc[tt + 1]);
-      } else {
+          for (int tt = 0; tt < HT; tt += 2) {
+            bf16x8 b[QS];
+            pack(Sc[tt], Sc[tt + 1], b);
+            accumulate_b(h0 + tt, b);
+          }
+        } else {
 #pragma unroll
-        for (int tt = 0; tt < CW / 16; ++tt) accumulate(tt, Sc[tt], Sc[tt]);
+          for (int tt = 0; tt < HT; ++tt) accumulate_f(h0 + tt, Sc[tt]);
+        }
       }
     }
   }
 
-  // ---- phase 5: Y = Xbar / Zbar ------------------------------------------------
+  // ---- phase 5: Y = Xbar / Z (Z from the denominator tile, lane group 0) ------
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
-    const float z = full_z(s);
+    const float z = __shfl(X[DT][s][0], c, kWave);
     if (!qvalid[s]) continue;
     const float rinv = 1.f / z;
     const int i = row0 + 16 * s + c;
@@ -563,8 +735,13 @@ hipError_t launch_attention_cfg(const AttnArgs& a, int BH, hipStream_t stream) {
   const long long grid = (long long)BH * a.n_tiles;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   const int waves = (a.block_q + 31) / 32;
+  using Cfg = AttnCfg<T, D, NT, MAXW>;
+  constexpr int slot = 8 + (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0) + (MAXW == 8 ? 1 : 0);
+  hipError_t e = ensure_dynamic_lds((const void*)attention_kernel<T, D, NT, MAXW>,
+                                    (int)Cfg::LDS_BYTES, slot);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attention_kernel<T, D, NT, MAXW>), dim3((unsigned)grid), dim3(waves * 64),
-                     0, stream, a);
+                     Cfg::LDS_BYTES, stream, a);
   return hipGetLastError();
 }
 
@@ -593,21 +770,15 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
   return launch_attention_cfg<T, D, 8, 8>(a, BH, stream);
 }
 
-template hipError_t launch_attention<bf16, 64>(int, int, int, int, int, int, int, const void*,
-                                               const void*, const void*, const float*,
-                                               const int32_t*, void*, int32_t*, float*,
-                                               hipStream_t);
-template hipError_t launch_attention<bf16, 128>(int, int, int, int, int, int, int, const void*,
-                                                const void*, const void*, const float*,
-                                                const int32_t*, void*, int32_t*, float*,
-                                                hipStream_t);
-template hipError_t launch_attention<float, 64>(int, int, int, int, int, int, int, const void*,
-                                                const void*, const void*, const float*,
-                                                const int32_t*, void*, int32_t*, float*,
-                                                hipStream_t);
-template hipError_t launch_attention<float, 128>(int, int, int, int, int, int, int, const void*,
-                                                 const void*, const void*, const float*,
-                                                 const int32_t*, void*, int32_t*, float*,
-                                                 hipStream_t);
+#define AVQ_INSTANTIATE(T, D)                                                                  \
+  template hipError_t launch_attention<T, D>(int, int, int, int, int, int, int, const void*,   \
+                                             const void*, const void*, const float*,           \
+                                             const int32_t*, void*, int32_t*, float*,          \
+                                             hipStream_t);
+AVQ_INSTANTIATE(bf16, 64)
+AVQ_INSTANTIATE(bf16, 128)
+AVQ_INSTANTIATE(float, 64)
+AVQ_INSTANTIATE(float, 128)
+#undef AVQ_INSTANTIATE
 
 }  // namespace avq

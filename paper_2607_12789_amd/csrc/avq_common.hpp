@@ -10,6 +10,7 @@ namespace avq {
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
@@ -41,11 +42,33 @@ __device__ __forceinline__ f32x4 mfma_f32(float a, float b, const f32x4& c) {
 __device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, kWave); }
 __device__ __forceinline__ int shfl_xor(int v, int mask) { return __shfl_xor(v, mask, kWave); }
 
-// fp32 exp(x) for x <= 0 (every weight here is exp of a logit minus a running
-// max): the hardware base-2 exponential of x * log2(e).
-__device__ __forceinline__ float exp_neg(float x) {
-  return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
+// Data-parallel-primitive lane moves inside each row of 16 lanes (VALU, no
+// LDS). CTRL encodings: quad_perm [1,0,3,2] = 0xB1, [2,3,0,1] = 0x4E,
+// [3,2,1,0] = 0x1B, row_half_mirror = 0x141, row_ror:8 = 0x128.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
+// Value of lane (i ^ MASK) for MASK in {1, 2, 4, 8}, within a row of 16 lanes.
+template <int MASK>
+__device__ __forceinline__ float xor16(float v) {
+  if constexpr (MASK == 1) return dpp<0xB1>(v);
+  if constexpr (MASK == 2) return dpp<0x4E>(v);
+  if constexpr (MASK == 4) return dpp<0x1B>(dpp<0x141>(v));  // i^7 then i^3
+  if constexpr (MASK == 8) return dpp<0x128>(v);               // rotate a row by 8
+  return v;
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// fp32 exp(x) (every weight here is exp of a logit minus a running max): the
+// hardware base-2 exponential of x * log2(e).
+__device__ __forceinline__ float exp_neg(float x) {
+  return __builtin_amdgcn_exp2f(x * kLog2e);
+}
+// Hardware base-2 exponential and logarithm (fp32).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float log2_hw(float x) { return __builtin_amdgcn_logf(x); }
 
 template <typename T>
 __device__ __forceinline__ float to_f32(T v) { return (float)v; }
@@ -71,5 +94,16 @@ __device__ __forceinline__ int xcd_remap(int i, int n) {
   if (n % kXcd != 0) return i;
   return (i % kXcd) * (n / kXcd) + i / kXcd;
 }
+
+// Per-device facts the launchers need, queried once per device.
+struct DeviceInfo {
+  int lds_max = 0;  // bytes of LDS one workgroup may use
+  int cus = 0;      // compute units
+};
+hipError_t device_info(DeviceInfo* out);
+
+// Raises a kernel's dynamic-LDS limit once per device (the attribute is a
+// property of the kernel on the current device).
+hipError_t ensure_dynamic_lds(const void* kernel, int bytes, int slot);
 
 }  // namespace avq

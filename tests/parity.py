@@ -14,8 +14,10 @@ Error bounds (u = 2^-24, gamma_n = n u / (1 - n u)):
 * parent distances ||c||^2 - 2 k.c: products of bf16 inputs are exact in
   fp32 and the sums over d take gamma_d, so the error of one candidate is at
   most gamma_d (||c||^2 + 2 ||k|| ||c||) + u |value|;
-* child and recomputed parent distances sum (k - c)^2 in fp32: error at most
-  gamma_(d+1) times the distance;
+* child and recomputed parent distances: fp32 sums of (k - c)^2 (error at
+  most gamma_(d+1) times the distance) or, for bf16, ||c||^2 - 2 k.c from
+  dot products of exact bf16 products (error at most
+  (gamma_d + u)(||c||^2 + 2 ||k|| ||c||)); both bounds are added;
 * importance: the logits carry gamma_d ||q|| ||c||, the weights exp(S - m)
   twice that plus the exp unit's rounding of (S - m) log2 e, and the
   normalised sums gamma_(M0 + block_q); w is compared relative to
@@ -74,9 +76,14 @@ def check_assign(x, w, g, o) -> tuple:
     bad = par_cert & (gp != op)
     assert not bad.any(), f"{bad.sum()} certified parent decisions differ, e.g. at {np.argwhere(bad)[:5]}"
 
-    err_c = 2 * gamma(d + 1) * (o["d_child"] + o["d_parent"]) + 1e-30
+    # child compare: bound both the direct form and ||c||^2 - 2 k.c (bf16)
+    cn = np.maximum(np.linalg.norm(Cc, axis=-1).max(axis=(-1, -2)),
+                    np.linalg.norm(Cp, axis=-1).max(axis=-1))[None, :, None]
+    err_x = (gamma(d) + U) * (cn ** 2 + 2 * knorm * cn)
+    err_c = 2 * err_x + gamma(d + 1) * (o["d_child"] + o["d_parent"]) + 1e-30
     move_cert = np.abs(o["d_child"] - o["d_parent"]) > 2 * err_c
-    child_cert = (o["d_child2"] - o["d_child"]) > 2 * 2 * gamma(d + 1) * o["d_child2"]
+    child_cert = (o["d_child2"] - o["d_child"]) > 2 * (2 * err_x + gamma(d + 1) * (
+        o["d_child"] + o["d_child2"]))
     code_cert = par_cert & move_cert & (child_cert | (oc < w.M0))
     bad = code_cert & (gc != oc)
     assert not bad.any(), f"{bad.sum()} certified code decisions differ, e.g. at {np.argwhere(bad)[:5]}"
@@ -90,13 +97,14 @@ def check_assign(x, w, g, o) -> tuple:
         p = gp[b, h, j]
         dc = ((Cc[h, p] - k) ** 2).sum(-1)
         dpar = dp[p]
+        tol = 4 * err_x[b, h, j] + 4 * gamma(d + 1) * (dpar + dc.max())
         if gc[b, h, j] >= w.M0:
             cc = gc[b, h, j] - w.M0
             assert cc // w.Ch == p
-            assert dc[cc % w.Ch] <= min(dc.min(), dpar) + 4 * gamma(d + 1) * (dpar + dc.max())
+            assert dc[cc % w.Ch] <= min(dc.min(), dpar) + tol
         else:
             assert gc[b, h, j] == p
-            assert dpar <= dc.min() + 4 * gamma(d + 1) * (dpar + dc.max())
+            assert dpar <= dc.min() + tol
     clean = ~diff.any(axis=-1)
     rep = Report(keys=int(diff.size), uncertified=int((~code_cert).sum()),
                  differing=int(diff.sum()), heads_excluded=int((~clean).sum()),
