@@ -150,70 +150,105 @@ __global__ __launch_bounds__(MAXW * 64) void attention_kernel(AttnArgs args) {
   }
 
   // ---- LDS staging of a chunk of CW codeword rows ---------------------------
+  // Every thread first issues a batch of global loads, then writes them to
+  // LDS, so a batch costs one memory latency instead of one per element.
   // stage_codes: row r of the chunk <- codebook row crow(r) (nullptr: zeros).
   auto stage_codes = [&](auto crow) {
     constexpr int VEC = 16 / sizeof(T);
     constexpr int VPR = D / VEC;
-    for (int v = tid; v < CW * VPR; v += nthr) {
-      const int r = v / VPR, col = (v % VPR) * VEC;
-      const T* src = crow(r);
-      uint4 val = {0u, 0u, 0u, 0u};
-      if (src) val = *reinterpret_cast<const uint4*>(src + col);
-      *reinterpret_cast<uint4*>(&lc[r * CROW + col]) = val;
+    constexpr int BATCH = 8;
+    for (int v0 = tid; v0 < CW * VPR; v0 += BATCH * nthr) {
+      uint4 val[BATCH];
+#pragma unroll
+      for (int b = 0; b < BATCH; ++b) {
+        const int v = v0 + b * nthr;
+        val[b] = uint4{0u, 0u, 0u, 0u};
+        if (v < CW * VPR) {
+          const T* src = crow(v / VPR);
+          if (src) val[b] = *reinterpret_cast<const uint4*>(src + (v % VPR) * VEC);
+        }
+      }
+#pragma unroll
+      for (int b = 0; b < BATCH; ++b) {
+        const int v = v0 + b * nthr;
+        if (v < CW * VPR)
+          *reinterpret_cast<uint4*>(&lc[(v / VPR) * CROW + (v % VPR) * VEC]) = val[b];
+      }
     }
   };
   // stage_values: mean values Vbar/n (transposed), n and log2 n of aggregate
-  // rows vrow(r) (-1: an empty row).
+  // rows vrow(r) (-1: an empty row). A row's values and its count are loaded
+  // together; an empty row has n = 0 and a zero sum, and is scaled by 0.
   const float* vb = Vbar + (size_t)bh * Mtot * D;
   const int32_t* cb = counts + (size_t)bh * Mtot;
+  auto load_row = [&](int a, int col, float4& x, float& inv) {
+    x = float4{0.f, 0.f, 0.f, 0.f};
+    inv = 0.f;
+    if (a >= 0) {
+      x = *reinterpret_cast<const float4*>(vb + (size_t)a * D + col);
+      const int n = cb[a];
+      inv = n > 0 ? __builtin_amdgcn_rcpf((float)n) : 0.f;
+    }
+  };
   auto stage_values = [&](auto vrow) {
     if constexpr (kB) {
       // bf16, codewords of each 32-block permuted so that lane group g reads
       // its 8 MFMA k-slots {4g..4g+3, 16+4g..16+4g+3} as one 16-byte word:
       // position 8g' + i holds codeword perm(g', i).
-      for (int v = tid; v < (CW / 32) * 4 * (D / 4); v += nthr) {
-        const int dq = v % (D / 4), gg = (v / (D / 4)) % 4, blk = v / (D / 4) / 4;
-        float4 x[8];
+      constexpr int ITEMS = (CW / 32) * 4 * (D / 4);
+      constexpr int IB = 2;  // items in flight per thread
+      for (int v0 = tid; v0 < ITEMS; v0 += IB * nthr) {
+        float4 x[IB][8];
+        float inv[IB][8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int r = 32 * blk + (i < 4 ? 4 * gg + i : 16 + 4 * gg + (i - 4));
-          const int a = vrow(r);
-          const int n = a >= 0 ? cb[a] : 0;
-          x[i] = float4{0.f, 0.f, 0.f, 0.f};
-          if (n > 0) {
-            const float inv = 1.f / (float)n;
-            const float4 y = *reinterpret_cast<const float4*>(vb + (size_t)a * D + 4 * dq);
-            x[i] = float4{y.x * inv, y.y * inv, y.z * inv, y.w * inv};
+        for (int b = 0; b < IB; ++b) {
+          const int v = v0 + b * nthr;
+          const int dq = v % (D / 4), gg = (v / (D / 4)) % 4, blk = v / (D / 4) / 4;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int r = 32 * blk + (i < 4 ? 4 * gg + i : 16 + 4 * gg + (i - 4));
+            load_row(v < ITEMS ? vrow(r) : -1, 4 * dq, x[b][i], inv[b][i]);
           }
         }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          bf16x8 o;
+        for (int b = 0; b < IB; ++b) {
+          const int v = v0 + b * nthr;
+          if (v >= ITEMS) continue;
+          const int dq = v % (D / 4), gg = (v / (D / 4)) % 4, blk = v / (D / 4) / 4;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) o[i] = (bf16)(&x[i].x)[e];
-          *reinterpret_cast<bf16x8*>(&lv[(4 * dq + e) * VROW + 32 * blk + 8 * gg]) = o;
+          for (int e = 0; e < 4; ++e) {
+            bf16x8 o;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) o[i] = (bf16)((&x[b][i].x)[e] * inv[b][i]);
+            *reinterpret_cast<bf16x8*>(&lv[(4 * dq + e) * VROW + 32 * blk + 8 * gg]) = o;
+          }
         }
       }
     } else {
       // fp32, natural codeword order, written as 4x4 transposes.
-      for (int v = tid; v < (CW / 4) * (D / 4); v += nthr) {
-        const int dq = v % (D / 4), rq = v / (D / 4);
-        float4 x[4];
+      constexpr int ITEMS = (CW / 4) * (D / 4);
+      constexpr int IB = 2;
+      for (int v0 = tid; v0 < ITEMS; v0 += IB * nthr) {
+        float4 x[IB][4];
+        float inv[IB][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int a = vrow(4 * rq + i);
-          const int n = a >= 0 ? cb[a] : 0;
-          x[i] = float4{0.f, 0.f, 0.f, 0.f};
-          if (n > 0) {
-            const float inv = 1.f / (float)n;
-            const float4 y = *reinterpret_cast<const float4*>(vb + (size_t)a * D + 4 * dq);
-            x[i] = float4{y.x * inv, y.y * inv, y.z * inv, y.w * inv};
-          }
+        for (int b = 0; b < IB; ++b) {
+          const int v = v0 + b * nthr;
+          const int dq = v % (D / 4), rq = v / (D / 4);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) load_row(v < ITEMS ? vrow(4 * rq + i) : -1, 4 * dq, x[b][i], inv[b][i]);
         }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float4 o = {(&x[0].x)[e], (&x[1].x)[e], (&x[2].x)[e], (&x[3].x)[e]};
-          *reinterpret_cast<float4*>(&lv[(4 * dq + e) * VROW + 4 * rq]) = o;
+        for (int b = 0; b < IB; ++b) {
+          const int v = v0 + b * nthr;
+          if (v >= ITEMS) continue;
+          const int dq = v % (D / 4), rq = v / (D / 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float4 o = {(&x[b][0].x)[e] * inv[b][0], (&x[b][1].x)[e] * inv[b][1],
+                        (&x[b][2].x)[e] * inv[b][2], (&x[b][3].x)[e] * inv[b][3]};
+            *reinterpret_cast<float4*>(&lv[(4 * dq + e) * VROW + 4 * rq]) = o;
+          }
         }
       }
     }
