@@ -87,6 +87,13 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
                         void* stream);
 
 /*
+ * Number of elements of the packed mean values of one (batch, head), see
+ * avq_aggregate: (ceil(M0/4) + M0 * ceil(Ch/4)) * 4 * d. Returns -1 for
+ * non-positive sizes.
+ */
+int64_t avq_packed_means_elems(int32_t M0, int32_t Ch, int32_t d);
+
+/*
  * avq_aggregate - per-codeword counts and value sums (Eq. (aggregates)).
  *
  * Parent rows p < M0 cover the whole parent cell (every key whose nearest
@@ -96,16 +103,27 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
  * (code_idx - M0) / Ch otherwise.
  *
  *   V         [B][H][N][d]      dtype
- *   code_idx  [B][H][N]         int32, values in [0, Mtot) (as avq_assign writes)
- *   Vbar      [B][H][Mtot][d]   fp32, out
+ *   code_idx  [B][H][N]         int32, values in [0, Mtot) (as avq_assign writes;
+ *                               other values are ignored)
+ *   Vbar      [B][H][Mtot][d]   fp32, out, nullable (the sums)
  *   counts    [B][H][Mtot]      int32, out
+ *   Vmean     [B][H][E]         dtype, out, nullable; E = avq_packed_means_elems():
+ *                               the mean value Vbar/n of every code (0 if n = 0),
+ *                               rounded to dtype, in the operand layout that
+ *                               avq_attention_fwd reads: first the parents in
+ *                               groups of 4 consecutive codes, group-major, each
+ *                               group [d][4] (slot s = code 4g+s, zero past M0);
+ *                               then, for every parent p, its children in
+ *                               ceil(Ch/4) groups [d][4] (slot s of group k =
+ *                               child 4k+s, zero past Ch).
+ * At least one of Vbar and Vmean must be given.
  *
- * Sums are accumulated in fp32 with atomics, so the rounding of Vbar may vary
- * between runs; counts are exact.
+ * Every sum is accumulated in fp32 by the one quarter wave that owns the
+ * parent family, keys in bucket order; counts are exact.
  */
 avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
                            int32_t M0, int32_t Ch, const void* V, const int32_t* code_idx,
-                           float* Vbar, int32_t* counts, void* stream);
+                           float* Vbar, int32_t* counts, void* Vmean, void* stream);
 
 /*
  * avq_attention_fwd - the fused refined-codebook attention (Alg. 2).
@@ -133,21 +151,25 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
  *                and top-P are computed per tile of block_q tokens)
  *   Q            [B][H][N][d]    dtype
  *   Cp, Cc       as in avq_assign
- *   Vbar, counts as written by avq_aggregate
+ *   Vmean, counts as written by avq_aggregate (Vmean is required here)
  *   Y            [B][H][N][d]    dtype, out
  *   topp_idx     [B][H][T][P]    int32, out, nullable; T = ceil(N / block_q);
  *                the selected parents in the order importance descending,
  *                index ascending
  *   importance   [B][H][T][M0]   fp32, out, nullable; w_p(I) of every parent
  *
+ * The kernel uses the log-count bias of App. D: a code's weight is
+ * exp(S + ln n - m) applied to its mean value Vbar/n, which equals
+ * exp(S - m) applied to Vbar; empty codes (n = 0) drop out without masks.
+ *
  * Arithmetic: bf16 inputs use bf16 MFMA with fp32 accumulation (the weights
- * A and dA and Vbar are rounded to bf16 as MFMA operands; softmax state,
- * importance and all sums stay fp32); fp32 inputs use fp32 MFMA throughout.
+ * and the mean values are bf16 MFMA operands; softmax state, importance and
+ * all sums stay fp32); fp32 inputs use fp32 MFMA throughout.
  */
 avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
                                int32_t d, int32_t M0, int32_t Ch, int32_t P,
                                int32_t block_q, const void* Q, const void* Cp,
-                               const void* Cc, const float* Vbar, const int32_t* counts,
+                               const void* Cc, const void* Vmean, const int32_t* counts,
                                void* Y, int32_t* topp_idx, float* importance,
                                void* stream);
 

@@ -20,6 +20,9 @@
 //      and adding every finished row sum into the family's register table.
 // At the end the parent row is the stay row plus the children (the whole
 // cell), every row is written once, and counts come from the histograms.
+// Optionally the mean values (sum / count) are also written, rounded to the
+// input type, in groups of 4 codes laid out as the attention kernel's MFMA
+// operands: [group][d][4].
 #include "avq_common.hpp"
 
 namespace avq {
@@ -50,7 +53,8 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
                                                                 const int32_t* __restrict__ code_idx,
                                                                 float* __restrict__ Vbar,
                                                                 int32_t* __restrict__ counts,
-                                                                int N, int M0, int Ch, int F,
+                                                                T* __restrict__ Vmean, int N,
+                                                                int M0, int Ch, int F,
                                                                 int ranges) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   AggLds& L = *reinterpret_cast<AggLds*>(lds_raw);
@@ -210,30 +214,98 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
     __syncthreads();
   }
 
-  // 2. parent row = stay + children; write every row once, and the counts
+  // 2. parent row = stay + children; write every row once, and the counts.
+  //    Packed means (Vmean, optional): the owner writes its children's groups
+  //    of 4 directly; the parents' groups (4 parents from 4 owners) are put
+  //    together through LDS (the queue area is free now).
+  const int PG = (M0 + 3) / 4, CG = (Ch + 3) / 4;
+  float* pmean = reinterpret_cast<float*>(L.qkey);  // [kQuarters][D]
+  float* vb = Vbar ? Vbar + (size_t)bh * Mtot * D : nullptr;
+  T* vm = Vmean ? Vmean + (size_t)bh * (PG + (size_t)M0 * CG) * 4 * D : nullptr;
   if (quarter < nfam) {
     const int p = p0 + quarter;
-    float* vb = Vbar + (size_t)bh * Mtot * D;
+    const int* tot = &L.total[quarter * (1 + Ch)];
     float par[CPL];
 #pragma unroll
     for (int i = 0; i < CPL; ++i) par[i] = acc[0][i];
+    int ncell = tot[0];
 #pragma unroll
     for (int r = 1; r <= kChMax; ++r) {
       if (r <= Ch) {
-        float4* dst =
-            reinterpret_cast<float4*>(vb + (size_t)(M0 + p * Ch + (r - 1)) * D + sub * CPL);
+        if (vb) {
+          float4* dst =
+              reinterpret_cast<float4*>(vb + (size_t)(M0 + p * Ch + (r - 1)) * D + sub * CPL);
 #pragma unroll
-        for (int i = 0; i < CPL; i += 4)
-          dst[i / 4] = float4{acc[r][i], acc[r][i + 1], acc[r][i + 2], acc[r][i + 3]};
+          for (int i = 0; i < CPL; i += 4)
+            dst[i / 4] = float4{acc[r][i], acc[r][i + 1], acc[r][i + 2], acc[r][i + 3]};
+        }
 #pragma unroll
         for (int i = 0; i < CPL; ++i) par[i] += acc[r][i];
+        ncell += tot[r];
       }
     }
-    float4* dst = reinterpret_cast<float4*>(vb + (size_t)p * D + sub * CPL);
+    if (vb) {
+      float4* dst = reinterpret_cast<float4*>(vb + (size_t)p * D + sub * CPL);
 #pragma unroll
-    for (int i = 0; i < CPL; i += 4) dst[i / 4] = float4{par[i], par[i + 1], par[i + 2], par[i + 3]};
+      for (int i = 0; i < CPL; i += 4)
+        dst[i / 4] = float4{par[i], par[i + 1], par[i + 2], par[i + 3]};
+    }
+    if (vm) {
+      const float pinv = ncell > 0 ? 1.f / (float)ncell : 0.f;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) pmean[quarter * D + sub * CPL + i] = par[i] * pinv;
+      // children groups of this parent: [CG][D][4]
+      T* cg = vm + ((size_t)PG + (size_t)p * CG) * 4 * D;
+      for (int k = 0; k < CG; ++k) {
+        float inv[4];
+#pragma unroll
+        for (int sl = 0; sl < 4; ++sl) {
+          const int c = 4 * k + sl;
+          const int n = c < Ch ? tot[1 + c] : 0;
+          inv[sl] = n > 0 ? 1.f / (float)n : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+          float v[4];
+#pragma unroll
+          for (int sl = 0; sl < 4; ++sl) {
+            float a = 0.f;
+#pragma unroll
+            for (int r = 1; r <= kChMax; ++r)
+              if (r == 1 + 4 * k + sl) a = acc[r][i];
+            v[sl] = a * inv[sl];
+          }
+          T* row = cg + ((size_t)k * D + sub * CPL + i) * 4;
+          if constexpr (Elem<T>::kBf16) {
+            bf16x4 o = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+            *reinterpret_cast<bf16x4*>(row) = o;
+          } else {
+            *reinterpret_cast<float4*>(row) = float4{v[0], v[1], v[2], v[3]};
+          }
+        }
+      }
+    }
   }
   __syncthreads();
+  if (vm) {  // parents' groups [D][4] of this range
+    const int ngroups = (nfam + 3) / 4;
+    for (int i = tid; i < ngroups * D; i += kAggThreads) {
+      const int gi = i / D, d = i % D;
+      float v[4];
+#pragma unroll
+      for (int sl = 0; sl < 4; ++sl) {
+        const int q = 4 * gi + sl;
+        v[sl] = q < nfam ? pmean[q * D + d] : 0.f;
+      }
+      T* row = vm + ((size_t)(p0 / 4 + gi) * D + d) * 4;
+      if constexpr (Elem<T>::kBf16) {
+        bf16x4 o = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+        *reinterpret_cast<bf16x4*>(row) = o;
+      } else {
+        *reinterpret_cast<float4*>(row) = float4{v[0], v[1], v[2], v[3]};
+      }
+    }
+  }
   int32_t* nb = counts + (size_t)bh * Mtot;
   for (int f = tid; f < nfam; f += kAggThreads) {
     const int* tot = &L.total[f * (1 + Ch)];
@@ -247,15 +319,18 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
 template <typename T, int D>
 hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
                               const int32_t* code_idx, float* Vbar, int32_t* counts,
-                              hipStream_t stream) {
+                              void* Vmean, hipStream_t stream) {
   DeviceInfo info;
   hipError_t e = device_info(&info);
   if (e != hipSuccess) return e;
   if (Ch > kChMax) return hipErrorInvalidValue;
   // families per workgroup: one per quarter wave, fewer while that leaves
-  // fewer workgroups than CUs
+  // fewer workgroups than CUs. Every range but the last starts at a multiple
+  // of 4 parents, so that each packed group of 4 parent means is written by
+  // one workgroup: F stays a multiple of 4 whenever there is more than one
+  // range.
   int F = kQuarters < M0 ? kQuarters : M0;
-  while (F > 8 && (long long)BH * ((M0 + F - 1) / F) < info.cus) F /= 2;
+  while (F > 8 && F % 8 == 0 && (long long)BH * ((M0 + F - 1) / F) < info.cus) F /= 2;
   const int ranges = (M0 + F - 1) / F;
   const int lds = (int)sizeof(AggLds);
   e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D>, lds,
@@ -264,23 +339,25 @@ hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
   const long long grid = (long long)BH * ranges;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((aggregate_kernel<T, D>), dim3((unsigned)grid), dim3(kAggThreads), lds,
-                     stream, static_cast<const T*>(V), code_idx, Vbar, counts, N, M0, Ch, F,
-                     ranges);
+                     stream, static_cast<const T*>(V), code_idx, Vbar, counts,
+                     static_cast<T*>(Vmean), N, M0, Ch, F, ranges);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
-                            const int32_t* code_idx, float* Vbar, int32_t* counts,
+                            const int32_t* code_idx, float* Vbar, int32_t* counts, void* Vmean,
                             hipStream_t stream) {
-  if (d == 64) return launch_aggregate_d<T, 64>(BH, N, M0, Ch, V, code_idx, Vbar, counts, stream);
-  if (d == 128) return launch_aggregate_d<T, 128>(BH, N, M0, Ch, V, code_idx, Vbar, counts, stream);
+  if (d == 64)
+    return launch_aggregate_d<T, 64>(BH, N, M0, Ch, V, code_idx, Vbar, counts, Vmean, stream);
+  if (d == 128)
+    return launch_aggregate_d<T, 128>(BH, N, M0, Ch, V, code_idx, Vbar, counts, Vmean, stream);
   return hipErrorInvalidValue;
 }
 
 template hipError_t launch_aggregate<bf16>(int, int, int, int, int, const void*, const int32_t*,
-                                           float*, int32_t*, hipStream_t);
+                                           float*, int32_t*, void*, hipStream_t);
 template hipError_t launch_aggregate<float>(int, int, int, int, int, const void*, const int32_t*,
-                                            float*, int32_t*, hipStream_t);
+                                            float*, int32_t*, void*, hipStream_t);
 
 }  // namespace avq

@@ -46,13 +46,31 @@ def to_gpu(x: dict) -> dict:
 def gpu_forward(xd: dict, w) -> dict:
     """Runs the three entry points and returns every output on the CPU."""
     par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
-    Vbar, counts = avq.aggregate(xd["V"], code, w.M0, w.Ch)
-    Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, w.P, w.block_q,
+    Vmean, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
+    Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, w.P, w.block_q,
                                      debug=True)
     torch.cuda.synchronize()
-    out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, counts=counts, Y=Y, topp=topp,
-               importance=imp)
+    out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, Vmean=Vmean, counts=counts, Y=Y,
+               topp=topp, importance=imp)
     return {k: v.cpu() for k, v in out.items()}
+
+
+def unpack_means(vm: np.ndarray, M0: int, Ch: int, d: int):
+    """Packed mean values [B, H, E] -> (means [B, H, Mtot, d], padding slots).
+
+    Layout: the parents in ceil(M0/4) groups [d][4] (slot s of group k is code
+    4k + s), then for every parent ceil(Ch/4) groups [d][4] of its children."""
+    B, H, E = vm.shape
+    PG, CG = (M0 + 3) // 4, (Ch + 3) // 4
+    assert E == (PG + M0 * CG) * 4 * d
+    par = vm[..., :PG * 4 * d].reshape(B, H, PG, d, 4).transpose(0, 1, 2, 4, 3)
+    par = par.reshape(B, H, PG * 4, d)
+    ch = vm[..., PG * 4 * d:].reshape(B, H, M0, CG, d, 4).transpose(0, 1, 2, 3, 5, 4)
+    ch = ch.reshape(B, H, M0, CG * 4, d)
+    means = np.concatenate([par[:, :, :M0], ch[:, :, :, :Ch].reshape(B, H, M0 * Ch, d)], axis=2)
+    pad = np.concatenate([par[:, :, M0:].reshape(B, H, -1), ch[:, :, :, Ch:].reshape(B, H, -1)],
+                         axis=2)
+    return means, pad
 
 
 class Report(dict):
@@ -124,7 +142,19 @@ def check_aggregate(x, w, g, o, clean) -> Report:
     err = np.abs(gV.astype(np.float64) - oV)
     assert (err[clean] <= tol[clean]).all(), f"Vbar error {err[clean].max()} above bound"
     assert (gn[..., :w.M0].sum(-1) == w.N).all()
-    return Report(max_vbar_err=float(err[clean].max()) if clean.any() else 0.0)
+    # Packed means: fl(fl(sum) * fl(1/n)) rounded to the storage dtype; empty
+    # codes and padding slots are exactly zero.
+    means, pad = unpack_means(g["Vmean"].float().numpy().astype(np.float64), w.M0, w.Ch, w.d)
+    assert (pad == 0).all(), "padding slots of the packed means are not zero"
+    n = np.maximum(on, 1)[..., None]
+    omean = oV / n
+    r_store = 2.0 ** -8 if w.dtype == "bf16" else U
+    tol_m = tol / n + (3 * U + r_store) * np.abs(omean) + 1e-30
+    err_m = np.abs(means - omean)
+    assert (err_m[clean] <= tol_m[clean]).all(), f"Vmean error {err_m[clean].max()} above bound"
+    assert (means[clean][on[clean] == 0] == 0).all(), "mean of an empty code is not zero"
+    return Report(max_vbar_err=float(err[clean].max()) if clean.any() else 0.0,
+                  max_mean_err=float(err_m[clean].max()) if clean.any() else 0.0)
 
 
 def importance_eps(x, w, o) -> float:

@@ -37,7 +37,7 @@ def test_header_declares_the_entry_points():
 def test_library_exports_every_declared_symbol(L):
     for name in declared_functions():
         assert hasattr(L, name), name
-    assert L.avq_version() == 100
+    assert L.avq_version() == 101
 
 
 NULL = None
@@ -48,7 +48,7 @@ def assign(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 5):
     return L.avq_assign(dtype, B, H, N, d, M0, Ch, *ptrs, NULL)
 
 
-def aggregate(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 4):
+def aggregate(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 5):
     return L.avq_aggregate(dtype, B, H, N, d, M0, Ch, *ptrs, NULL)
 
 
@@ -75,15 +75,34 @@ def test_null_pointers_are_rejected(L):
         ptrs = [FAKE] * 5
         ptrs[i] = NULL
         assert assign(L, ptrs=ptrs) == INVALID
-    for i in range(4):
-        ptrs = [FAKE] * 4
+    # V, code_idx, counts are required; of Vbar and Vmean at least one
+    for i in (0, 1, 3):
+        ptrs = [FAKE] * 5
         ptrs[i] = NULL
         assert aggregate(L, ptrs=ptrs) == INVALID
+    assert aggregate(L, ptrs=(FAKE, FAKE, NULL, FAKE, NULL)) == INVALID
     for i in range(6):
         ptrs = [FAKE] * 6
         ptrs[i] = NULL
         assert attn(L, ptrs=ptrs) == INVALID
     assert "null" in L.avq_last_error().decode()
+
+
+def test_packed_means_size(L):
+    # parents in ceil(M0/4) groups of 4 codes, then ceil(Ch/4) groups per parent
+    assert L.avq_packed_means_elems(5, 2, 64) == (2 + 5 * 1) * 4 * 64
+    assert L.avq_packed_means_elems(256, 8, 128) == (64 + 256 * 2) * 4 * 128
+    assert L.avq_packed_means_elems(512, 16, 128) == (128 + 512 * 4) * 4 * 128
+    assert L.avq_packed_means_elems(0, 2, 64) == -1
+    assert L.avq_packed_means_elems(4, 2, -1) == -1
+
+
+def test_misaligned_pointers_are_rejected(L):
+    odd = ctypes.c_void_p(24)
+    assert assign(L, ptrs=(odd,) + (FAKE,) * 4) == INVALID
+    assert aggregate(L, ptrs=(FAKE, FAKE, FAKE, FAKE, odd)) == INVALID
+    assert attn(L, ptrs=(FAKE,) * 3 + (odd,) + (FAKE,) * 2) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
 
 
 @pytest.mark.parametrize("P,bq,status", [(-1, 64, INVALID), (5, 64, INVALID), (1, 0, INVALID),

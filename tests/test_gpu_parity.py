@@ -66,6 +66,10 @@ EDGE = {
     "bq1": small(N=50, block_q=1, P=2),
     "m0_512_bq256": small(M0=512, Ch=8, P=64, block_q=256, N=1536, d=128, B=1, H=2),
     "m0_300_bq128": small(M0=300, Ch=4, P=30, block_q=128, N=1024, B=1, H=2),
+    # few heads: the aggregation splits the parents over several workgroups
+    "m0_24_split": small(M0=24, Ch=2, P=5, B=1, H=1, N=700),
+    "m0_44_split": small(M0=44, Ch=4, P=5, B=1, H=1, N=700),
+    "fp32_ch16_d64": small(dtype="f32", M0=70, Ch=16, P=9, N=600),
 }
 
 
@@ -92,9 +96,9 @@ def test_children_equal_parent_gives_vq_attention():
     assert (g["counts"][..., w.M0:] == 0).all()
     from paper_2607_12789_amd import avq
     xd = {k: v.cuda() for k, v in x.items()}
-    Vbar, counts = g["Vbar"].cuda(), g["counts"].cuda()
-    y_ref = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, w.P, w.block_q)
-    y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vbar, counts, 0, w.block_q)
+    Vmean, counts = g["Vmean"].cuda(), g["counts"].cuda()
+    y_ref = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, w.P, w.block_q)
+    y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, 0, w.block_q)
     assert torch.equal(y_ref, y0)
 
 
