@@ -110,15 +110,15 @@ def main():
     B, H, N, d, M0, Ch, P = w.B, w.H, w.N, w.d, w.M0, w.Ch, w.P
     par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
     code = torch.empty_like(par)
-    Vmean = torch.empty((B, H, avq.packed_means_elems(M0, Ch, d)), dtype=w.torch_dtype,
-                        device=dev)
+    packed = torch.empty((B, H, avq.packed_bytes(w.torch_dtype, M0, Ch, d)), dtype=torch.uint8,
+                         device=dev)
     counts = torch.empty((B, H, w.Mtot), dtype=torch.int32, device=dev)
     Y = torch.empty_like(xd["Q"])
 
     def step():
         avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code)
-        avq.aggregate(xd["V"], code, M0, Ch, Vmean, counts)
-        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, P, w.block_q, Y=Y)
+        avq.aggregate(xd["V"], code, M0, Ch, packed, counts)
+        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, P, w.block_q, Y=Y)
 
     for _ in range(args.warmup):
         step()
@@ -142,8 +142,8 @@ def main():
 
     reps = max(args.steps, 1)
     t_assign = timed(lambda: avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code), reps)
-    t_agg = timed(lambda: avq.aggregate(xd["V"], code, M0, Ch, Vmean, counts), reps)
-    t_attn = timed(lambda: avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, P,
+    t_agg = timed(lambda: avq.aggregate(xd["V"], code, M0, Ch, packed, counts), reps)
+    t_attn = timed(lambda: avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, P,
                                              w.block_q, Y=Y), reps)
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4

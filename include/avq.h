@@ -26,7 +26,8 @@
  *   - Codes: Mtot = M0*(1+Ch). Code p < M0 is parent p; code M0 + p*Ch + c is
  *     child c of parent p.
  *   - dtype selects the element type of Q, K, V, Cp, Cc and Y: AVQ_F32 (fp32)
- *     or AVQ_BF16 (bfloat16). Aggregated values are always fp32, counts int32.
+ *     or AVQ_BF16 (bfloat16). Value sums are fp32, counts int32; the packed
+ *     aggregates hold mean values in dtype.
  *   - Logits are exactly Q.C (the paper leaves the 1/sqrt(d) scale out of its
  *     formulas, Eq. (standardattention)); callers fold any scale into Q.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
@@ -57,7 +58,7 @@ typedef enum {
 
 typedef enum { AVQ_F32 = 0, AVQ_BF16 = 1 } avq_dtype_t;
 
-/* Version of this ABI (major * 10000 + minor * 100 + patch). */
+/* Version of this ABI (major * 100 + minor). */
 int avq_version(void);
 
 /* Message for the last non-OK status returned to the calling thread
@@ -87,11 +88,11 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
                         void* stream);
 
 /*
- * Number of elements of the packed mean values of one (batch, head), see
- * avq_aggregate: (ceil(M0/4) + M0 * ceil(Ch/4)) * 4 * d. Returns -1 for
- * non-positive sizes.
+ * Bytes of the packed aggregates of one (batch, head) (see avq_aggregate) for
+ * the given dtype and sizes. Returns -1 for an unknown dtype or sizes outside
+ * 1 <= M0 <= 512, 1 <= Ch <= 16, 1 <= d <= 128.
  */
-int64_t avq_packed_means_elems(int32_t M0, int32_t Ch, int32_t d);
+int64_t avq_packed_bytes(avq_dtype_t dtype, int32_t M0, int32_t Ch, int32_t d);
 
 /*
  * avq_aggregate - per-codeword counts and value sums (Eq. (aggregates)).
@@ -107,23 +108,26 @@ int64_t avq_packed_means_elems(int32_t M0, int32_t Ch, int32_t d);
  *                               other values are ignored)
  *   Vbar      [B][H][Mtot][d]   fp32, out, nullable (the sums)
  *   counts    [B][H][Mtot]      int32, out
- *   Vmean     [B][H][E]         dtype, out, nullable; E = avq_packed_means_elems():
- *                               the mean value Vbar/n of every code (0 if n = 0),
- *                               rounded to dtype, in the operand layout that
- *                               avq_attention_fwd reads: first the parents in
- *                               groups of 4 consecutive codes, group-major, each
- *                               group [d][4] (slot s = code 4g+s, zero past M0);
- *                               then, for every parent p, its children in
- *                               ceil(Ch/4) groups [d][4] (slot s of group k =
- *                               child 4k+s, zero past Ch).
- * At least one of Vbar and Vmean must be given.
+ *   packed    [B][H][E] bytes, out, nullable; E = avq_packed_bytes(): the
+ *             aggregates in the operand layout avq_attention_fwd reads. Codes
+ *             are grouped in octets of 8; the octets are, in order, the parents
+ *             (parents 8o .. 8o+7, padded with empty octets to a multiple of 8
+ *             octets), then for every parent p its ceil(Ch/8) child octets
+ *             (children 8j .. 8j+7 of p), then one empty octet. The buffer is
+ *               means [n_oct][d][8] in dtype: mean value Vbar/n of each code
+ *                     of the octet (0 for n = 0 and for padding slots),
+ *                     rounded from fp32;
+ *               info  [n_oct][16] fp32: n of each code (slots 0..7) and ln n
+ *                     (slots 8..15; -inf for n = 0 and padding);
+ *             means first, info right after it.
+ * At least one of Vbar and packed must be given.
  *
  * Every sum is accumulated in fp32 by the one quarter wave that owns the
  * parent family, keys in bucket order; counts are exact.
  */
 avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
                            int32_t M0, int32_t Ch, const void* V, const int32_t* code_idx,
-                           float* Vbar, int32_t* counts, void* Vmean, void* stream);
+                           float* Vbar, int32_t* counts, void* packed, void* stream);
 
 /*
  * avq_attention_fwd - the fused refined-codebook attention (Alg. 2).
@@ -151,7 +155,7 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
  *                and top-P are computed per tile of block_q tokens)
  *   Q            [B][H][N][d]    dtype
  *   Cp, Cc       as in avq_assign
- *   Vmean, counts as written by avq_aggregate (Vmean is required here)
+ *   packed       the packed aggregates written by avq_aggregate (required)
  *   Y            [B][H][N][d]    dtype, out
  *   topp_idx     [B][H][T][P]    int32, out, nullable; T = ceil(N / block_q);
  *                the selected parents in the order importance descending,
@@ -169,8 +173,8 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
 avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
                                int32_t d, int32_t M0, int32_t Ch, int32_t P,
                                int32_t block_q, const void* Q, const void* Cp,
-                               const void* Cc, const void* Vmean, const int32_t* counts,
-                               void* Y, int32_t* topp_idx, float* importance,
+                               const void* Cc, const void* packed, void* Y,
+                               int32_t* topp_idx, float* importance,
                                void* stream);
 
 #ifdef __cplusplus

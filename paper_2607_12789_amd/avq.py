@@ -20,7 +20,7 @@ _lib = None
 AVQ_OK, AVQ_ERR_INVALID_ARG, AVQ_ERR_UNSUPPORTED, AVQ_ERR_DEVICE = 0, 1, 2, 3
 AVQ_F32, AVQ_BF16 = 0, 1
 _DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
-SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_means_elems", "avq_assign",
+SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_bytes", "avq_assign",
            "avq_aggregate", "avq_attention_fwd")
 
 
@@ -45,13 +45,13 @@ def lib():
         i32, vp = ctypes.c_int32, ctypes.c_void_p
         L.avq_version.restype = ctypes.c_int
         L.avq_last_error.restype = ctypes.c_char_p
-        L.avq_packed_means_elems.argtypes = [i32, i32, i32]
-        L.avq_packed_means_elems.restype = ctypes.c_int64
+        L.avq_packed_bytes.argtypes = [ctypes.c_int, i32, i32, i32]
+        L.avq_packed_bytes.restype = ctypes.c_int64
         L.avq_assign.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         L.avq_aggregate.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32,
                                     vp, vp, vp, vp, vp, vp]
         L.avq_attention_fwd.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32, i32,
-                                        vp, vp, vp, vp, vp, vp, vp, vp, vp]
+                                        vp, vp, vp, vp, vp, vp, vp, vp]
         for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -108,43 +108,45 @@ def assign(K, Cp, Cc, parent_idx=None, code_idx=None, stream=None):
     return parent_idx, code_idx
 
 
-def packed_means_elems(M0: int, Ch: int, d: int) -> int:
-    """Elements of the packed mean values of one (batch, head)."""
-    n = lib().avq_packed_means_elems(M0, Ch, d)
+def packed_bytes(dtype: torch.dtype, M0: int, Ch: int, d: int) -> int:
+    """Bytes of the packed aggregates of one (batch, head)."""
+    if dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dtype}: use float32 or bfloat16")
+    n = lib().avq_packed_bytes(_DTYPES[dtype], M0, Ch, d)
     if n < 0:
         raise ValueError(f"invalid sizes M0={M0} Ch={Ch} d={d}")
     return n
 
 
-def aggregate(V, code_idx, M0: int, Ch: int, Vmean=None, counts=None, Vbar=None,
+def aggregate(V, code_idx, M0: int, Ch: int, packed=None, counts=None, Vbar=None,
               sums: bool = False, stream=None):
-    """Per-codeword counts, packed mean values and optionally fp32 sums (``avq_aggregate``).
+    """Per-codeword counts, packed aggregates and optionally fp32 sums (``avq_aggregate``).
 
-    Returns (Vmean, counts, Vbar); Vbar is None unless ``sums`` is set or a
-    buffer is given. Vmean has shape [B, H, packed_means_elems(M0, Ch, d)] in
-    the dtype of V.
+    Returns (packed, counts, Vbar); Vbar is None unless ``sums`` is set or a
+    buffer is given. ``packed`` is a uint8 tensor [B, H, packed_bytes(...)]
+    that ``attention_fwd`` takes.
     """
     B, H, N, d = V.shape
     Mtot = M0 * (1 + Ch)
     _dev(V, "V")
     _dev(code_idx, "code_idx", torch.int32, (B, H, N))
-    E = packed_means_elems(M0, Ch, d)
-    if Vmean is None:
-        Vmean = torch.empty((B, H, E), dtype=V.dtype, device=V.device)
+    E = packed_bytes(V.dtype, M0, Ch, d)
+    if packed is None:
+        packed = torch.empty((B, H, E), dtype=torch.uint8, device=V.device)
     if counts is None:
         counts = torch.empty((B, H, Mtot), dtype=torch.int32, device=V.device)
     if Vbar is None and sums:
         Vbar = torch.empty((B, H, Mtot, d), dtype=torch.float32, device=V.device)
-    _dev(Vmean, "Vmean", V.dtype, (B, H, E))
+    _dev(packed, "packed", torch.uint8, (B, H, E))
     _dev(counts, "counts", torch.int32, (B, H, Mtot))
     if Vbar is not None:
         _dev(Vbar, "Vbar", torch.float32, (B, H, Mtot, d))
     _check(lib().avq_aggregate(_dtype_code(V), B, H, N, d, M0, Ch, _ptr(V), _ptr(code_idx),
-                               _ptr(Vbar), _ptr(counts), _ptr(Vmean), _stream(stream)))
-    return Vmean, counts, Vbar
+                               _ptr(Vbar), _ptr(counts), _ptr(packed), _stream(stream)))
+    return packed, counts, Vbar
 
 
-def attention_fwd(Q, Cp, Cc, Vmean, counts, P: int, block_q: int, Y=None, topp_idx=None,
+def attention_fwd(Q, Cp, Cc, packed, P: int, block_q: int, Y=None, topp_idx=None,
                   importance=None, debug: bool = False, stream=None):
     """Refined-codebook attention (``avq_attention_fwd``).
 
@@ -153,13 +155,11 @@ def attention_fwd(Q, Cp, Cc, Vmean, counts, P: int, block_q: int, Y=None, topp_i
     """
     B, H, N, d = Q.shape
     M0, Ch = Cc.shape[1], Cc.shape[2]
-    Mtot = M0 * (1 + Ch)
     T = (N + block_q - 1) // block_q if block_q > 0 else 0
     _dev(Q, "Q")
     _dev(Cp, "Cp", Q.dtype, (H, M0, d))
     _dev(Cc, "Cc", Q.dtype, (H, M0, Ch, d))
-    _dev(Vmean, "Vmean", Q.dtype, (B, H, packed_means_elems(M0, Ch, d)))
-    _dev(counts, "counts", torch.int32, (B, H, Mtot))
+    _dev(packed, "packed", torch.uint8, (B, H, packed_bytes(Q.dtype, M0, Ch, d)))
     if Y is None:
         Y = torch.empty_like(Q)
     _dev(Y, "Y", Q.dtype, Q.shape)
@@ -173,7 +173,7 @@ def attention_fwd(Q, Cp, Cc, Vmean, counts, P: int, block_q: int, Y=None, topp_i
     if importance is not None:
         _dev(importance, "importance", torch.float32, (B, H, T, M0))
     _check(lib().avq_attention_fwd(_dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(Q),
-                                   _ptr(Cp), _ptr(Cc), _ptr(Vmean), _ptr(counts), _ptr(Y),
+                                   _ptr(Cp), _ptr(Cc), _ptr(packed), _ptr(Y),
                                    _ptr(topp_idx), _ptr(importance), _stream(stream)))
     if debug:
         return Y, topp_idx, importance
@@ -184,5 +184,5 @@ def forward(Q, K, V, Cp, Cc, P: int, block_q: int, stream=None):
     """The whole forward pass: assign, aggregate, attention. Returns Y."""
     M0, Ch = Cc.shape[1], Cc.shape[2]
     _, code_idx = assign(K, Cp, Cc, stream=stream)
-    Vmean, counts, _ = aggregate(V, code_idx, M0, Ch, stream=stream)
-    return attention_fwd(Q, Cp, Cc, Vmean, counts, P, block_q, stream=stream)
+    packed, _, _ = aggregate(V, code_idx, M0, Ch, stream=stream)
+    return attention_fwd(Q, Cp, Cc, packed, P, block_q, stream=stream)

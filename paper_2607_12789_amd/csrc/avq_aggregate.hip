@@ -20,10 +20,12 @@
 //      and adding every finished row sum into the family's register table.
 // At the end the parent row is the stay row plus the children (the whole
 // cell), every row is written once, and counts come from the histograms.
-// Optionally the mean values (sum / count) are also written, rounded to the
-// input type, in groups of 4 codes laid out as the attention kernel's MFMA
-// operands: [group][d][4].
+// Optionally the packed aggregates are also written (avq_packed.hpp): the
+// mean value (sum / count) of every code rounded to the input type, in octets
+// of 8 codes laid out as the attention kernel's MFMA operands, [octet][d][8],
+// with n and ln n per code.
 #include "avq_common.hpp"
+#include "avq_packed.hpp"
 
 namespace avq {
 
@@ -53,7 +55,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
                                                                 const int32_t* __restrict__ code_idx,
                                                                 float* __restrict__ Vbar,
                                                                 int32_t* __restrict__ counts,
-                                                                T* __restrict__ Vmean, int N,
+                                                                unsigned char* __restrict__ packed, int N,
                                                                 int M0, int Ch, int F,
                                                                 int ranges) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
@@ -215,13 +217,18 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   }
 
   // 2. parent row = stay + children; write every row once, and the counts.
-  //    Packed means (Vmean, optional): the owner writes its children's groups
-  //    of 4 directly; the parents' groups (4 parents from 4 owners) are put
+  //    Packed aggregates (optional): the owner writes its children's octets
+  //    directly; the parents' octets (8 parents from 8 owners) are put
   //    together through LDS (the queue area is free now).
-  const int PG = (M0 + 3) / 4, CG = (Ch + 3) / 4;
+  const PackedLayout PL = packed_layout(M0, Ch, D, (int)sizeof(T));
   float* pmean = reinterpret_cast<float*>(L.qkey);  // [kQuarters][D]
+  int* pcell = reinterpret_cast<int*>(L.skey);      // [kQuarters] cell sizes
   float* vb = Vbar ? Vbar + (size_t)bh * Mtot * D : nullptr;
-  T* vm = Vmean ? Vmean + (size_t)bh * (PG + (size_t)M0 * CG) * 4 * D : nullptr;
+  unsigned char* pk = packed ? packed + (size_t)bh * PL.bytes : nullptr;
+  T* means = reinterpret_cast<T*>(pk);
+  float* info = reinterpret_cast<float*>(pk + PL.info_off);
+  constexpr float kNegInf = -__builtin_inff();
+  constexpr float kLn2 = 0.6931471805599453f;
   if (quarter < nfam) {
     const int p = p0 + quarter;
     const int* tot = &L.total[quarter * (1 + Ch)];
@@ -250,60 +257,88 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       for (int i = 0; i < CPL; i += 4)
         dst[i / 4] = float4{par[i], par[i + 1], par[i + 2], par[i + 3]};
     }
-    if (vm) {
+    if (pk) {
       const float pinv = ncell > 0 ? 1.f / (float)ncell : 0.f;
 #pragma unroll
       for (int i = 0; i < CPL; ++i) pmean[quarter * D + sub * CPL + i] = par[i] * pinv;
-      // children groups of this parent: [CG][D][4]
-      T* cg = vm + ((size_t)PG + (size_t)p * CG) * 4 * D;
-      for (int k = 0; k < CG; ++k) {
-        float inv[4];
+      if (sub == 0) pcell[quarter] = ncell;
+      // this parent's child octets: [CO][D][8], and their info
 #pragma unroll
-        for (int sl = 0; sl < 4; ++sl) {
-          const int c = 4 * k + sl;
+      for (int j = 0; j < (kChMax + 7) / 8; ++j) {
+        if (j < PL.CO) {
+          const int o = PL.PO + p * PL.CO + j;
+          float inv[8];
+#pragma unroll
+          for (int sl = 0; sl < 8; ++sl) {
+            const int c = 8 * j + sl;
+            const int n = c < Ch ? tot[1 + c] : 0;
+            inv[sl] = n > 0 ? 1.f / (float)n : 0.f;
+          }
+#pragma unroll
+          for (int i = 0; i < CPL; ++i) {
+            float v[8];
+#pragma unroll
+            for (int sl = 0; sl < 8; ++sl) {
+              float a = 0.f;
+#pragma unroll
+              for (int r = 1; r <= kChMax; ++r)
+                if (r == 1 + 8 * j + sl) a = acc[r][i];
+              v[sl] = a * inv[sl];
+            }
+            T* dst = means + ((size_t)o * D + sub * CPL + i) * 8;
+            if constexpr (Elem<T>::kBf16) {
+              bf16x8 w = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
+                          (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+              *reinterpret_cast<bf16x8*>(dst) = w;
+            } else {
+              reinterpret_cast<float4*>(dst)[0] = float4{v[0], v[1], v[2], v[3]};
+              reinterpret_cast<float4*>(dst)[1] = float4{v[4], v[5], v[6], v[7]};
+            }
+          }
+          // lane sub writes info slot sub: n (slots 0..7), ln n (slots 8..15)
+          const int c = 8 * j + (sub & 7);
           const int n = c < Ch ? tot[1 + c] : 0;
-          inv[sl] = n > 0 ? 1.f / (float)n : 0.f;
-        }
-#pragma unroll
-        for (int i = 0; i < CPL; ++i) {
-          float v[4];
-#pragma unroll
-          for (int sl = 0; sl < 4; ++sl) {
-            float a = 0.f;
-#pragma unroll
-            for (int r = 1; r <= kChMax; ++r)
-              if (r == 1 + 4 * k + sl) a = acc[r][i];
-            v[sl] = a * inv[sl];
-          }
-          T* row = cg + ((size_t)k * D + sub * CPL + i) * 4;
-          if constexpr (Elem<T>::kBf16) {
-            bf16x4 o = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
-            *reinterpret_cast<bf16x4*>(row) = o;
-          } else {
-            *reinterpret_cast<float4*>(row) = float4{v[0], v[1], v[2], v[3]};
-          }
+          info[(size_t)o * 16 + sub] =
+              sub < 8 ? (float)n : (n > 0 ? log2_hw((float)n) * kLn2 : kNegInf);
         }
       }
     }
   }
   __syncthreads();
-  if (vm) {  // parents' groups [D][4] of this range
-    const int ngroups = (nfam + 3) / 4;
-    for (int i = tid; i < ngroups * D; i += kAggThreads) {
-      const int gi = i / D, d = i % D;
-      float v[4];
+  if (pk) {
+    // the parent octets of this range (the last range also writes the
+    // padding octets, the first one the empty octet)
+    const int o_begin = p0 / 8;
+    const int o_end = (p0 + nfam >= M0) ? PL.PO : (p0 + nfam) / 8;
+    const int nrow = (o_end - o_begin) * D;
+    for (int i = tid; i < nrow; i += kAggThreads) {
+      const int o = o_begin + i / D, d = i % D;
+      float v[8];
 #pragma unroll
-      for (int sl = 0; sl < 4; ++sl) {
-        const int q = 4 * gi + sl;
+      for (int sl = 0; sl < 8; ++sl) {
+        const int q = 8 * o + sl - p0;
         v[sl] = q < nfam ? pmean[q * D + d] : 0.f;
       }
-      T* row = vm + ((size_t)(p0 / 4 + gi) * D + d) * 4;
+      T* dst = means + ((size_t)o * D + d) * 8;
       if constexpr (Elem<T>::kBf16) {
-        bf16x4 o = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
-        *reinterpret_cast<bf16x4*>(row) = o;
+        bf16x8 w = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
+                    (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+        *reinterpret_cast<bf16x8*>(dst) = w;
       } else {
-        *reinterpret_cast<float4*>(row) = float4{v[0], v[1], v[2], v[3]};
+        reinterpret_cast<float4*>(dst)[0] = float4{v[0], v[1], v[2], v[3]};
+        reinterpret_cast<float4*>(dst)[1] = float4{v[4], v[5], v[6], v[7]};
       }
+    }
+    for (int i = tid; i < (o_end - o_begin) * 16; i += kAggThreads) {
+      const int o = o_begin + i / 16, sl = i % 16;
+      const int q = 8 * o + (sl & 7) - p0;
+      const int n = q < nfam ? pcell[q] : 0;
+      info[(size_t)o * 16 + sl] =
+          sl < 8 ? (float)n : (n > 0 ? log2_hw((float)n) * kLn2 : kNegInf);
+    }
+    if (p0 == 0) {  // the empty octet
+      for (int i = tid; i < D * 8; i += kAggThreads) means[(size_t)PL.zero_oct * D * 8 + i] = T(0.f);
+      if (tid < 16) info[(size_t)PL.zero_oct * 16 + tid] = tid < 8 ? 0.f : kNegInf;
     }
   }
   int32_t* nb = counts + (size_t)bh * Mtot;
@@ -319,18 +354,17 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
 template <typename T, int D>
 hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
                               const int32_t* code_idx, float* Vbar, int32_t* counts,
-                              void* Vmean, hipStream_t stream) {
+                              void* packed, hipStream_t stream) {
   DeviceInfo info;
   hipError_t e = device_info(&info);
   if (e != hipSuccess) return e;
   if (Ch > kChMax) return hipErrorInvalidValue;
   // families per workgroup: one per quarter wave, fewer while that leaves
   // fewer workgroups than CUs. Every range but the last starts at a multiple
-  // of 4 parents, so that each packed group of 4 parent means is written by
-  // one workgroup: F stays a multiple of 4 whenever there is more than one
-  // range.
+  // of 8 parents, so that each packed octet of parent means is written by one
+  // workgroup: F stays a multiple of 8 whenever there is more than one range.
   int F = kQuarters < M0 ? kQuarters : M0;
-  while (F > 8 && F % 8 == 0 && (long long)BH * ((M0 + F - 1) / F) < info.cus) F /= 2;
+  while (F > 8 && F % 16 == 0 && (long long)BH * ((M0 + F - 1) / F) < info.cus) F /= 2;
   const int ranges = (M0 + F - 1) / F;
   const int lds = (int)sizeof(AggLds);
   e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D>, lds,
@@ -340,18 +374,18 @@ hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((aggregate_kernel<T, D>), dim3((unsigned)grid), dim3(kAggThreads), lds,
                      stream, static_cast<const T*>(V), code_idx, Vbar, counts,
-                     static_cast<T*>(Vmean), N, M0, Ch, F, ranges);
+                     static_cast<unsigned char*>(packed), N, M0, Ch, F, ranges);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
-                            const int32_t* code_idx, float* Vbar, int32_t* counts, void* Vmean,
+                            const int32_t* code_idx, float* Vbar, int32_t* counts, void* packed,
                             hipStream_t stream) {
   if (d == 64)
-    return launch_aggregate_d<T, 64>(BH, N, M0, Ch, V, code_idx, Vbar, counts, Vmean, stream);
+    return launch_aggregate_d<T, 64>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
   if (d == 128)
-    return launch_aggregate_d<T, 128>(BH, N, M0, Ch, V, code_idx, Vbar, counts, Vmean, stream);
+    return launch_aggregate_d<T, 128>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
   return hipErrorInvalidValue;
 }
 

@@ -8,6 +8,7 @@
 
 #include "../../include/avq.h"
 #include "avq_common.hpp"
+#include "avq_packed.hpp"
 
 namespace avq {
 template <typename T, int D>
@@ -16,12 +17,12 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
                          hipStream_t stream);
 template <typename T>
 hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
-                            const int32_t* code_idx, float* Vbar, int32_t* counts, void* Vmean,
+                            const int32_t* code_idx, float* Vbar, int32_t* counts, void* packed,
                             hipStream_t stream);
 template <typename T, int D>
 hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
-                            const void* Q, const void* Cp, const void* Cc, const void* Vmean,
-                            const int32_t* counts, void* Y, int32_t* topp_idx,
+                            const void* Q, const void* Cp, const void* Cc, const void* packed,
+                            void* Y, int32_t* topp_idx,
                             float* importance, hipStream_t stream);
 }  // namespace avq
 
@@ -115,14 +116,14 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 extern "C" {
 
-int avq_version(void) { return 101; }
+int avq_version(void) { return 200; }
 
 const char* avq_last_error(void) { return g_err; }
 
-int64_t avq_packed_means_elems(int32_t M0, int32_t Ch, int32_t d) {
-  if (M0 < 1 || Ch < 1 || d < 1) return -1;
-  const int64_t pg = (M0 + 3) / 4, cg = (Ch + 3) / 4;
-  return (pg + (int64_t)M0 * cg) * 4 * d;
+int64_t avq_packed_bytes(avq_dtype_t dtype, int32_t M0, int32_t Ch, int32_t d) {
+  if (dtype != AVQ_F32 && dtype != AVQ_BF16) return -1;
+  if (M0 < 1 || Ch < 1 || d < 1 || M0 > 512 || Ch > 16 || d > 128) return -1;
+  return (int64_t)avq::packed_layout(M0, Ch, d, dtype == AVQ_BF16 ? 2 : 4).bytes;
 }
 
 avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
@@ -149,53 +150,53 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
 
 avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
                            int32_t M0, int32_t Ch, const void* V, const int32_t* code_idx,
-                           float* Vbar, int32_t* counts, void* Vmean, void* stream) {
+                           float* Vbar, int32_t* counts, void* packed, void* stream) {
   avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
   if (st != AVQ_OK) return st;
   if (!V || !code_idx || !counts)
     return fail(AVQ_ERR_INVALID_ARG, "avq_aggregate: null pointer argument");
-  if (!Vbar && !Vmean)
-    return fail(AVQ_ERR_INVALID_ARG, "avq_aggregate: Vbar and Vmean are both null");
+  if (!Vbar && !packed)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_aggregate: Vbar and packed are both null");
   if (!aligned16(V) || !aligned16(code_idx) || !aligned16(Vbar) || !aligned16(counts) ||
-      !aligned16(Vmean))
+      !aligned16(packed))
     return fail(AVQ_ERR_INVALID_ARG, "avq_aggregate: arrays must be 16-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int BH = B * H;
   hipError_t e =
       dtype == AVQ_BF16
-          ? avq::launch_aggregate<avq::bf16>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, Vmean, s)
-          : avq::launch_aggregate<float>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, Vmean, s);
+          ? avq::launch_aggregate<avq::bf16>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, s)
+          : avq::launch_aggregate<float>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, s);
   return from_hip(e, "avq_aggregate launch");
 }
 
 avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
                                int32_t M0, int32_t Ch, int32_t P, int32_t block_q,
                                const void* Q, const void* Cp, const void* Cc,
-                               const void* Vmean, const int32_t* counts, void* Y,
+                               const void* packed, void* Y,
                                int32_t* topp_idx, float* importance, void* stream) {
   avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
   if (st != AVQ_OK) return st;
   if (P < 0 || P > M0) return fail(AVQ_ERR_INVALID_ARG, "P=%d outside [0, M0=%d]", P, M0);
   if (block_q < 1) return fail(AVQ_ERR_INVALID_ARG, "block_q=%d must be positive", block_q);
   if (block_q > 256) return fail(AVQ_ERR_UNSUPPORTED, "block_q=%d: at most 256", block_q);
-  if (!Q || !Cp || !Cc || !Vmean || !counts || !Y)
+  if (!Q || !Cp || !Cc || !packed || !Y)
     return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: null pointer argument");
-  if (!aligned16(Q) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(Vmean) ||
-      !aligned16(counts) || !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance))
+  if (!aligned16(Q) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(packed) ||
+      !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance))
     return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: arrays must be 16-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int BH = B * H;
   hipError_t e;
   if (dtype == AVQ_BF16)
-    e = d == 64 ? avq::launch_attention<avq::bf16, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vmean,
-                                                       counts, Y, topp_idx, importance, s)
-                : avq::launch_attention<avq::bf16, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vmean,
-                                                        counts, Y, topp_idx, importance, s);
+    e = d == 64 ? avq::launch_attention<avq::bf16, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
+                                                       Y, topp_idx, importance, s)
+                : avq::launch_attention<avq::bf16, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
+                                                        Y, topp_idx, importance, s);
   else
-    e = d == 64 ? avq::launch_attention<float, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vmean,
-                                                   counts, Y, topp_idx, importance, s)
-                : avq::launch_attention<float, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, Vmean,
-                                                    counts, Y, topp_idx, importance, s);
+    e = d == 64 ? avq::launch_attention<float, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
+                                                   Y, topp_idx, importance, s)
+                : avq::launch_attention<float, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
+                                                    Y, topp_idx, importance, s);
   return from_hip(e, "avq_attention_fwd launch");
 }
 

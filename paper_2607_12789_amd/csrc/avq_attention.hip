@@ -2,47 +2,56 @@
 //
 // One workgroup processes one query tile (block_q consecutive tokens of one
 // (batch, head)); each wave owns 32 query rows. Everything is computed
-// transposed, codewords x queries: S^T = C . Q^T and Xbar^T = Vmean^T . W^T.
-// With the 16x16 MFMA layouts a lane owns one query column and four
-// consecutive codeword rows, so
-//   - the weights that come out of exp2() are already in the register layout
-//     of the MFMA operand of the next product (no shuffles);
-//   - the Ch children of one parent sit in one lane's consecutive rows (plus
-//     the partner lane groups for Ch = 8, 16): the recovered parent logit of
-//     Eq. (parent_recovery) is an in-register sum;
+// transposed, codewords x queries: S^T = C . Q^T and Xbar^T = Vmean^T . W^T,
+// with 16x16x32 bf16 (16x16x4 fp32) MFMA. A lane owns one query column and,
+// in a pair of 16-row logit tiles, 8 consecutive codes (one octet of the
+// packed aggregates): the 16 rows of tile tt are chunk rows
+// 32 (tt/2) + 8 g + 4 (tt%2) + r for lane group g and r = 0..3. So
+//   - the weights that come out of exp2() are already the B operand of the
+//     value product, and its A operand, the 8 mean values of the octet at one
+//     column, is one 16-byte LDS read;
+//   - the 8 children of a parent (Ch = 8) are one lane's 8 values: the
+//     recovered parent logit of Eq. (parent_recovery) is an in-register sum
+//     (Ch = 16: plus one cross-lane-group exchange);
 //   - per-query softmax state is per lane.
 //
-// Log-count bias (App. D): a codeword's logit enters as
-// t = S log2(e) + log2(n), so its weight exp2(t - m) is n exp(S - m'); empty
-// codewords get t = -inf and drop out of the running max and of every sum
-// without masks. The values are the means Vbar/n written by the aggregation
-// (groups of 4 codes, [d][4]), so sum_j n_j exp(S_j - m') Vbar_j / n_j is the
-// numerator of Eq. (vqflashattention). The parent logit recovered from the
-// children uses the unbiased child logits, and the correcting weight of child
-// c is n_c (exp(T_c - m') - exp(Srec - m')), Eq. (correcting_attention) times
-// n_c. The denominator (the sum of the weights) comes out of the value MFMA
-// through one extra d-tile whose first row is all ones, so numerator and
-// denominator use the same rounded weights.
+// Log-count bias (App. D): a parent's logit enters as t = S + ln n (the MFMA
+// accumulator starts at ln n), so its weight exp(t - m) is n exp(S - m) and an
+// empty parent (ln n = -inf) drops out of the max and of every sum without
+// masks. It is applied to the parent's mean value Vbar/n, so
+// sum_p n_p exp(S_p - m) Vbar_p / n_p is the numerator of
+// Eq. (vqflashattention). The children keep their raw logits (the recovered
+// parent logit needs them) and their correcting weight is
+// n_c (exp(T_c - m) - exp(Srec - m)), Eq. (correcting_attention) times n_c,
+// which is zero for empty children and padding rows (n = 0). The denominator
+// comes out of the value MFMA through one extra d-tile whose first row is all
+// ones, so numerator and denominator use the same rounded weights.
 //
-// Codewords stream through LDS in chunks of CW rows, copied by direct
-// global->LDS loads (no registers, no VALU): codeword rows XOR-swizzled by
-// 16-byte unit so that the 16 lanes reading 16 rows hit different banks, and
-// the packed mean values as they lie in memory. Phases per tile:
-//   1. parent sweep: per chunk, logits, running max, weights, fp32 parent
-//      denominator, Xbar += Vmean^T W (online softmax);
+// Running max (in log2 units): it only moves when a chunk's logits exceed it
+// by more than kLazy, so the rescaling of the accumulators and the reduction
+// of the chunk max across lanes are rare; weights stay below 2^kLazy, far
+// inside fp32 and bf16 range, and the result does not depend on the shift.
+//
+// Codewords stream through LDS in chunks of 64 rows (8 octets): codeword rows
+// XOR-swizzled by 16-byte unit (the 16 rows of a logit tile hit different
+// banks), packed mean octets and their count info as they lie in HBM, all by
+// direct global->LDS loads (no registers, no VALU), double buffered: the next
+// chunk is in flight while the current one is computed. Phases per tile:
+//   1. parent sweep: logits, running max, weights, fp32 parent denominator,
+//      Xbar += Vmean^T W;
 //   2. importance (Eq. (importance)) with the final max and denominator: a
-//      second sweep recomputes the parent logits chunk by chunk (or reuses
-//      them when all parents fit one chunk) and sums W_ip / Z_i over the
-//      tile's queries (a reduce-scatter butterfly over lanes, then a fixed
-//      order over waves);
+//      second sweep recomputes the parent logits (or reuses them when all
+//      parents fit one chunk) and takes exp(t - m - ln Z) directly; sums over
+//      the tile's queries by a reduce-scatter butterfly over lanes, then a
+//      fixed order over waves;
 //   3. top-P: histogram of the importance exponents finds the bin holding
 //      the P-th largest value; exact ranks (w desc, index asc) inside that bin
 //      decide the rest; the selected parents are listed in index order;
-//   4. child sweep over the selected parents' children, chunk by chunk:
-//      logits, running max raised (Xbar rescaled), recovered parent logit,
-//      correcting weights, Xbar += Vmean^T dW;
+//   4. child sweep over the child octets of the selected parents: logits,
+//      recovered parent logit, correcting weights, Xbar += Vmean^T dW;
 //   5. Y = Xbar / Z.
 #include "avq_common.hpp"
+#include "avq_packed.hpp"
 
 #include <type_traits>
 
@@ -61,32 +70,39 @@ struct AttnCfg {
   static constexpr int ESZ = sizeof(T);
   static constexpr int EPU = 16 / ESZ;            // elements per 16-byte unit
   static constexpr int U = D * ESZ / 16;          // 16-byte units per codeword row
-  static constexpr int RB = (256 / (D * ESZ)) > 1 ? 256 / (D * ESZ) : 1;  // rows per 256 B
+  static constexpr int COPIES = CW * U / 64;      // wave copies per array per chunk
+  static constexpr int CPW = COPIES / MAXW;       // ... per wave
+  static constexpr int OCT_ELEMS = 8 * D;         // elements of one mean octet
+  static constexpr int OCPY = OCT_ELEMS * ESZ / 1024;  // wave copies per mean octet
   static constexpr int M0MAX = 512;
-  static constexpr int kWavesPerEu = (kB && D == 64 && MAXW == 4) ? 3 : 2;
-  static constexpr int CHUNK_BYTES = CW * D * ESZ;  // codeword rows (= packed means)
-  // dynamic LDS layout (bytes)
-  static constexpr size_t OFF_C = 0;
-  static constexpr size_t OFF_V = OFF_C + CHUNK_BYTES;
-  static constexpr size_t OFF_N = OFF_V + CHUNK_BYTES;                // [CW] f32 n
-  static constexpr size_t OFF_L = OFF_N + CW * 4;                     // [CW] f32 log2 n
-  static constexpr size_t OFF_W = OFF_L + CW * 4;                     // [MAXW][M0MAX] f32
-  static constexpr size_t OFF_WF = OFF_W + (size_t)MAXW * M0MAX * 4;  // [M0MAX] f32
-  static constexpr size_t OFF_SEL = OFF_WF + M0MAX * 4;               // [M0MAX] i32
-  static constexpr size_t OFF_FLAG = OFF_SEL + M0MAX * 4;             // [M0MAX] i32
-  static constexpr size_t OFF_HIST = OFF_FLAG + M0MAX * 4;            // [256] i32
-  static constexpr size_t OFF_MISC = OFF_HIST + 256 * 4;              // [4] i32
+  static constexpr int CHUNK_BYTES = CW * D * ESZ;
+  // one chunk buffer: codeword rows, mean octets, count info
+  static constexpr int OFF_C = 0;
+  static constexpr int OFF_V = CHUNK_BYTES;
+  static constexpr int OFF_I = 2 * CHUNK_BYTES;
+  static constexpr int BUF_BYTES = 2 * CHUNK_BYTES + 8 * 64;
+  static constexpr int NBUF = 2 * BUF_BYTES <= 72 * 1024 ? 2 : 1;
+  // after the buffers
+  static constexpr size_t OFF_LW = (size_t)NBUF * BUF_BYTES;    // [2][MAXW][CW] f32
+  static constexpr size_t OFF_WF = OFF_LW + 2 * MAXW * CW * 4;  // [M0MAX] f32
+  static constexpr size_t OFF_SEL = OFF_WF + M0MAX * 4;         // [M0MAX] i32
+  static constexpr size_t OFF_MISC = OFF_SEL + M0MAX * 4;       // [4] i32
   static constexpr size_t LDS_BYTES = OFF_MISC + 16;
-  static_assert(CHUNK_BYTES % 1024 == 0, "a chunk is a whole number of wave copies");
-  static_assert(TPC * 4 == 16, "importance butterfly takes 16 codewords per lane");
+  // top-P scratch in buffer 0 (no chunk is in flight during top-P)
+  static constexpr int OFF_FLAG = 0;                   // [M0MAX] i32
+  static constexpr int OFF_HIST = M0MAX * 4;           // [256] i32
+  static constexpr int OFF_BMEM = OFF_HIST + 256 * 4;  // [M0MAX] i32
+  static constexpr int kWavesPerEu = (kB && D == 64) ? 3 : 2;
+  static_assert(COPIES % MAXW == 0 && CPW >= 1, "copies split evenly over the waves");
+  static_assert(OCPY >= 1 && (OCPY & (OCPY - 1)) == 0, "whole wave copies per octet");
+  static_assert(OFF_BMEM + M0MAX * 4 <= BUF_BYTES, "top-P scratch fits one buffer");
 };
 
 struct AttnArgs {
   const void* Q;
   const void* Cp;
   const void* Cc;
-  const void* Vmean;
-  const int32_t* counts;
+  const unsigned char* packed;
   void* Y;
   int32_t* topp_idx;
   float* importance;
@@ -100,9 +116,17 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, void* lds) {
                                    (void __attribute__((address_space(3)))*)lds, 16, 0, 0);
 }
 
+// XOR swizzle of the 16-byte units of a staged codeword row: the 16 rows a
+// logit tile reads (8 (c/4) + 4 h + c % 4 for lanes c) get distinct units for
+// the same logical unit, so 16 lanes reading one unit each hit distinct banks.
+template <int U>
+__device__ __forceinline__ int row_swizzle(int r) {
+  if constexpr (U >= 16) return ((r >> 3) & 3) * 4 + (r & 3);
+  return ((r >> 3) & 3) * 2 + ((r >> 1) & 1);  // U = 8: two rows per 256 bytes
+}
+
 // Register budget: two or three waves per SIMD (at most 256 or 168 registers
-// each), so that other tiles' MFMA work runs while one workgroup waits for
-// its chunk to arrive.
+// each), so that other tiles' MFMA work runs while one workgroup waits.
 template <typename T, int D, int MAXW>
 __global__ __launch_bounds__(MAXW * 64)
 __attribute__((amdgpu_waves_per_eu(AttnCfg<T, D, MAXW>::kWavesPerEu)))
@@ -110,31 +134,30 @@ void attention_kernel(AttnArgs args) {
   using Cfg = AttnCfg<T, D, MAXW>;
   constexpr bool kB = Cfg::kB;
   constexpr int QS = Cfg::QS, CW = Cfg::CW, TPC = Cfg::TPC, KQ = Cfg::KQ, DT = Cfg::DT,
-                XT = Cfg::XT, U = Cfg::U, EPU = Cfg::EPU, RB = Cfg::RB, M0MAX = Cfg::M0MAX;
+                XT = Cfg::XT, U = Cfg::U, EPU = Cfg::EPU, CPW = Cfg::CPW,
+                OCPY = Cfg::OCPY, OCT_ELEMS = Cfg::OCT_ELEMS;
   using QFrag = typename std::conditional<kB, bf16x8, float>::type;
-  constexpr float kNegInf = -__builtin_inff();
+  constexpr float kLn2 = 0.6931471805599453f;
+  constexpr float kLazy = 8.f;         // log2 units the max may lag behind
+  constexpr float kMaxFloor = -1e30f;  // finite start of the running max
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
-  T* lc = reinterpret_cast<T*>(lds_raw + Cfg::OFF_C);            // codeword rows (swizzled)
-  T* lv = reinterpret_cast<T*>(lds_raw + Cfg::OFF_V);            // mean values [CW/4][D][4]
-  float* ln = reinterpret_cast<float*>(lds_raw + Cfg::OFF_N);    // counts of the rows
-  float* ll = reinterpret_cast<float*>(lds_raw + Cfg::OFF_L);    // log2 of the counts
-  float* lw = reinterpret_cast<float*>(lds_raw + Cfg::OFF_W);    // per-wave importance
+  float* lw = reinterpret_cast<float*>(lds_raw + Cfg::OFF_LW);   // per-wave importance
   float* lwf = reinterpret_cast<float*>(lds_raw + Cfg::OFF_WF);  // importance
   int* lsel = reinterpret_cast<int*>(lds_raw + Cfg::OFF_SEL);    // selected, index order
-  int* lflag = reinterpret_cast<int*>(lds_raw + Cfg::OFF_FLAG);  // selected flags
-  int* lhist = reinterpret_cast<int*>(lds_raw + Cfg::OFF_HIST);  // exponent histogram
   int* lmisc = reinterpret_cast<int*>(lds_raw + Cfg::OFF_MISC);
+  int* lflag = reinterpret_cast<int*>(lds_raw + Cfg::OFF_FLAG);  // top-P only
+  int* lhist = reinterpret_cast<int*>(lds_raw + Cfg::OFF_HIST);
+  int* bmem = reinterpret_cast<int*>(lds_raw + Cfg::OFF_BMEM);
 
   const T* __restrict__ Q = static_cast<const T*>(args.Q);
   const T* __restrict__ Cp = static_cast<const T*>(args.Cp);
   const T* __restrict__ Cc = static_cast<const T*>(args.Cc);
-  const int32_t* __restrict__ counts = args.counts;
   const int N = args.N, M0 = args.M0, Ch = args.Ch, P = args.P;
-  const int Mtot = M0 * (1 + Ch);
-  const int PG = (M0 + 3) / 4, CG = (Ch + 3) / 4, PS = 4 * CG;  // groups; rows per parent
+  const PackedLayout PL = packed_layout(M0, Ch, D, Cfg::ESZ);
+  const int PO = PL.PO, CO = PL.CO, ZO = PL.zero_oct;
 
-  const int tid = threadIdx.x, nthr = blockDim.x, nwaves = nthr / kWave;
+  const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
   const int g = lane / 16, c = lane % 16;
   const int tile = xcd_remap(blockIdx.x, gridDim.x);
@@ -143,10 +166,11 @@ void attention_kernel(AttnArgs args) {
   const int q_begin = t * args.block_q;
   const int q_end = min(q_begin + args.block_q, N);
   const int row0 = q_begin + wave * Cfg::RPW;
-  const T* vm_par =
-      static_cast<const T*>(args.Vmean) + (size_t)bh * (PG + (size_t)M0 * CG) * 4 * D;
-  const T* vm_child = vm_par + (size_t)PG * 4 * D;
-  const int32_t* cb = counts + (size_t)bh * Mtot;
+  const bool has_rows = row0 < q_end;                                 // wave-uniform
+  const int n_active = (q_end - q_begin + Cfg::RPW - 1) / Cfg::RPW;  // waves with rows
+  const unsigned char* pk = args.packed + (size_t)bh * PL.bytes;
+  const T* means = reinterpret_cast<const T*>(pk);
+  const float* info = reinterpret_cast<const float*>(pk + PL.info_off);
   const T* cp_head = Cp + (size_t)h * M0 * D;
   const T* cc_head = Cc + (size_t)h * M0 * Ch * D;
 
@@ -171,61 +195,88 @@ void attention_kernel(AttnArgs args) {
   }
 
   // ---- chunk staging --------------------------------------------------------
-  // Codeword row r of the chunk holds its 16-byte unit u at unit u ^ swz(r).
-  auto swz = [](int r) { return (r / RB) % U; };
-  // stage(crow, vgroup, count, with_values): crow(r) = codebook row of chunk
-  // row r (any valid row for padding), vgroup(k) = first element of the packed
-  // means of chunk group k (rows 4k .. 4k+3), count(r) = n of chunk row r
-  // (0 for padding).
-  auto stage = [&](auto crow, auto vgroup, auto count, bool with_values) {
-    constexpr int COPIES = CW * U / 64;  // wave copies per array
-    for (int j = wave; j < COPIES; j += nwaves) {
-      const int q = 64 * j + lane;
-      const int r = q / U, pu = q % U;
-      copy16_to_lds(crow(r) + (pu ^ swz(r)) * EPU, lds_raw + Cfg::OFF_C + 1024 * j);
+  // Copy i of this wave is wave copy j = wave + MAXW i of each array. For the
+  // codeword rows it covers chunk rows (64 j + lane) / U; their octet
+  // (row / 8) is the same for the whole wave copy.
+  int crow[CPW], ccol[CPW];
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int q = 64 * (wave + MAXW * i) + lane;
+    crow[i] = q / U;
+    ccol[i] = ((q % U) ^ row_swizzle<U>(q / U)) * EPU;
+  }
+  auto buffer = [&](int b) { return lds_raw + b * Cfg::BUF_BYTES; };
+  // octet_of(os): packed octet index of chunk octet os; row_of(os, r8):
+  // codebook row of row r8 (0..7) of chunk octet os.
+  auto issue = [&](unsigned char* B, bool with_values, auto octet_of, auto row_of) {
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int j = wave + MAXW * i;
+      copy16_to_lds(row_of(crow[i] / 8, crow[i] % 8) + ccol[i], B + Cfg::OFF_C + 1024 * j);
     }
     if (with_values) {
-      constexpr int UPG = D * 4 * Cfg::ESZ / 16;  // 16-byte units per group
-      for (int j = wave; j < COPIES; j += nwaves) {
-        const int q = 64 * j + lane;
-        copy16_to_lds(vgroup(q / UPG) + (q % UPG) * EPU, lds_raw + Cfg::OFF_V + 1024 * j);
+#pragma unroll
+      for (int i = 0; i < CPW; ++i) {
+        const int j = wave + MAXW * i;
+        const T* src = means + (size_t)octet_of(j / OCPY) * OCT_ELEMS +
+                       (j % OCPY) * 64 * EPU + lane * EPU;
+        copy16_to_lds(src, B + Cfg::OFF_V + 1024 * j);
       }
     }
-    for (int r = tid; r < CW; r += nthr) {
-      const float n = (float)count(r);
-      ln[r] = n;
-      ll[r] = n > 0.f ? log2_hw(n) : kNegInf;
-    }
+    if (wave == MAXW - 1 && lane < 32)  // 8 octets x 64 bytes of count info
+      copy16_to_lds(info + (size_t)octet_of(lane / 4) * 16 + (lane % 4) * 4, B + Cfg::OFF_I);
+  };
+  auto issue_parent = [&](int k, unsigned char* B, bool with_values) {
+    issue(
+        B, with_values, [&](int os) { return 8 * k + os; },
+        [&](int os, int r8) { return cp_head + (size_t)min(64 * k + 8 * os + r8, M0 - 1) * D; });
+  };
+  // child octet o belongs to selected parent o >> co_shift (CO is 1 or 2)
+  const int n_child_oct = Ch > 1 ? P * CO : 0;
+  const int co_shift = CO == 2 ? 1 : 0;
+  auto issue_child = [&](int k, unsigned char* B) {
+    issue(
+        B, true,
+        [&](int os) {
+          const int o = 8 * k + os;
+          if (o >= n_child_oct) return ZO;
+          const int sl = o >> co_shift;
+          return PO + (lsel[sl] << co_shift) + (o - (sl << co_shift));
+        },
+        [&](int os, int r8) {
+          const int o = min(8 * k + os, n_child_oct - 1);
+          const int sl = o >> co_shift;
+          const int cc = min((o - (sl << co_shift)) * 8 + r8, Ch - 1);
+          return cc_head + ((size_t)lsel[sl] * Ch + cc) * D;
+        });
+  };
+  auto wait_chunk = [&]() {
     __builtin_amdgcn_s_waitcnt(0);
-  };
-  auto parent_crow = [=](int cbase) {
-    return [=](int r) { return cp_head + (size_t)min(cbase + r, M0 - 1) * D; };
-  };
-  auto parent_vgroup = [=](int cbase) {
-    return [=](int k) { return vm_par + (size_t)min(cbase / 4 + k, PG - 1) * 4 * D; };
-  };
-  auto parent_count = [=](int cbase) {
-    return [=](int r) { return cbase + r < M0 ? cb[cbase + r] : 0; };
+    __syncthreads();
   };
 
   // ---- S^T tile (16 codewords x 16 queries) for chunk tile tt ----------------
-  auto logits = [&](int tt, f32x4 (&out)[QS]) {
-    const int r = 16 * tt + c;
-#pragma unroll
-    for (int s = 0; s < QS; ++s) out[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto logits = [&](const unsigned char* B, int tt, f32x4 (&out)[QS], const f32x4& init) {
+    const T* lc = reinterpret_cast<const T*>(B + Cfg::OFF_C);
+    const int r = 32 * (tt / 2) + 8 * (c / 4) + 4 * (tt % 2) + (c % 4);
+    const int sw = row_swizzle<U>(r);
 #pragma unroll
     for (int kq = 0; kq < KQ; ++kq) {
       if constexpr (kB) {
-        const int u = 4 * kq + g;
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lc[r * D + (u ^ swz(r)) * EPU]);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
 #pragma unroll
-        for (int s = 0; s < QS; ++s) out[s] = mfma_bf16(a, qf[s][kq], out[s]);
+        for (int s = 0; s < QS; ++s) out[s] = mfma_bf16(a, qf[s][kq], kq == 0 ? init : out[s]);
       } else {
-        const float a = lc[r * D + (kq ^ swz(r)) * EPU + g];
+        const float a = lc[r * D + (kq ^ sw) * EPU + g];
 #pragma unroll
-        for (int s = 0; s < QS; ++s) out[s] = mfma_f32(a, qf[s][kq], out[s]);
+        for (int s = 0; s < QS; ++s) out[s] = mfma_f32(a, qf[s][kq], kq == 0 ? init : out[s]);
       }
     }
+  };
+  // count info of the lane's 4 rows in tile tt: n (part 0) or ln n (part 1)
+  auto info4 = [&](const unsigned char* B, int tt, int part) {
+    const float* li = reinterpret_cast<const float*>(B + Cfg::OFF_I);
+    return *reinterpret_cast<const f32x4*>(&li[(4 * (tt / 2) + g) * 16 + 8 * part + 4 * (tt % 2)]);
   };
 
   // ---- Xbar^T += Vmean^T . W^T; the extra tile DT has an all-ones first row
@@ -235,40 +286,40 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
     for (int s = 0; s < QS; ++s) X[dt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // bf16: the weights of chunk tiles tt and tt+1 form one B operand; k-slots
-  // 8g .. 8g+3 are rows 4g .. 4g+3 of tile tt, 8g+4 .. 8g+7 those of tile tt+1
-  auto accumulate_b = [&](int tt, const f32x4 (&w0)[QS], const f32x4 (&w1)[QS]) {
-    bf16x8 b[QS];
+  // bf16: tiles 2b, 2b+1 form one B operand (k-slots 8 g .. 8 g + 7 = the 8
+  // codes of octet 4 b + g); the A operand is that octet at column d
+  auto accumulate_b = [&](const unsigned char* B, int b, const f32x4 (&w0)[QS],
+                          const f32x4 (&w1)[QS]) {
+    bf16x8 bw[QS];
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        b[s][r] = (bf16)w0[s][r];
-        b[s][4 + r] = (bf16)w1[s][r];
+        bw[s][r] = (bf16)w0[s][r];
+        bw[s][4 + r] = (bf16)w1[s][r];
       }
     }
-    const bf16* g0 = reinterpret_cast<const bf16*>(lv) + (4 * tt + g) * 4 * D;
-    const bf16* g1 = reinterpret_cast<const bf16*>(lv) + (4 * (tt + 1) + g) * 4 * D;
+    const bf16* oct = reinterpret_cast<const bf16*>(B + Cfg::OFF_V) + (4 * b + g) * OCT_ELEMS;
+    bf16x8 a[DT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const int d = 16 * dt + c;
-      const bf16x4 lo = *reinterpret_cast<const bf16x4*>(g0 + 4 * d);
-      const bf16x4 hi = *reinterpret_cast<const bf16x4*>(g1 + 4 * d);
-      const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    for (int dt = 0; dt < DT; ++dt) a[dt] = *reinterpret_cast<const bf16x8*>(oct + 8 * (16 * dt + c));
 #pragma unroll
-      for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(a, b[s], X[dt][s]);
-    }
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(a[dt], bw[s], X[dt][s]);
     const bf16 one = (bf16)(c == 0 ? 1.f : 0.f);
     const bf16x8 ones = {one, one, one, one, one, one, one, one};
 #pragma unroll
-    for (int s = 0; s < QS; ++s) X[DT][s] = mfma_bf16(ones, b[s], X[DT][s]);
+    for (int s = 0; s < QS; ++s) X[DT][s] = mfma_bf16(ones, bw[s], X[DT][s]);
   };
-  // fp32: the r-th product of tile tt takes row 4g + r as k-slot g
-  auto accumulate_f = [&](int tt, const f32x4 (&w0)[QS]) {
-    const float* g0 = reinterpret_cast<const float*>(lv) + (4 * tt + g) * 4 * D;
+  // fp32: the r-th product of tile tt takes row r of the lane's half octet
+  // as k-slot g
+  auto accumulate_f = [&](const unsigned char* B, int tt, const f32x4 (&w0)[QS]) {
+    const float* oct = reinterpret_cast<const float*>(B + Cfg::OFF_V) +
+                       (4 * (tt / 2) + g) * OCT_ELEMS + 4 * (tt % 2);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const float4 a = *reinterpret_cast<const float4*>(g0 + 4 * (16 * dt + c));
+      const float4 a = *reinterpret_cast<const float4*>(oct + 8 * (16 * dt + c));
 #pragma unroll
       for (int s = 0; s < QS; ++s) {
         X[dt][s] = mfma_f32(a.x, w0[s][0], X[dt][s]);
@@ -283,90 +334,159 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) X[DT][s] = mfma_f32(one, w0[s][r], X[DT][s]);
   };
-  auto accumulate_chunk = [&](const f32x4 (&W)[TPC][QS]) {
+  auto accumulate_pair = [&](const unsigned char* B, int b, const f32x4 (&W)[2][QS]) {
     if constexpr (kB) {
-#pragma unroll
-      for (int tt = 0; tt < TPC; tt += 2) accumulate_b(tt, W[tt], W[tt + 1]);
+      accumulate_b(B, b, W[0], W[1]);
     } else {
-#pragma unroll
-      for (int tt = 0; tt < TPC; ++tt) accumulate_f(tt, W[tt]);
+      accumulate_f(B, 2 * b, W[0]);
+      accumulate_f(B, 2 * b + 1, W[1]);
     }
   };
 
-  // Per-lane softmax state for query columns c + 16 s, in log2 units: m is
-  // the running max of t, started at a finite floor so that t - m stays -inf
-  // (weight 0) for empty codewords even before any non-empty one was seen.
-  // zp is this lane group's partial fp32 sum of the parent weights (for
-  // importance); the four groups are summed when needed.
-  constexpr float kMaxFloor = -1e30f;
-  float m[QS], zp[QS];
+  // Per-lane softmax state for query columns c + 16 s: m is the running max
+  // in log2 units (lagging by at most kLazy), thr the raw logit (natural
+  // units) that would pass m + kLazy, zp this lane group's partial fp32 sum of
+  // the parent weights (for importance).
+  float m[QS], thr[QS], zp[QS];
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
     m[s] = kMaxFloor;
+    thr[s] = (kMaxFloor + kLazy) * kLn2;
     zp[s] = 0.f;
   }
-  auto raise_max = [&](float (&mnew)[QS]) {
-    bool moved = false;
+  // Raises the running max if some lane's logit in the tile pair S passed the
+  // threshold, rescaling the accumulators; returns whether it moved (the same
+  // for the whole wave) and the factors applied, sc.
+  auto check_pair = [&](const f32x4 (&S)[2][QS], float (&sc)[QS]) -> bool {
+    float mx[QS];
+    bool over = false;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
-      mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 16));
-      mnew[s] = fmaxf(mnew[s], shfl_xor(mnew[s], 32));
-      moved |= mnew[s] != m[s];
+      mx[s] = S[0][s][0];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx[s] = fmaxf(mx[s], S[h2][s][r]);
+      over |= mx[s] > thr[s];
     }
-    if (__ballot(moved) == 0) return;  // wave-uniform: nothing to rescale
+    if (__ballot(over) == 0) return false;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
-      const float sc = exp2_hw(m[s] - mnew[s]);
-      zp[s] *= sc;
+      mx[s] = fmaxf(mx[s], shfl_xor(mx[s], 16));
+      mx[s] = fmaxf(mx[s], shfl_xor(mx[s], 32));
+      const float mnew = mx[s] > thr[s] ? mx[s] * kLog2e : m[s];
+      sc[s] = exp2_hw(m[s] - mnew);
+      zp[s] *= sc[s];
 #pragma unroll
-      for (int dt = 0; dt < XT; ++dt) X[dt][s] *= sc;
-      m[s] = mnew[s];
+      for (int dt = 0; dt < XT; ++dt) X[dt][s] *= sc[s];
+      m[s] = mnew;
+      thr[s] = (mnew + kLazy) * kLn2;
     }
+    return true;
   };
-  // t = S log2(e) + log2 n over the chunk
-  auto bias = [&](f32x4 (&S)[TPC][QS]) {
+  auto rescale_pair = [&](f32x4 (&W)[2][QS], const float (&sc)[QS]) {
 #pragma unroll
-    for (int tt = 0; tt < TPC; ++tt) {
-      const float4 l4 = *reinterpret_cast<const float4*>(&ll[16 * tt + 4 * g]);
+    for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-      for (int s = 0; s < QS; ++s) {
-        S[tt][s][0] = fmaf(S[tt][s][0], kLog2e, l4.x);
-        S[tt][s][1] = fmaf(S[tt][s][1], kLog2e, l4.y);
-        S[tt][s][2] = fmaf(S[tt][s][2], kLog2e, l4.z);
-        S[tt][s][3] = fmaf(S[tt][s][3], kLog2e, l4.w);
-      }
-    }
+      for (int s = 0; s < QS; ++s) W[h2][s] *= sc[s];
   };
-  auto chunk_max = [&](const f32x4 (&S)[TPC][QS], float (&mnew)[QS]) {
+  // parent weights n exp(S - m) = exp2((S + ln n) log2 e - m), in place
+  auto parent_weights = [&](f32x4 (&S)[2][QS]) {
 #pragma unroll
-    for (int s = 0; s < QS; ++s) mnew[s] = m[s];
-#pragma unroll
-    for (int tt = 0; tt < TPC; ++tt)
+    for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
       for (int s = 0; s < QS; ++s)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mnew[s] = fmaxf(mnew[s], S[tt][s][r]);
+        for (int r = 0; r < 4; ++r) {
+          const float w = exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s]));
+          S[h2][s][r] = w;
+          zp[s] += w;
+        }
+  };
+  // correcting weights n (exp(T - m) - exp(Srec - m)) of tile pair b, in
+  // place. Recovered parent logit over the octet rows: Ch = 2: rows 0-1 of the
+  // even tile (the rest is padding); Ch = 4: the 4 rows of each tile (one
+  // parent per tile); Ch = 8: the whole octet; Ch = 16: and the partner lane
+  // group's octet.
+  auto child_weights = [&](const unsigned char* B, int b, f32x4 (&S)[2][QS]) {
+    float er[2][QS];
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      const f32x4 v0 = S[0][s], v1 = S[1][s];
+      float s0, s1;
+      if (Ch == 2) {
+        s0 = v0[0] + v0[1];
+        s1 = s0;
+      } else {
+        s0 = (v0[0] + v0[1]) + (v0[2] + v0[3]);
+        s1 = (v1[0] + v1[1]) + (v1[2] + v1[3]);
+        if (Ch >= 8) {
+          s0 += s1;
+          if (Ch == 16) s0 += shfl_xor(s0, 16);
+          s1 = s0;
+        }
+      }
+      const float scale = kLog2e / (float)Ch;
+      er[0][s] = exp2_hw(fminf(fmaf(s0, scale, -m[s]), 64.f));
+      er[1][s] = exp2_hw(fminf(fmaf(s1, scale, -m[s]), 64.f));
+    }
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const f32x4 n4 = info4(B, 2 * b + h2, 0);
+#pragma unroll
+      for (int s = 0; s < QS; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          S[h2][s][r] = n4[r] * (exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])) - er[h2][s]);
+    }
+  };
+  // logits of the chunk's two tile pairs; parents start from ln n
+  // (bf16: all 16 A fragments of the chunk are read before the first product,
+  // so the LDS latency is paid once per chunk, not once per k-step)
+  auto chunk_logits = [&](const unsigned char* B, bool with_ln, f32x4 (&S0)[2][QS],
+                          f32x4 (&S1)[2][QS]) {
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    f32x4 init[TPC];
+#pragma unroll
+    for (int tt = 0; tt < TPC; ++tt) init[tt] = with_ln ? info4(B, tt, 1) : zero;
+    if constexpr (kB) {
+      const T* lc = reinterpret_cast<const T*>(B + Cfg::OFF_C);
+      bf16x8 a[TPC][KQ];
+#pragma unroll
+      for (int tt = 0; tt < TPC; ++tt) {
+        const int r = 32 * (tt / 2) + 8 * (c / 4) + 4 * (tt % 2) + (c % 4);
+        const int sw = row_swizzle<U>(r);
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq)
+          a[tt][kq] = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
+      }
+#pragma unroll
+      for (int tt = 0; tt < TPC; ++tt)
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq)
+#pragma unroll
+          for (int s = 0; s < QS; ++s) {
+            f32x4& o = tt < 2 ? S0[tt][s] : S1[tt - 2][s];
+            o = mfma_bf16(a[tt][kq], qf[s][kq], kq == 0 ? init[tt] : o);
+          }
+    } else {
+      logits(B, 0, S0[0], init[0]);
+      logits(B, 1, S0[1], init[1]);
+      logits(B, 2, S1[0], init[2]);
+      logits(B, 3, S1[1], init[3]);
+    }
   };
 
   const bool need_importance =
       (P > 0 && P < M0) || args.importance != nullptr || (P > 0 && args.topp_idx != nullptr);
-  const int n_pchunks = (M0 + CW - 1) / CW;
-  float rz[QS];
-  auto set_rz = [&]() {
-#pragma unroll
-    for (int s = 0; s < QS; ++s) {
-      float z = zp[s];
-      z += shfl_xor(z, 16);
-      z += shfl_xor(z, 32);
-      rz[s] = qvalid[s] ? 1.f / z : 0.f;
-    }
-  };
-  // u_a = sum over this wave's queries of W_ia / Z_i for the chunk in W:
-  // first over the query subtiles in registers, then over the 16 query
-  // columns by a reduce-scatter butterfly over lane bits 3, 0, 1, 2 that
-  // leaves lane c with value k = 8 b3 + 4 b0 + 2 b1 + b2 of its lane group
-  // (value k = codeword row 16 (k / 4) + 4 g + k % 4 of the chunk).
-  auto importance_partials = [&](const f32x4 (&W)[TPC][QS], int cbase) {
+  const int n_pchunks = PO / 8;
+  // importance: u_a = sum over this wave's queries of p_ia for the chunk in W
+  // (already normalised): first over the query subtiles in registers, then
+  // over the 16 query columns by a reduce-scatter butterfly over lane bits 3,
+  // 0, 1, 2 that leaves lane c with value k = 8 b3 + 4 b0 + 2 b1 + b2 of its
+  // lane group, value k being row r = k % 4 of tile tt = k / 4.
+  auto importance_partials = [&](const f32x4 (&W0)[2][QS], const f32x4 (&W1)[2][QS],
+                                 const float (&mul)[QS], int slot) {
     float u[16];
 #pragma unroll
     for (int tt = 0; tt < TPC; ++tt)
@@ -374,7 +494,8 @@ void attention_kernel(AttnArgs args) {
       for (int r = 0; r < 4; ++r) {
         float acc = 0.f;
 #pragma unroll
-        for (int s = 0; s < QS; ++s) acc = fmaf(W[tt][s][r], rz[s], acc);
+        for (int s = 0; s < QS; ++s)
+          acc = fmaf(tt < 2 ? W0[tt][s][r] : W1[tt - 2][s][r], mul[s], acc);
         u[4 * tt + r] = acc;
       }
     auto step = [&](auto mask_tag, auto half_tag) {
@@ -392,81 +513,115 @@ void attention_kernel(AttnArgs args) {
     step(std::integral_constant<int, 2>{}, std::integral_constant<int, 2>{});
     step(std::integral_constant<int, 4>{}, std::integral_constant<int, 1>{});
     const int k = 8 * ((c >> 3) & 1) + 4 * (c & 1) + 2 * ((c >> 1) & 1) + ((c >> 2) & 1);
-    lw[wave * M0MAX + cbase + 16 * (k / 4) + 4 * g + (k % 4)] = u[0];
+    const int tt = k / 4, r = k % 4;
+    lw[(slot * MAXW + wave) * CW + 32 * (tt / 2) + 8 * g + 4 * (tt % 2) + r] = u[0];
   };
-
-  // ---- phase 1: parent sweep (online softmax over chunks) ---------------------
-  for (int pc = 0; pc < n_pchunks; ++pc) {
-    const int cbase = pc * CW;
-    __syncthreads();
-    stage(parent_crow(cbase), parent_vgroup(cbase), parent_count(cbase), true);
-    __syncthreads();
-    f32x4 S[TPC][QS];
-#pragma unroll
-    for (int tt = 0; tt < TPC; ++tt) logits(tt, S[tt]);
-    bias(S);
-    float mnew[QS];
-    chunk_max(S, mnew);
-    raise_max(mnew);
-#pragma unroll
-    for (int tt = 0; tt < TPC; ++tt)
-#pragma unroll
-      for (int s = 0; s < QS; ++s)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float w = exp2_hw(S[tt][s][r] - m[s]);
-          S[tt][s][r] = w;
-          zp[s] += w;
-        }
-    // a single chunk has its final max and denominators already: importance
-    // comes straight from these weights
-    if (n_pchunks == 1 && need_importance) {
-      set_rz();
-      importance_partials(S, cbase);
-    }
-    accumulate_chunk(S);
-  }
-
-  // ---- phase 2: importance with the final max and denominators ----------------
-  if (need_importance) {
-    if (n_pchunks > 1) {
-      set_rz();
-      for (int pc = 0; pc < n_pchunks; ++pc) {
-        const int cbase = pc * CW;
-        __syncthreads();
-        stage(parent_crow(cbase), parent_vgroup(cbase), parent_count(cbase), false);
-        __syncthreads();
-        f32x4 S[TPC][QS];
-#pragma unroll
-        for (int tt = 0; tt < TPC; ++tt) logits(tt, S[tt]);
-        bias(S);
-#pragma unroll
-        for (int tt = 0; tt < TPC; ++tt)
-#pragma unroll
-          for (int s = 0; s < QS; ++s)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) S[tt][s][r] = exp2_hw(S[tt][s][r] - m[s]);
-        importance_partials(S, cbase);
+  // sum the wave partials of chunk k (slot k % 2) in a fixed order
+  auto importance_flush = [&](int k) {
+    if (tid < CW) {
+      const int a = CW * k + tid;
+      float acc = 0.f;
+      for (int wv = 0; wv < n_active; ++wv) acc += lw[((k % 2) * MAXW + wv) * CW + tid];
+      if (a < M0) {
+        lwf[a] = acc;
+        if (args.importance) args.importance[((size_t)bh * args.n_tiles + t) * M0 + a] = acc;
       }
     }
-    __syncthreads();
-    // sum the wave partials in a fixed order
-    for (int a = tid; a < M0; a += nthr) {
-      float acc = 0.f;
-      for (int wv = 0; wv < nwaves; ++wv) acc += lw[wv * M0MAX + a];
-      lwf[a] = acc;
-      if (args.importance) args.importance[((size_t)bh * args.n_tiles + t) * M0 + a] = acc;
+  };
+  // per-query log2 shift that turns exp2(t - m) into exp2(t - m) / Z
+  float mz[QS];
+  auto set_mz = [&]() {
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      float z = zp[s];
+      z += shfl_xor(z, 16);
+      z += shfl_xor(z, 32);
+      mz[s] = qvalid[s] ? m[s] + log2_hw(z) : __builtin_inff();
     }
-    __syncthreads();
+  };
+
+  // ---- phase 1: parent sweep -------------------------------------------------
+  // Per chunk: the logits of both tile pairs are issued first; the second
+  // pair's MFMAs run while the first pair's weights are computed, and the
+  // first pair's value MFMAs while the second pair's weights are computed.
+  issue_parent(0, buffer(0), true);
+  for (int k = 0; k < n_pchunks; ++k) {
+    wait_chunk();
+    if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, buffer((k + 1) % 2), true);
+    const unsigned char* B = buffer(k % Cfg::NBUF);
+    if (has_rows) {
+      f32x4 S0[2][QS], S1[2][QS];
+      chunk_logits(B, true, S0, S1);
+      float sc[QS];
+      check_pair(S0, sc);
+      parent_weights(S0);
+      if (check_pair(S1, sc)) rescale_pair(S0, sc);
+      accumulate_pair(B, 0, S0);
+      parent_weights(S1);
+      accumulate_pair(B, 1, S1);
+      if (n_pchunks == 1 && need_importance) {  // max and denominators are final
+        set_mz();
+        float rz[QS];
+#pragma unroll
+        for (int s = 0; s < QS; ++s) rz[s] = exp2_hw(m[s] - mz[s]);
+        importance_partials(S0, S1, rz, 0);
+      }
+    }
+    if (Cfg::NBUF == 1 && k + 1 < n_pchunks) {
+      __syncthreads();
+      issue_parent(k + 1, buffer(0), true);
+    }
   }
+
+  // ---- phase 2: importance with the final max and denominators ---------------
+  if (need_importance) {
+    if (n_pchunks == 1) {
+      __syncthreads();
+      importance_flush(0);
+    } else {
+      if (has_rows) set_mz();
+      float one[QS];
+#pragma unroll
+      for (int s = 0; s < QS; ++s) one[s] = 1.f;
+      __syncthreads();
+      issue_parent(0, buffer(0), false);
+      for (int k = 0; k < n_pchunks; ++k) {
+        wait_chunk();
+        if (k > 0) importance_flush(k - 1);
+        if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, buffer((k + 1) % 2), false);
+        const unsigned char* B = buffer(k % Cfg::NBUF);
+        if (has_rows) {
+          f32x4 S0[2][QS], S1[2][QS];
+          chunk_logits(B, true, S0, S1);
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+            for (int s = 0; s < QS; ++s)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                S0[h2][s][r] = exp2_hw(fmaf(S0[h2][s][r], kLog2e, -mz[s]));
+                S1[h2][s][r] = exp2_hw(fmaf(S1[h2][s][r], kLog2e, -mz[s]));
+              }
+          importance_partials(S0, S1, one, k % 2);
+        }
+        if (Cfg::NBUF == 1 && k + 1 < n_pchunks) {
+          __syncthreads();
+          issue_parent(k + 1, buffer(0), false);
+        }
+      }
+      __syncthreads();
+      importance_flush(n_pchunks - 1);
+    }
+  }
+  __syncthreads();
 
   // ---- phase 3: top-P (w desc, index asc) -------------------------------------
   if (P > 0) {
     if (P < M0) {
-      for (int i = tid; i < 256; i += nthr) lhist[i] = 0;
+      for (int i = tid; i < 256; i += blockDim.x) lhist[i] = 0;
       if (tid == 0) lmisc[2] = 0;
       __syncthreads();
-      for (int a = tid; a < M0; a += nthr)
+      for (int a = tid; a < M0; a += blockDim.x)
         atomicAdd(&lhist[(__float_as_uint(lwf[a]) >> 23) & 255], 1);
       __syncthreads();
       if (wave == 0) {
@@ -495,15 +650,14 @@ void attention_kernel(AttnArgs args) {
       }
       __syncthreads();
       const int bstar = lmisc[0], need = P - lmisc[1];
-      int* bmem = reinterpret_cast<int*>(lw);  // boundary-bin members (lw is free now)
-      for (int a = tid; a < M0; a += nthr) {
+      for (int a = tid; a < M0; a += blockDim.x) {
         const int bin = (int)((__float_as_uint(lwf[a]) >> 23) & 255);
         lflag[a] = bin > bstar ? 1 : 0;
         if (bin == bstar) bmem[atomicAdd(&lmisc[2], 1)] = a;
       }
       __syncthreads();
       const int nbm = lmisc[2];
-      for (int q = tid; q < nbm; q += nthr) {
+      for (int q = tid; q < nbm; q += blockDim.x) {
         const int a = bmem[q];
         const float wa = lwf[a];
         int rank = 0;
@@ -515,7 +669,7 @@ void attention_kernel(AttnArgs args) {
         if (rank < need) lflag[a] = 1;
       }
     } else {
-      for (int a = tid; a < M0; a += nthr) lflag[a] = 1;
+      for (int a = tid; a < M0; a += blockDim.x) lflag[a] = 1;
     }
     __syncthreads();
     if (wave == 0) {  // selected parents in ascending index order
@@ -530,7 +684,7 @@ void attention_kernel(AttnArgs args) {
     }
     __syncthreads();
     if (args.topp_idx) {  // canonical order (w desc, index asc) for the caller
-      for (int q = tid; q < P; q += nthr) {
+      for (int q = tid; q < P; q += blockDim.x) {
         const int a = lsel[q];
         const float wa = lwf[a];
         int rank = 0;
@@ -542,69 +696,29 @@ void attention_kernel(AttnArgs args) {
         args.topp_idx[((size_t)bh * args.n_tiles + t) * P + rank] = a;
       }
     }
+    __syncthreads();  // the top-P scratch in buffer 0 is free again
 
     // ---- phase 4: child sweep ----------------------------------------------
-    // Each selected parent owns PS = 4 ceil(Ch/4) consecutive chunk rows: its
-    // Ch children, padded to whole groups of 4 with rows of count 0. With one
-    // child the recovered parent logit is that child's own logit, so every
-    // correcting weight is exactly zero: nothing to do.
-    const int rows = Ch > 1 ? P * PS : 0;
-    for (int cbase = 0; cbase < rows; cbase += CW) {
-      auto child_crow = [=](int r) {
-        const int q = cbase + r;
-        const int k = min(q / PS, P - 1), cc = min(q % PS, Ch - 1);
-        return cc_head + ((size_t)lsel[k] * Ch + cc) * D;
-      };
-      auto child_vgroup = [=](int gl) {
-        const int gg = cbase / 4 + gl;
-        const int k = min(gg / CG, P - 1);
-        return vm_child + ((size_t)lsel[k] * CG + gg % CG) * 4 * D;
-      };
-      auto child_count = [=](int r) {
-        const int q = cbase + r;
-        const int k = q / PS, cc = q % PS;
-        return (q < rows && cc < Ch) ? cb[M0 + lsel[k] * Ch + cc] : 0;
-      };
-      __syncthreads();
-      stage(child_crow, child_vgroup, child_count, true);
-      __syncthreads();
-      f32x4 Sc[TPC][QS];
-      float sp[TPC][QS];  // recovered parent logit of the lane's rows
-#pragma unroll
-      for (int tt = 0; tt < TPC; ++tt) {
-        logits(tt, Sc[tt]);
-#pragma unroll
-        for (int s = 0; s < QS; ++s) {
-          const f32x4 v = Sc[tt][s];
-          if (Ch == 2) {
-            sp[tt][s] = (v[0] + v[1]) * 0.5f;  // rows 2, 3 are padding
-          } else {
-            float sum = (v[0] + v[1]) + (v[2] + v[3]);
-            if (Ch >= 8) sum += shfl_xor(sum, 16);
-            if (Ch >= 16) sum += shfl_xor(sum, 32);
-            sp[tt][s] = sum * (1.f / (float)Ch);
-          }
-        }
+    // The selected parents' child octets, 8 per chunk. With one child the
+    // recovered parent logit is that child's own logit, so every correcting
+    // weight is exactly zero: nothing to do.
+    const int n_cchunks = (n_child_oct + 7) / 8;
+    if (n_cchunks > 0) issue_child(0, buffer(0));
+    for (int k = 0; k < n_cchunks; ++k) {
+      wait_chunk();
+      if (Cfg::NBUF == 2 && k + 1 < n_cchunks) issue_child(k + 1, buffer((k + 1) % 2));
+      const unsigned char* B = buffer(k % Cfg::NBUF);
+      if (has_rows) {
+        f32x4 S0[2][QS], S1[2][QS];
+        chunk_logits(B, false, S0, S1);
+        float sc[QS];
+        check_pair(S0, sc);
+        child_weights(B, 0, S0);
+        if (check_pair(S1, sc)) rescale_pair(S0, sc);
+        accumulate_pair(B, 0, S0);
+        child_weights(B, 1, S1);
+        accumulate_pair(B, 1, S1);
       }
-      bias(Sc);
-      float mnew[QS];
-      chunk_max(Sc, mnew);
-      raise_max(mnew);
-      // dW = n_c (exp(T_c - m) - exp(Srec - m)); padding and empty rows have
-      // n = 0 and t = -inf, so dW = 0 (the recovered term is clamped finite)
-#pragma unroll
-      for (int tt = 0; tt < TPC; ++tt) {
-        const float4 n4 = *reinterpret_cast<const float4*>(&ln[16 * tt + 4 * g]);
-#pragma unroll
-        for (int s = 0; s < QS; ++s) {
-          const float e = exp2_hw(fminf(fmaf(sp[tt][s], kLog2e, -m[s]), 64.f));
-          Sc[tt][s][0] = fmaf(-n4.x, e, exp2_hw(Sc[tt][s][0] - m[s]));
-          Sc[tt][s][1] = fmaf(-n4.y, e, exp2_hw(Sc[tt][s][1] - m[s]));
-          Sc[tt][s][2] = fmaf(-n4.z, e, exp2_hw(Sc[tt][s][2] - m[s]));
-          Sc[tt][s][3] = fmaf(-n4.w, e, exp2_hw(Sc[tt][s][3] - m[s]));
-        }
-      }
-      accumulate_chunk(Sc);
     }
   }
 
@@ -633,28 +747,25 @@ template <typename T, int D, int MAXW>
 hipError_t launch_attention_cfg(const AttnArgs& a, int BH, hipStream_t stream) {
   const long long grid = (long long)BH * a.n_tiles;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  const int waves = (a.block_q + 31) / 32;
   using Cfg = AttnCfg<T, D, MAXW>;
   constexpr int slot = 8 + (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0) + (MAXW == 8 ? 1 : 0);
   hipError_t e = ensure_dynamic_lds((const void*)attention_kernel<T, D, MAXW>,
                                     (int)Cfg::LDS_BYTES, slot);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attention_kernel<T, D, MAXW>), dim3((unsigned)grid), dim3(waves * 64),
+  hipLaunchKernelGGL((attention_kernel<T, D, MAXW>), dim3((unsigned)grid), dim3(MAXW * 64),
                      Cfg::LDS_BYTES, stream, a);
   return hipGetLastError();
 }
 
 template <typename T, int D>
 hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
-                            const void* Q, const void* Cp, const void* Cc, const void* Vmean,
-                            const int32_t* counts, void* Y, int32_t* topp_idx,
-                            float* importance, hipStream_t stream) {
+                            const void* Q, const void* Cp, const void* Cc, const void* packed,
+                            void* Y, int32_t* topp_idx, float* importance, hipStream_t stream) {
   AttnArgs a;
   a.Q = Q;
   a.Cp = Cp;
   a.Cc = Cc;
-  a.Vmean = Vmean;
-  a.counts = counts;
+  a.packed = static_cast<const unsigned char*>(packed);
   a.Y = Y;
   a.topp_idx = topp_idx;
   a.importance = importance;
@@ -671,9 +782,8 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
 
 #define AVQ_INSTANTIATE(T, D)                                                                \
   template hipError_t launch_attention<T, D>(int, int, int, int, int, int, int, const void*, \
-                                             const void*, const void*, const void*,          \
-                                             const int32_t*, void*, int32_t*, float*,        \
-                                             hipStream_t);
+                                             const void*, const void*, const void*, void*,   \
+                                             int32_t*, float*, hipStream_t);
 AVQ_INSTANTIATE(bf16, 64)
 AVQ_INSTANTIATE(bf16, 128)
 AVQ_INSTANTIATE(float, 64)

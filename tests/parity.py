@@ -25,6 +25,8 @@ Error bounds (u = 2^-24, gamma_n = n u / (1 - n u)):
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 import torch
 
@@ -46,31 +48,54 @@ def to_gpu(x: dict) -> dict:
 def gpu_forward(xd: dict, w) -> dict:
     """Runs the three entry points and returns every output on the CPU."""
     par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
-    Vmean, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
-    Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, w.P, w.block_q,
+    packed, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
+    Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q,
                                      debug=True)
     torch.cuda.synchronize()
-    out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, Vmean=Vmean, counts=counts, Y=Y,
+    out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, packed=packed, counts=counts, Y=Y,
                topp=topp, importance=imp)
     return {k: v.cpu() for k, v in out.items()}
 
 
-def unpack_means(vm: np.ndarray, M0: int, Ch: int, d: int):
-    """Packed mean values [B, H, E] -> (means [B, H, Mtot, d], padding slots).
+def unpack_packed(pk: np.ndarray, M0: int, Ch: int, d: int, dtype: str):
+    """Packed aggregates [B, H, bytes] -> (means [B, H, Mtot, d] float64,
+    n [B, H, Mtot], ln n [B, H, Mtot], padding dict).
 
-    Layout: the parents in ceil(M0/4) groups [d][4] (slot s of group k is code
-    4k + s), then for every parent ceil(Ch/4) groups [d][4] of its children."""
-    B, H, E = vm.shape
-    PG, CG = (M0 + 3) // 4, (Ch + 3) // 4
-    assert E == (PG + M0 * CG) * 4 * d
-    par = vm[..., :PG * 4 * d].reshape(B, H, PG, d, 4).transpose(0, 1, 2, 4, 3)
-    par = par.reshape(B, H, PG * 4, d)
-    ch = vm[..., PG * 4 * d:].reshape(B, H, M0, CG, d, 4).transpose(0, 1, 2, 3, 5, 4)
-    ch = ch.reshape(B, H, M0, CG * 4, d)
+    Layout: octets of 8 codes; the parent octets (padded to a multiple of 8
+    octets), then ceil(Ch/8) child octets per parent, then one empty octet.
+    Means [n_oct][d][8] in the storage dtype, then info [n_oct][16] fp32
+    (n, then ln n)."""
+    B, H, E = pk.shape
+    PO, CO = -(-M0 // 64) * 8, -(-Ch // 8)
+    n_oct = PO + M0 * CO + 1
+    esz = 2 if dtype == "bf16" else 4
+    info_off = n_oct * 8 * d * esz
+    assert E == info_off + n_oct * 64
+    raw = np.ascontiguousarray(pk[..., :info_off])
+    if dtype == "bf16":
+        bits = raw.view(np.uint16).astype(np.uint32) << 16
+        vals = bits.view(np.float32)
+    else:
+        vals = raw.view(np.float32)
+    vals = vals.astype(np.float64).reshape(B, H, n_oct, d, 8).transpose(0, 1, 2, 4, 3)
+    info = np.ascontiguousarray(pk[..., info_off:]).view(np.float32).reshape(B, H, n_oct, 16)
+    par = vals[:, :, :PO].reshape(B, H, PO * 8, d)
+    ch = vals[:, :, PO:PO + M0 * CO].reshape(B, H, M0, CO * 8, d)
     means = np.concatenate([par[:, :, :M0], ch[:, :, :, :Ch].reshape(B, H, M0 * Ch, d)], axis=2)
-    pad = np.concatenate([par[:, :, M0:].reshape(B, H, -1), ch[:, :, :, Ch:].reshape(B, H, -1)],
-                         axis=2)
-    return means, pad
+    pn = info[:, :, :PO, :8].reshape(B, H, PO * 8)
+    pl = info[:, :, :PO, 8:].reshape(B, H, PO * 8)
+    cn = info[:, :, PO:PO + M0 * CO, :8].reshape(B, H, M0, CO * 8)
+    cl = info[:, :, PO:PO + M0 * CO, 8:].reshape(B, H, M0, CO * 8)
+    n = np.concatenate([pn[:, :, :M0], cn[:, :, :, :Ch].reshape(B, H, -1)], axis=2)
+    ln = np.concatenate([pl[:, :, :M0], cl[:, :, :, :Ch].reshape(B, H, -1)], axis=2)
+    pad = dict(
+        means=np.concatenate([par[:, :, M0:].reshape(B, H, -1), ch[:, :, :, Ch:].reshape(B, H, -1),
+                              vals[:, :, -1].reshape(B, H, -1)], axis=2),
+        n=np.concatenate([pn[:, :, M0:], cn[:, :, :, Ch:].reshape(B, H, -1), info[:, :, -1, :8]],
+                         axis=2),
+        ln=np.concatenate([pl[:, :, M0:], cl[:, :, :, Ch:].reshape(B, H, -1), info[:, :, -1, 8:]],
+                          axis=2))
+    return means, n, ln, pad
 
 
 class Report(dict):
@@ -142,16 +167,24 @@ def check_aggregate(x, w, g, o, clean) -> Report:
     err = np.abs(gV.astype(np.float64) - oV)
     assert (err[clean] <= tol[clean]).all(), f"Vbar error {err[clean].max()} above bound"
     assert (gn[..., :w.M0].sum(-1) == w.N).all()
-    # Packed means: fl(fl(sum) * fl(1/n)) rounded to the storage dtype; empty
-    # codes and padding slots are exactly zero.
-    means, pad = unpack_means(g["Vmean"].float().numpy().astype(np.float64), w.M0, w.Ch, w.d)
-    assert (pad == 0).all(), "padding slots of the packed means are not zero"
+    # Packed aggregates: means fl(fl(sum) * fl(1/n)) rounded to the storage
+    # dtype; n exact; ln n within a few ulp; empty codes and padding slots
+    # exactly 0 (means, n) and -inf (ln n).
+    means, n_pk, ln_pk, pad = unpack_packed(g["packed"].numpy(), w.M0, w.Ch, w.d, w.dtype)
+    assert (pad["means"] == 0).all(), "padding means of the packed aggregates are not zero"
+    assert (pad["n"] == 0).all() and np.isneginf(pad["ln"]).all(), "padding info is not empty"
+    np.testing.assert_array_equal(n_pk[clean], on[clean].astype(np.float32))
+    nz = on > 0
+    ln_err = np.abs(ln_pk.astype(np.float64) - np.log(np.maximum(on, 1)))
+    assert (ln_err[nz & clean[..., None]] <= 8 * U * np.log(np.maximum(on, 2))[nz & clean[..., None]]
+            + 1e-7).all(), "ln n of the packed aggregates is off"
+    assert np.isneginf(ln_pk[~nz & clean[..., None]]).all()
     n = np.maximum(on, 1)[..., None]
     omean = oV / n
     r_store = 2.0 ** -8 if w.dtype == "bf16" else U
     tol_m = tol / n + (3 * U + r_store) * np.abs(omean) + 1e-30
     err_m = np.abs(means - omean)
-    assert (err_m[clean] <= tol_m[clean]).all(), f"Vmean error {err_m[clean].max()} above bound"
+    assert (err_m[clean] <= tol_m[clean]).all(), f"mean error {err_m[clean].max()} above bound"
     assert (means[clean][on[clean] == 0] == 0).all(), "mean of an empty code is not zero"
     return Report(max_vbar_err=float(err[clean].max()) if clean.any() else 0.0,
                   max_mean_err=float(err_m[clean].max()) if clean.any() else 0.0)
@@ -163,7 +196,13 @@ def importance_eps(x, w, o) -> float:
     cmax = np.linalg.norm(Cp, axis=-1).max()
     S = np.einsum("bhnd,hmd->bhnm", Q[:, :, :64], Cp)
     spread = float((S.max(-1) - S.min(-1)).max()) * 1.5
-    return 4 * gamma(w.d) * qmax * cmax + 2 * U * (spread + 8) + 2 * gamma(w.M0 + w.block_q)
+    # the kernel evaluates exp2((S + ln n) log2 e - m - log2 Z): the logit sum
+    # starts at ln n (gamma_d ln N more), and the shift m + log2 Z (|m| at most
+    # about 1.5 max|S| + log2 N + the lazy margin) is rounded once more
+    logN = math.log(max(w.N, 2))
+    shift = 1.5 * qmax * cmax + logN / math.log(2) + 16
+    return (4 * gamma(w.d) * qmax * cmax + gamma(w.d) * logN + 2 * U * (spread + 8)
+            + 2 * U * shift + 2 * gamma(w.M0 + w.block_q))
 
 
 def check_topp(x, w, g, o, clean, tile_mask) -> tuple:

@@ -37,7 +37,7 @@ def test_header_declares_the_entry_points():
 def test_library_exports_every_declared_symbol(L):
     for name in declared_functions():
         assert hasattr(L, name), name
-    assert L.avq_version() == 101
+    assert L.avq_version() == 200
 
 
 NULL = None
@@ -52,7 +52,7 @@ def aggregate(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 5):
     return L.avq_aggregate(dtype, B, H, N, d, M0, Ch, *ptrs, NULL)
 
 
-def attn(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,) * 6):
+def attn(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,) * 5):
     return L.avq_attention_fwd(dtype, B, H, N, d, M0, Ch, P, bq, *ptrs, NULL, NULL, NULL)
 
 
@@ -75,33 +75,40 @@ def test_null_pointers_are_rejected(L):
         ptrs = [FAKE] * 5
         ptrs[i] = NULL
         assert assign(L, ptrs=ptrs) == INVALID
-    # V, code_idx, counts are required; of Vbar and Vmean at least one
+    # V, code_idx, counts are required; of Vbar and packed at least one
     for i in (0, 1, 3):
         ptrs = [FAKE] * 5
         ptrs[i] = NULL
         assert aggregate(L, ptrs=ptrs) == INVALID
     assert aggregate(L, ptrs=(FAKE, FAKE, NULL, FAKE, NULL)) == INVALID
-    for i in range(6):
-        ptrs = [FAKE] * 6
+    for i in range(5):
+        ptrs = [FAKE] * 5
         ptrs[i] = NULL
         assert attn(L, ptrs=ptrs) == INVALID
     assert "null" in L.avq_last_error().decode()
 
 
-def test_packed_means_size(L):
-    # parents in ceil(M0/4) groups of 4 codes, then ceil(Ch/4) groups per parent
-    assert L.avq_packed_means_elems(5, 2, 64) == (2 + 5 * 1) * 4 * 64
-    assert L.avq_packed_means_elems(256, 8, 128) == (64 + 256 * 2) * 4 * 128
-    assert L.avq_packed_means_elems(512, 16, 128) == (128 + 512 * 4) * 4 * 128
-    assert L.avq_packed_means_elems(0, 2, 64) == -1
-    assert L.avq_packed_means_elems(4, 2, -1) == -1
+def test_packed_size(L):
+    # octets of 8 codes: parents padded to a multiple of 64, ceil(Ch/8) child
+    # octets per parent, one empty octet; each octet is 8 d values plus 64
+    # bytes of count info
+    def expect(M0, Ch, d, esz):
+        n_oct = -(-M0 // 64) * 8 + M0 * -(-Ch // 8) + 1
+        return n_oct * (8 * d * esz + 64)
+    assert L.avq_packed_bytes(BF16, 256, 8, 128) == expect(256, 8, 128, 2)
+    assert L.avq_packed_bytes(BF16, 256, 8, 128) == (32 + 256 + 1) * (2048 + 64)
+    assert L.avq_packed_bytes(F32, 37, 16, 64) == expect(37, 16, 64, 4)
+    assert L.avq_packed_bytes(BF16, 5, 2, 64) == expect(5, 2, 64, 2)
+    assert L.avq_packed_bytes(BF16, 0, 2, 64) == -1
+    assert L.avq_packed_bytes(BF16, 4, 2, -1) == -1
+    assert L.avq_packed_bytes(7, 4, 2, 64) == -1
 
 
 def test_misaligned_pointers_are_rejected(L):
     odd = ctypes.c_void_p(24)
     assert assign(L, ptrs=(odd,) + (FAKE,) * 4) == INVALID
     assert aggregate(L, ptrs=(FAKE, FAKE, FAKE, FAKE, odd)) == INVALID
-    assert attn(L, ptrs=(FAKE,) * 3 + (odd,) + (FAKE,) * 2) == INVALID
+    assert attn(L, ptrs=(FAKE,) * 3 + (odd,) + (FAKE,)) == INVALID
     assert "aligned" in L.avq_last_error().decode()
 
 

@@ -96,9 +96,9 @@ def test_children_equal_parent_gives_vq_attention():
     assert (g["counts"][..., w.M0:] == 0).all()
     from paper_2607_12789_amd import avq
     xd = {k: v.cuda() for k, v in x.items()}
-    Vmean, counts = g["Vmean"].cuda(), g["counts"].cuda()
-    y_ref = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, w.P, w.block_q)
-    y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], Vmean, counts, 0, w.block_q)
+    packed = g["packed"].cuda()
+    y_ref = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q)
+    y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, 0, w.block_q)
     assert torch.equal(y_ref, y0)
 
 
