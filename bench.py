@@ -40,7 +40,7 @@ TRAFFIC_SUMMARY = ROOT / "profiles" / "attention_fwd_c4_traffic.md"
 
 def kernel_hash() -> str:
     h = hashlib.sha256()
-    for name in ("avq_attention.hip", "avq_common.hpp"):
+    for name in ("avq_attention.hip", "avq_common.hpp", "avq_packed.hpp"):
         h.update((KERNEL_SRC.parent / name).read_bytes())
     return h.hexdigest()[:16]
 

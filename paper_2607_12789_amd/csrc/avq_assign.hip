@@ -1,32 +1,54 @@
 // Tree vector quantisation of the keys (Sec. 3.2 nearest-codeword assignment,
-// Sec. 4.2 / Alg. 1 parent then child loop) for gfx950.
+// Sec. 4.2 / Alg. 1 parent then child loop) for gfx950, in two kernels.
 //
-// One workgroup = 4 waves = 256 keys of one (batch, head). Each wave owns 64
-// keys (4 subtiles of 16). The parent codebook of the head streams through LDS
-// in chunks of 64 rows; every chunk is used by all four waves.
+// Distances are evaluated as ||c||^2 - 2 k.c, which has the argmin of
+// ||k - c||^2. k.c comes from MFMA on the transposed product C . K^T
+// (codewords as rows, keys as columns), so each lane owns one key column and
+// four consecutive codewords; ||c||^2 is summed per codeword with one fixed
+// routine, so identical codewords give identical distances.
 //
-// Parent argmin: distances are evaluated as ||c||^2 - 2 k.c, the form whose
-// argmin over c equals that of ||k - c||^2. k.c comes from MFMA computing the
-// transposed product C . K^T (codewords as rows, keys as columns), so each lane
-// owns one key column and four consecutive codewords; the lane keeps a running
-// (distance, index) minimum over its rows in ascending codeword order (strict
-// <, so the lowest index wins exact ties), and the four lane groups merge
-// lexicographically. ||c||^2 is summed once per staged row in fixed order, so
-// identical codewords give identical distances.
+// In both kernels one side of the product is scaled by -2 (exact in bf16 and
+// fp32: the keys in the parent kernel, the candidate rows in the child
+// kernel) and the MFMA accumulator starts at ||c||^2, so the accumulator holds
+// the distance itself.
 //
-// Child compare: the key is compared with the Ch children of its parent and,
-// with the same routine, with the parent itself, so that a child identical to
-// its parent gives exactly the parent's distance. For bf16 the routine is
-// ||c||^2 - 2 k.c with both dot products taken by packed bf16 dot2
-// instructions (products exact, fp32 accumulation); for fp32 it is the direct
-// sum of (k - c)^2. Each lane group sums its quarter of d and the quarters are
-// combined by the same butterfly for every candidate. A key moves to its
-// nearest child only if that value is strictly below the parent's (equal
-// values keep the parent). Candidates are gathered four at a time so their
-// loads overlap.
+// parent_assign_kernel: one workgroup = 4 waves = 256 keys of one
+// (batch, head), 64 keys per wave (4 subtiles of 16). The norms of the head's
+// parents are summed once per workgroup (one row per thread, in order); the
+// parent codebook streams through LDS in chunks of 64 rows by direct
+// global->LDS copies, double buffered. Every lane keeps a running
+// (distance, index) minimum over its rows in ascending codeword order with a
+// strict <, and the four lane groups merge lexicographically, so exact ties
+// go to the lowest index.
+//
+// child_assign_kernel: one workgroup owns one (batch, head) and a range of F
+// parents. It scans the head's parent indices in rounds, buckets the keys of
+// its parents by parent (integer LDS atomics: histogram, prefix sum,
+// scatter), and turns each parent's bucket into groups of 16 keys. For a
+// group, one MFMA tile holds the candidates of Alg. 1's child loop as rows:
+// row 0 the parent, rows 1..Ch its children (Ch = 16: a second tile for the
+// last child). All candidates, the parent included, go through the same
+// routine, so a child equal to its parent has exactly the parent's distance.
+// The nearest child (strict <, lowest index) replaces the parent only if its
+// distance is strictly smaller.
 #include "avq_common.hpp"
 
+#include <type_traits>
+
 namespace avq {
+
+// XOR swizzle of the 16-byte units of a staged codebook row: the 16 rows a
+// tile reads (16 tt + c) get distinct units for the same logical unit.
+template <int U>
+__device__ __forceinline__ int assign_swizzle(int r) {
+  if constexpr (U >= 16) return r & 15;
+  return (r >> 1) & 7;  // U = 8: two rows per 256 bytes
+}
+
+__device__ __forceinline__ void copy16_lds(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                   (void __attribute__((address_space(3)))*)lds, 16, 0, 0);
+}
 
 template <typename T, int D>
 struct AssignCfg {
@@ -34,28 +56,70 @@ struct AssignCfg {
   static constexpr int kWaves = 4;
   static constexpr int KS = 4;                    // key subtiles (of 16) per wave
   static constexpr int kKeysPerBlock = kWaves * KS * 16;
-  static constexpr int CW = 64;                   // codebook rows per LDS chunk
+  static constexpr int CW = 64;                   // codebook rows per chunk
   static constexpr int KQ = kB ? D / 32 : D / 4;  // MFMA k-steps over d
-  static constexpr int PAD = kB ? 8 : 4;          // 16 bytes of row padding
-  static constexpr int ROW = D + PAD;
-  static constexpr int SLOT = kB ? 8 : 1;         // d values per lane per k-step
+  static constexpr int ESZ = sizeof(T);
+  static constexpr int EPU = 16 / ESZ;
+  static constexpr int U = D * ESZ / 16;          // 16-byte units per row
+  static constexpr int COPIES = CW * U / 64;      // wave copies per chunk
+  static constexpr int CPW = COPIES / kWaves;
+  static constexpr int CHUNK_BYTES = CW * D * ESZ;
+  static constexpr int BUF_BYTES = CHUNK_BYTES;
+  static constexpr int M0MAX = 512;
+  static constexpr int LDS_BYTES = 2 * BUF_BYTES + M0MAX * 4;  // two chunks + all norms
+  static_assert(COPIES % kWaves == 0, "copies split evenly over the waves");
 };
 
+// Sum of squares of the 8 (bf16) or 1 (fp32) values of a fragment, in order.
+template <typename T>
+__device__ __forceinline__ float frag_sq(const typename std::conditional<Elem<T>::kBf16, bf16x8, float>::type& v,
+                                         float acc) {
+  if constexpr (Elem<T>::kBf16) {
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+      const bf16x2 p = {v[i], v[i + 1]};
+      acc = __builtin_amdgcn_fdot2_f32_bf16(p, p, acc, false);
+    }
+    return acc;
+  } else {
+    return fmaf(v, v, acc);
+  }
+}
+
+// -2 x, exactly (a power-of-two scale)
+__device__ __forceinline__ bf16x8 times_minus2(const bf16x8& v) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (bf16)(-2.f * (float)v[i]);
+  return r;
+}
+__device__ __forceinline__ float times_minus2(float v) { return -2.f * v; }
+
+// ||row||^2 of a codebook row in one fixed order (consecutive pairs of d)
 template <typename T, int D>
-__global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
-                                                     const T* __restrict__ Cp,
-                                                     const T* __restrict__ Cc,
-                                                     int32_t* __restrict__ parent_idx,
-                                                     int32_t* __restrict__ code_idx, int H,
-                                                     int N, int M0, int Ch,
-                                                     int blocks_per_bh) {
+__device__ __forceinline__ float row_norm(const T* row) {
+  float acc = 0.f;
+  if constexpr (Elem<T>::kBf16) {
+#pragma unroll
+    for (int d0 = 0; d0 < D; d0 += 8) acc = frag_sq<T>(*reinterpret_cast<const bf16x8*>(row + d0), acc);
+  } else {
+#pragma unroll 8
+    for (int d0 = 0; d0 < D; ++d0) acc = fmaf(row[d0], row[d0], acc);
+  }
+  return acc;
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict__ K,
+                                                            const T* __restrict__ Cp,
+                                                            int32_t* __restrict__ parent_idx, int H,
+                                                            int N, int M0, int blocks_per_bh) {
   using Cfg = AssignCfg<T, D>;
   constexpr bool kB = Cfg::kB;
-  constexpr int KS = Cfg::KS, CW = Cfg::CW, KQ = Cfg::KQ, ROW = Cfg::ROW;
+  constexpr int KS = Cfg::KS, CW = Cfg::CW, KQ = Cfg::KQ, U = Cfg::U, EPU = Cfg::EPU,
+                CPW = Cfg::CPW;
   using Frag = typename std::conditional<kB, bf16x8, float>::type;
-
-  __shared__ __attribute__((aligned(16))) T lc[CW * ROW];
-  __shared__ float lnorm[CW];
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
 
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
@@ -64,9 +128,28 @@ __global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
   const int bh = blk / blocks_per_bh;
   const int h = bh % H;
   const int key0 = (blk % blocks_per_bh) * Cfg::kKeysPerBlock + wave * KS * 16;
+  const T* cp_head = Cp + (size_t)h * M0 * D;
 
-  // Key fragments: subtile s holds key key0 + 16 s + c; lane group g holds the
-  // d values of k-step kq at 32 kq + 8 g (bf16) or 4 kq + g (fp32).
+  // chunk staging: copy i of this wave covers rows (64 j + lane) / U
+  auto issue = [&](int k) {
+    unsigned char* B = lds_raw + (k % 2) * Cfg::BUF_BYTES;
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int j = wave + Cfg::kWaves * i;
+      const int q = 64 * j + lane;
+      const int r = q / U, pu = q % U;
+      const T* src = cp_head + (size_t)min(CW * k + r, M0 - 1) * D + (pu ^ assign_swizzle<U>(r)) * EPU;
+      copy16_lds(src, B + 1024 * j);
+    }
+  };
+  const int n_chunks = (M0 + CW - 1) / CW;
+  issue(0);
+  float* lnorm = reinterpret_cast<float*>(lds_raw + 2 * Cfg::BUF_BYTES);  // [M0MAX]
+  for (int r = tid; r < n_chunks * CW; r += blockDim.x)
+    lnorm[r] = r < M0 ? row_norm<T, D>(cp_head + (size_t)r * D) : __builtin_inff();
+
+  // key fragments: subtile s holds key key0 + 16 s + c; lane group g holds
+  // the d values of k-step kq at 32 kq + 8 g (bf16) or 4 kq + g (fp32)
   Frag kf[KS][KQ];
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
@@ -76,10 +159,10 @@ __global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
     for (int kq = 0; kq < KQ; ++kq) {
       if constexpr (kB) {
         bf16x8 v = *reinterpret_cast<const bf16x8*>(row + 32 * kq + 8 * g);
-        kf[s][kq] = (j < N) ? v : bf16x8{};
+        kf[s][kq] = times_minus2((j < N) ? v : bf16x8{});
       } else {
         float v = row[4 * kq + g];
-        kf[s][kq] = (j < N) ? v : 0.f;
+        kf[s][kq] = times_minus2((j < N) ? v : 0.f);
       }
     }
   }
@@ -92,73 +175,47 @@ __global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
     bidx[s] = 0;
   }
 
-  const T* cp_head = Cp + (size_t)h * M0 * D;
-  for (int base = 0; base < M0; base += CW) {
-    // Stage rows [base, base + CW) of the parent codebook (zero rows past M0).
-    constexpr int VEC = 16 / sizeof(T);
-    constexpr int VPR = D / VEC;
-    for (int v = tid; v < CW * VPR; v += blockDim.x) {
-      const int r = v / VPR, col = (v % VPR) * VEC;
-      uint4 val = {0u, 0u, 0u, 0u};
-      if (base + r < M0)
-        val = *reinterpret_cast<const uint4*>(cp_head + (size_t)(base + r) * D + col);
-      *reinterpret_cast<uint4*>(&lc[r * ROW + col]) = val;
-    }
+  for (int k = 0; k < n_chunks; ++k) {
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    {
-      // ||c||^2 of every staged row: four threads per row, each summing a
-      // quarter of d in order, combined in a fixed order (identical codewords
-      // give identical norms).
-      static_assert(CW * 4 == 256, "four threads per staged row");
-      const int r = tid / 4, qd = tid % 4;
-      float s2 = 0.f;
-      for (int e = qd * (D / 4); e < (qd + 1) * (D / 4); ++e) {
-        const float x = to_f32(lc[r * ROW + e]);
-        s2 = fmaf(x, x, s2);
-      }
-      s2 += shfl_xor(s2, 1);
-      s2 += shfl_xor(s2, 2);
-      if (qd == 0) lnorm[r] = (base + r < M0) ? s2 : __builtin_inff();
-    }
-    __syncthreads();
-
+    if (k + 1 < n_chunks) issue(k + 1);
+    const unsigned char* B = lds_raw + (k % 2) * Cfg::BUF_BYTES;
+    const T* lc = reinterpret_cast<const T*>(B);
 #pragma unroll
     for (int tt = 0; tt < CW / 16; ++tt) {
-      if (base + 16 * tt >= M0) break;
+      const int r = 16 * tt + c;
+      const int sw = assign_swizzle<U>(r);
+      // the accumulator starts at ||c||^2 of the lane's rows 4 g + q
+      const f32x4 nr = *reinterpret_cast<const f32x4*>(&lnorm[CW * k + 16 * tt + 4 * g]);
       f32x4 acc[KS];
-#pragma unroll
-      for (int s = 0; s < KS; ++s) acc[s] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kq = 0; kq < KQ; ++kq) {
         if constexpr (kB) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8*>(&lc[(16 * tt + c) * ROW + 32 * kq + 8 * g]);
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
 #pragma unroll
-          for (int s = 0; s < KS; ++s) acc[s] = mfma_bf16(a, kf[s][kq], acc[s]);
+          for (int s = 0; s < KS; ++s) acc[s] = mfma_bf16(a, kf[s][kq], kq == 0 ? nr : acc[s]);
         } else {
-          const float a = lc[(16 * tt + c) * ROW + 4 * kq + g];
+          const float a = lc[r * D + (kq ^ sw) * EPU + g];
 #pragma unroll
-          for (int s = 0; s < KS; ++s) acc[s] = mfma_f32(a, kf[s][kq], acc[s]);
+          for (int s = 0; s < KS; ++s) acc[s] = mfma_f32(a, kf[s][kq], kq == 0 ? nr : acc[s]);
         }
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 16 * tt + 4 * g + r;
-        const float nrm = lnorm[row];
+      for (int q = 0; q < 4; ++q) {
+        const int row = CW * k + 16 * tt + 4 * g + q;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-          const float dist = fmaf(-2.f, acc[s][r], nrm);
+          const float dist = acc[s][q];
           if (dist < best[s]) {
             best[s] = dist;
-            bidx[s] = base + row;
+            bidx[s] = row;
           }
         }
       }
     }
-    __syncthreads();
   }
 
-  // Merge the four lane groups: lexicographic (distance, index) minimum.
+  // merge the four lane groups: lexicographic (distance, index) minimum
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
 #pragma unroll
@@ -170,76 +227,233 @@ __global__ __launch_bounds__(256) void assign_kernel(const T* __restrict__ K,
         bidx[s] = oi;
       }
     }
-  }
-
-  // Child compare (Alg. 1): the parent and its children through one routine.
-  // Candidate 0 is the parent, candidate 1 + c is child c.
-  constexpr int kBatch = 4;
-#pragma unroll
-  for (int s = 0; s < KS; ++s) {
     const int j = key0 + 16 * s + c;
-    const int p = bidx[s];
-    const T* kids = Cc + ((size_t)h * M0 + p) * Ch * D;
-    float dpar = 0.f, dch = __builtin_inff();
-    int cbest = 0;
-    for (int b0 = 0; b0 <= Ch; b0 += kBatch) {
-      Frag cv[kBatch][KQ];
+    if (g == 0 && j < N) parent_idx[(size_t)bh * N + j] = bidx[s];
+  }
+}
+
+// ---------------------------------------------------------------------------
+constexpr int kChildThreads = 256;
+constexpr int kChildWaves = kChildThreads / kWave;
+constexpr int kScanPerThread = 16;
+constexpr int kChildRound = kChildThreads * kScanPerThread;  // parent indices per round
+constexpr int kMaxFam = 32;
+
+struct ChildLds {
+  int qkey[kChildRound];           // keys of this range, scan order
+  unsigned char qfam[kChildRound]; // their family (parent - p0)
+  int skey[kChildRound];           // keys bucketed by family
+  int hist[kMaxFam];
+  int start[kMaxFam + 1];
+  int cursor[kMaxFam];
+  int item_start[kMaxFam + 1];     // first group index of each family
+  int wave_count[kScanPerThread][kChildWaves];
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
+    const T* __restrict__ K, const T* __restrict__ Cp, const T* __restrict__ Cc,
+    const int32_t* __restrict__ parent_idx, int32_t* __restrict__ code_idx, int H, int N, int M0,
+    int Ch, int F, int ranges) {
+  using Frag = typename std::conditional<Elem<T>::kBf16, bf16x8, float>::type;
+  constexpr bool kB = Elem<T>::kBf16;
+  constexpr int KQ = kB ? D / 32 : D / 4;
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
+  ChildLds& L = *reinterpret_cast<ChildLds*>(lds_raw);
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int g = lane / 16, c = lane % 16;
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = blk / ranges;
+  const int h = bh % H;
+  const int p0 = (blk % ranges) * F;
+  const int nfam = min(F, M0 - p0);
+  const int32_t* pidx = parent_idx + (size_t)bh * N;
+  const T* kh = K + (size_t)bh * N * D;
+  const int n_tiles = (Ch + 1 + 15) / 16;  // candidate tiles: parent + children
+  int cur_fam = -1;  // the family whose rows the wave holds
+  Frag cf[2][KQ];
+  f32x4 cn[2];
+
+  // candidate rows of a family (A operand): lane (g, c) holds row c of each
+  // tile; row 0 = the parent, row 1 + j = child j (rows past Ch repeat the
+  // last child and are ignored)
+  auto load_rows = [&](int p, Frag (&cf)[2][KQ]) {
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int cand = min(b0 + u, Ch);  // clamped: slots past Ch are ignored
-        const T* code = cand == 0 ? cp_head + (size_t)p * D : kids + (size_t)(cand - 1) * D;
+    for (int t2 = 0; t2 < 2; ++t2) {
+      if (t2 < n_tiles) {
+        const int cand = 16 * t2 + c;
+        const T* row = cand == 0 ? Cp + ((size_t)h * M0 + p) * D
+                                 : Cc + (((size_t)h * M0 + p) * Ch + min(cand - 1, Ch - 1)) * D;
 #pragma unroll
         for (int kq = 0; kq < KQ; ++kq) {
           if constexpr (kB)
-            cv[u][kq] = *reinterpret_cast<const bf16x8*>(code + 32 * kq + 8 * g);
+            cf[t2][kq] = *reinterpret_cast<const bf16x8*>(row + 32 * kq + 8 * g);
           else
-            cv[u][kq] = code[4 * kq + g];
+            cf[t2][kq] = row[4 * kq + g];
         }
       }
+    }
+  };
+  // ||c||^2 of the lane's rows 4 g + r of each tile: each lane sums its
+  // quarter of row c in order, the quarters are combined in a fixed order,
+  // then the rows are moved to the lanes that hold their products. The rows
+  // are then scaled by -2 (exact), so that the product accumulated onto
+  // ||c||^2 is the distance.
+  auto row_norms = [&](Frag (&cf)[2][KQ], f32x4 (&cn)[2]) {
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        float part;
-        if constexpr (kB) {
-          float dotkc = 0.f, dotcc = 0.f;
+    for (int t2 = 0; t2 < 2; ++t2) {
+      if (t2 < n_tiles) {
+        float part = 0.f;
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) part = frag_sq<T>(cf[t2][kq], part);
+        const float p01 = part + shfl_xor(part, 16);
+        const float p23 = shfl_xor(p01, 32);
+        const float nrm = (g < 2) ? p01 + p23 : p23 + p01;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) cn[t2][r] = __shfl(nrm, 4 * g + r, kWave);
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) cf[t2][kq] = times_minus2(cf[t2][kq]);
+      }
+    }
+  };
+  // the 16 keys of group it (B operand); key index of lane c
+  auto load_keys = [&](int f, int it, Frag (&kf)[KQ], int& key, bool& valid) {
+    const int kb = L.start[f] + 16 * (it - L.item_start[f]);
+    valid = kb + c < L.start[f + 1];
+    key = L.skey[valid ? kb + c : kb];
+    const T* krow = kh + (size_t)key * D;
+#pragma unroll
+    for (int kq = 0; kq < KQ; ++kq) {
+      if constexpr (kB)
+        kf[kq] = *reinterpret_cast<const bf16x8*>(krow + 32 * kq + 8 * g);
+      else
+        kf[kq] = krow[4 * kq + g];
+    }
+  };
+
+  for (int base = 0; base < N; base += kChildRound) {
+    // 1. queue the keys of this range in scan order
+    int cur[kScanPerThread];
+#pragma unroll
+    for (int k = 0; k < kScanPerThread; ++k) {
+      const int j = base + k * kChildThreads + tid;
+      const int p = j < N ? pidx[j] : -1;
+      cur[k] = (p >= p0 && p < p0 + nfam) ? p - p0 : -1;
+    }
+    unsigned long long mask[kScanPerThread];
+#pragma unroll
+    for (int k = 0; k < kScanPerThread; ++k) {
+      mask[k] = __ballot(cur[k] >= 0);
+      if (lane == 0) L.wave_count[k][wave] = __popcll(mask[k]);
+    }
+    if (tid < kMaxFam) L.hist[tid] = 0;
+    __syncthreads();
+    int offset = 0;
+#pragma unroll
+    for (int k = 0; k < kScanPerThread; ++k) {
+      int before = offset, all = 0;
+      for (int wv = 0; wv < kChildWaves; ++wv) {
+        if (wv < wave) before += L.wave_count[k][wv];
+        all += L.wave_count[k][wv];
+      }
+      if (cur[k] >= 0) {
+        const int slot = before + __popcll(mask[k] & ((1ull << lane) - 1ull));
+        L.qkey[slot] = base + k * kChildThreads + tid;
+        L.qfam[slot] = (unsigned char)cur[k];
+        atomicAdd(&L.hist[cur[k]], 1);
+      }
+      offset += all;
+    }
+    const int qlen = offset;
+    __syncthreads();
+    if (qlen == 0) continue;  // uniform
+    // 2. bucket by family; groups of 16 keys per family
+    if (wave == 0) {
+      const int v = lane < nfam ? L.hist[lane] : 0;
+      const int gv = (v + 15) / 16;
+      int incl = v, gincl = gv;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        const int gy = __shfl_up(gincl, off, kWave);
+        if (lane >= off) {
+          incl += y;
+          gincl += gy;
+        }
+      }
+      if (lane < nfam) {
+        L.start[lane] = incl - v;
+        L.cursor[lane] = incl - v;
+        L.item_start[lane] = gincl - gv;
+      }
+      if (lane == nfam - 1) {
+        L.start[nfam] = incl;
+        L.item_start[nfam] = gincl;
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < qlen; e += kChildThreads)
+      L.skey[atomicAdd(&L.cursor[L.qfam[e]], 1)] = L.qkey[e];
+    __syncthreads();
+    // 3. each wave takes groups w, w + 4, ... (a group is 16 keys of one
+    //    family); consecutive groups of a wave mostly share the family, whose
+    //    rows stay in registers
+    const int n_items = L.item_start[nfam];
+    int f = 0;
+    for (int it = wave; it < n_items; it += kChildWaves) {
+      while (L.item_start[f + 1] <= it) ++f;  // wave-uniform
+      const int p = p0 + f;
+      Frag kf[KQ];
+      int key;
+      bool valid;
+      load_keys(f, it, kf, key, valid);
+      if (p != cur_fam) {
+        load_rows(p, cf);
+        row_norms(cf, cn);
+        cur_fam = p;
+      }
+      // distances (accumulators start at ||c||^2, rows enter as -2 c)
+      float dpar = 0.f, dch = __builtin_inff();
+      int cbest = 0;
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        if (t2 < n_tiles) {
+          f32x4 acc = cn[t2];
 #pragma unroll
           for (int kq = 0; kq < KQ; ++kq) {
+            if constexpr (kB)
+              acc = mfma_bf16(cf[t2][kq], kf[kq], acc);
+            else
+              acc = mfma_f32(cf[t2][kq], kf[kq], acc);
+          }
 #pragma unroll
-            for (int i = 0; i < 8; i += 2) {
-              const bf16x2 kk = {kf[s][kq][i], kf[s][kq][i + 1]};
-              const bf16x2 cc = {cv[u][kq][i], cv[u][kq][i + 1]};
-              dotkc = __builtin_amdgcn_fdot2_f32_bf16(kk, cc, dotkc, false);
-              dotcc = __builtin_amdgcn_fdot2_f32_bf16(cc, cc, dotcc, false);
+          for (int r = 0; r < 4; ++r) {
+            const int cand = 16 * t2 + 4 * g + r;
+            if (cand == 0) dpar = acc[r];
+            if (cand >= 1 && cand <= Ch && acc[r] < dch) {
+              dch = acc[r];
+              cbest = cand - 1;
             }
           }
-          dotkc += shfl_xor(dotkc, 16);
-          dotkc += shfl_xor(dotkc, 32);
-          dotcc += shfl_xor(dotcc, 16);
-          dotcc += shfl_xor(dotcc, 32);
-          part = fmaf(-2.f, dotkc, dotcc);
-        } else {
-          part = 0.f;
-#pragma unroll
-          for (int kq = 0; kq < KQ; ++kq) {
-            const float diff = kf[s][kq] - cv[u][kq];
-            part = fmaf(diff, diff, part);
-          }
-          part += shfl_xor(part, 16);
-          part += shfl_xor(part, 32);
-        }
-        const int cand = b0 + u;
-        if (cand == 0) {
-          dpar = part;
-        } else if (cand <= Ch && part < dch) {
-          dch = part;
-          cbest = cand - 1;
         }
       }
+      // merge the lane groups: parent distance from group 0, children by
+      // lexicographic (distance, child) minimum
+      dpar = __shfl(dpar, c, kWave);
+#pragma unroll
+      for (int m = 16; m <= 32; m <<= 1) {
+        const float ob = shfl_xor(dch, m);
+        const int oi = shfl_xor(cbest, m);
+        if (ob < dch || (ob == dch && oi < cbest)) {
+          dch = ob;
+          cbest = oi;
+        }
+      }
+      if (g == 0 && valid)
+        code_idx[(size_t)bh * N + key] = (dch < dpar) ? (M0 + p * Ch + cbest) : p;
     }
-    if (g == 0 && j < N) {
-      const size_t o = (size_t)bh * N + j;
-      parent_idx[o] = p;
-      code_idx[o] = (dch < dpar) ? (M0 + p * Ch + cbest) : p;
-    }
+    __syncthreads();  // the queue is reused by the next round
   }
 }
 
@@ -249,11 +463,30 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
                          hipStream_t stream) {
   using Cfg = AssignCfg<T, D>;
   const int per_bh = (N + Cfg::kKeysPerBlock - 1) / Cfg::kKeysPerBlock;
-  const long long grid = (long long)BH * per_bh;
+  long long grid = (long long)BH * per_bh;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((assign_kernel<T, D>), dim3((unsigned)grid), dim3(Cfg::kWaves * kWave), 0,
-                     stream, static_cast<const T*>(K), static_cast<const T*>(Cp),
-                     static_cast<const T*>(Cc), parent_idx, code_idx, H, N, M0, Ch, per_bh);
+  constexpr int slot_a = 24 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
+  hipError_t e = ensure_dynamic_lds((const void*)parent_assign_kernel<T, D>, Cfg::LDS_BYTES,
+                                    slot_a);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid), dim3(256),
+                     Cfg::LDS_BYTES, stream, static_cast<const T*>(K),
+                     static_cast<const T*>(Cp), parent_idx, H, N, M0, per_bh);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  // child compare: F parents per workgroup
+  const int F = M0 <= 256 ? 8 : 16;
+  const int ranges = (M0 + F - 1) / F;
+  grid = (long long)BH * ranges;
+  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+  constexpr int slot_b = 28 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
+  e = ensure_dynamic_lds((const void*)child_assign_kernel<T, D>, (int)sizeof(ChildLds), slot_b);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((child_assign_kernel<T, D>), dim3((unsigned)grid), dim3(kChildThreads),
+                     sizeof(ChildLds), stream, static_cast<const T*>(K),
+                     static_cast<const T*>(Cp), static_cast<const T*>(Cc), parent_idx, code_idx,
+                     H, N, M0, Ch, F, ranges);
   return hipGetLastError();
 }
 
