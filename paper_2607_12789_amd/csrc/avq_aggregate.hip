@@ -2,11 +2,11 @@
 // convention that a parent row covers its whole cell and a child row the keys
 // that moved to it.
 //
-// One workgroup owns one (batch, head) and a range of up to 32 parent
-// families (a family = parent p and its Ch children); each quarter wave (16
-// lanes) owns one family and is the only writer of its rows, so no float
-// atomics are needed (LDS float atomics serialise on gfx950; integer ones do
-// not). The workgroup
+// One workgroup owns one (batch, head) and a range of 32 parent families (a
+// family = parent p and its Ch children); each half wave (32 lanes) owns one
+// family and is the only writer of its rows, so no float atomics are needed
+// (LDS float atomics serialise on gfx950; integer ones do not). The
+// workgroup
 //   1. scans the codes of every key of the head (the next round's codes are
 //      prefetched while the current one is queued) and appends the keys whose
 //      parent is in its range to an LDS queue, in key order (wave ballot +
@@ -14,10 +14,10 @@
 //   2. when the queue is full or the codes are exhausted, buckets the queued
 //      keys by their row (stay row of the parent, or one of its children) with
 //      integer LDS atomics: histogram, prefix sum, scatter;
-//   3. lets each quarter wave walk the rows of its family, summing the value
-//      rows of each row's keys in fp32 registers (lane l holds columns
-//      l*CPL .. l*CPL+CPL-1 of the row, up to 16 keys' rows in flight),
-//      and adding every finished row sum into the family's register table.
+//   3. lets each half wave walk its family's keys in bucket order, 16 value
+//      rows in flight at a time whatever rows they belong to (lane l holds
+//      columns l*CPL .. l*CPL+CPL-1), summing in fp32 into a running row sum
+//      that is added to the family's register table when the row ends.
 // At the end the parent row is the stay row plus the children (the whole
 // cell), every row is written once, and counts come from the histograms.
 // Optionally the packed aggregates are also written (avq_packed.hpp): the
@@ -29,15 +29,15 @@
 
 namespace avq {
 
-constexpr int kAggThreads = 512;
+constexpr int kAggThreads = 1024;
 constexpr int kAggWaves = kAggThreads / kWave;
-constexpr int kQuarters = kAggThreads / 16;        // families per workgroup at most
-constexpr int kCodesPerThread = 4;                 // codes scanned per thread per round
+constexpr int kFamLanes = 32;                          // lanes per family
+constexpr int kFamilies = kAggThreads / kFamLanes;     // families per workgroup
+constexpr int kCodesPerThread = 8;                     // codes scanned per thread per round
 constexpr int kRound = kAggThreads * kCodesPerThread;
-constexpr int kQueueCap = 8192;                    // queued keys per flush
-constexpr int kMaxRows = kQuarters * 17;           // families x (1 + Ch), Ch <= 16
-constexpr int kInFlight = 16;                      // value rows loaded ahead per quarter wave (max)
-constexpr int kChMax = 16;
+constexpr int kQueueCap = 8192;                        // queued keys per flush
+constexpr int kMaxRows = kFamilies * 17;               // families x (1 + Ch), Ch <= 16
+constexpr int kInFlight = 16;                          // value rows in flight per family
 
 struct AggLds {
   int qkey[kQueueCap];       // queued keys, key order
@@ -47,43 +47,60 @@ struct AggLds {
   int start[kMaxRows + 1];   // bucket starts
   int cursor[kMaxRows];      // scatter cursors
   int total[kMaxRows];       // keys per row over all flushes (the counts)
-  int wave_count[kCodesPerThread][kAggWaves];
+  int wave_count[kCodesPerThread][kAggWaves];  // queued keys per (round slot, wave)
+  int wave_off[kCodesPerThread][kAggWaves];    // their queue offsets in this round
+  int round_total;
+};
+static_assert(kCodesPerThread * kAggWaves <= 128, "one wave scans the slot offsets");
+
+// CPL values of type T as one load: 4, 8 or 16 bytes
+template <int BYTES>
+struct Chunk;
+template <>
+struct Chunk<4> {
+  typedef uint32_t type;
+};
+template <>
+struct Chunk<8> {
+  typedef uint2 type;
+};
+template <>
+struct Chunk<16> {
+  typedef uint4 type;
 };
 
-template <typename T, int D>
+template <typename T, int D, int CHM>
 __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restrict__ V,
                                                                 const int32_t* __restrict__ code_idx,
                                                                 float* __restrict__ Vbar,
                                                                 int32_t* __restrict__ counts,
-                                                                unsigned char* __restrict__ packed, int N,
-                                                                int M0, int Ch, int F,
-                                                                int ranges) {
+                                                                unsigned char* __restrict__ packed,
+                                                                int N, int M0, int Ch, int ranges) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   AggLds& L = *reinterpret_cast<AggLds*>(lds_raw);
-  constexpr int CPL = D / 16;                      // columns per lane (16 lanes per row)
-  constexpr int VEC = 8 / sizeof(T);               // elements per 8-byte chunk
-  constexpr int LPL = CPL / VEC;                   // 8-byte chunks per lane per row
-  constexpr int INF = 256 / (CPL * sizeof(T)) < kInFlight ? 256 / (CPL * sizeof(T)) : kInFlight;
-  static_assert(LPL >= 1 && CPL % 4 == 0, "lane slice is whole 8-byte chunks and float4s");
+  constexpr int CPL = D / kFamLanes;  // columns per lane
+  using Raw = typename Chunk<CPL * sizeof(T)>::type;
+  static_assert(CPL % 2 == 0, "whole pairs of columns per lane");
 
   const int Mtot = M0 * (1 + Ch);
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = blk / ranges;
-  const int p0 = (blk % ranges) * F;
-  const int nfam = min(F, M0 - p0);
+  const int p0 = (blk % ranges) * kFamilies;
+  const int nfam = min(kFamilies, M0 - p0);
   const int rows = nfam * (1 + Ch);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const int sub = lane % 16, quarter = tid / 16;
+  const int sub = lane % kFamLanes, fam = tid / kFamLanes;
+  const int ch_shift = 31 - __builtin_clz(Ch);
 
   for (int r = tid; r < kMaxRows; r += kAggThreads) L.total[r] = 0;
 
   const int32_t* codes = code_idx + (size_t)bh * N;
   const T* vhead = V + (size_t)bh * N * D;
 
-  // the family table of this quarter wave: row 0 = stay, row 1 + c = child c
-  float acc[1 + kChMax][CPL];
+  // the family table of this half wave: row 0 = stay, row 1 + c = child c
+  float acc[1 + CHM][CPL];
 #pragma unroll
-  for (int r = 0; r <= kChMax; ++r)
+  for (int r = 0; r <= CHM; ++r)
 #pragma unroll
     for (int i = 0; i < CPL; ++i) acc[r][i] = 0.f;
 
@@ -107,9 +124,10 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         const int code = next[k];
         row[k] = -1;
         if (code >= 0 && code < Mtot) {
-          const int p = code < M0 ? code : (code - M0) / Ch;
+          // Ch is a power of two: child code M0 + p Ch + c
+          const int p = code < M0 ? code : (code - M0) >> ch_shift;
           if (p >= p0 && p < p0 + nfam)
-            row[k] = (p - p0) * (1 + Ch) + (code < M0 ? 0 : 1 + (code - M0) % Ch);
+            row[k] = (p - p0) * (1 + Ch) + (code < M0 ? 0 : 1 + ((code - M0) & (Ch - 1)));
         }
       }
 #pragma unroll
@@ -123,8 +141,13 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         if (lane == 0) L.wave_count[k][wave] = __popcll(mask[k]);
       }
       __syncthreads();
-      for (int k = 0; k < kCodesPerThread; ++k)
-        for (int wv = 0; wv < kAggWaves; ++wv) round_total += L.wave_count[k][wv];
+      if (wave == 0) {
+        const int tot = prefix128(&L.wave_count[0][0], &L.wave_off[0][0],
+                                  kCodesPerThread * kAggWaves, lane);
+        if (lane == 0) L.round_total = tot;
+      }
+      __syncthreads();
+      round_total = L.round_total;
     }
     // uniform across the workgroup
     const bool flush = done ? qlen > 0 : qlen + round_total > kQueueCap;
@@ -157,94 +180,92 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       for (int e = tid; e < qlen; e += kAggThreads)
         L.skey[atomicAdd(&L.cursor[L.qrow[e]], 1)] = L.qkey[e];
       __syncthreads();
-      if (quarter < nfam) {
-        const int r_begin = quarter * (1 + Ch);
-        for (int rr = 0; rr <= Ch; ++rr) {
-          const int b = L.start[r_begin + rr], e = L.start[r_begin + rr + 1];
-          if (b == e) continue;
-          float cur[CPL];
+      if (fam < nfam) {
+        // the family's keys, bucketed by row, in kInFlight batches; the
+        // running row sum goes into the table when its row ends
+        const int r_begin = fam * (1 + Ch);
+        const int kb = L.start[r_begin], ke = L.start[r_begin + 1 + Ch];
+        int rr = 0;                          // current row of the family
+        int row_end = L.start[r_begin + 1];  // end of its bucket
+        float cur[CPL];
 #pragma unroll
-          for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
-          for (int k0 = b; k0 < e; k0 += INF) {
-            uint2 raw[INF][LPL];
+        for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
+        auto close_row = [&]() {
 #pragma unroll
-            for (int u = 0; u < INF; ++u) {
-              const int k = k0 + u;
-              const T* vrow = vhead + (size_t)L.skey[k < e ? k : b] * D + sub * CPL;
-#pragma unroll
-              for (int l = 0; l < LPL; ++l) raw[u][l] = reinterpret_cast<const uint2*>(vrow)[l];
-            }
-#pragma unroll
-            for (int u = 0; u < INF; ++u) {
-              if (k0 + u < e) {
-#pragma unroll
-                for (int l = 0; l < LPL; ++l) {
-                  const T* x = reinterpret_cast<const T*>(&raw[u][l]);
-#pragma unroll
-                  for (int v = 0; v < VEC; ++v) cur[l * VEC + v] += to_f32(x[v]);
-                }
-              }
-            }
-          }
-#pragma unroll
-          for (int r = 0; r <= kChMax; ++r)
+          for (int r = 0; r <= CHM; ++r)
             if (r == rr)
 #pragma unroll
               for (int i = 0; i < CPL; ++i) acc[r][i] += cur[i];
+#pragma unroll
+          for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
+        };
+        for (int k0 = kb; k0 < ke; k0 += kInFlight) {
+          Raw raw[kInFlight];
+#pragma unroll
+          for (int u = 0; u < kInFlight; ++u) {
+            const int k = min(k0 + u, ke - 1);
+            raw[u] = *reinterpret_cast<const Raw*>(vhead + (size_t)L.skey[k] * D + sub * CPL);
+          }
+#pragma unroll
+          for (int u = 0; u < kInFlight; ++u) {
+            if (k0 + u < ke) {
+              while (k0 + u >= row_end) {  // uniform within the half wave
+                close_row();
+                ++rr;
+                row_end = L.start[r_begin + rr + 1];
+              }
+              const T* x = reinterpret_cast<const T*>(&raw[u]);
+#pragma unroll
+              for (int i = 0; i < CPL; ++i) cur[i] += to_f32(x[i]);
+            }
+          }
         }
+        if (kb < ke) close_row();
       }
       __syncthreads();
       qlen = 0;
     }
     if (done) break;
-    int offset = qlen;
 #pragma unroll
     for (int k = 0; k < kCodesPerThread; ++k) {
-      int before = offset, all = 0;
-      for (int wv = 0; wv < kAggWaves; ++wv) {
-        if (wv < wave) before += L.wave_count[k][wv];
-        all += L.wave_count[k][wv];
-      }
       if (row[k] >= 0) {
-        const int slot = before + __popcll(mask[k] & ((1ull << lane) - 1ull));
+        const int slot = qlen + L.wave_off[k][wave] + __popcll(mask[k] & ((1ull << lane) - 1ull));
         L.qkey[slot] = base + k * kAggThreads + tid;
         L.qrow[slot] = (uint16_t)row[k];
       }
-      offset += all;
     }
-    qlen = offset;
+    qlen += round_total;
     __syncthreads();
   }
 
   // 2. parent row = stay + children; write every row once, and the counts.
   //    Packed aggregates (optional): the owner writes its children's octets
-  //    directly; the parents' octets (8 parents from 8 owners) are put
+  //    directly; the parents' octets (8 parents from 8 owners each) are put
   //    together through LDS (the queue area is free now).
   const PackedLayout PL = packed_layout(M0, Ch, D, (int)sizeof(T));
-  float* pmean = reinterpret_cast<float*>(L.qkey);  // [kQuarters][D]
-  int* pcell = reinterpret_cast<int*>(L.skey);      // [kQuarters] cell sizes
+  float* pmean = reinterpret_cast<float*>(L.qkey);  // [kFamilies][D]
+  int* pcell = reinterpret_cast<int*>(L.skey);      // [kFamilies] cell sizes
   float* vb = Vbar ? Vbar + (size_t)bh * Mtot * D : nullptr;
   unsigned char* pk = packed ? packed + (size_t)bh * PL.bytes : nullptr;
   T* means = reinterpret_cast<T*>(pk);
   float* info = reinterpret_cast<float*>(pk + PL.info_off);
   constexpr float kNegInf = -__builtin_inff();
   constexpr float kLn2 = 0.6931471805599453f;
-  if (quarter < nfam) {
-    const int p = p0 + quarter;
-    const int* tot = &L.total[quarter * (1 + Ch)];
+  if (fam < nfam) {
+    const int p = p0 + fam;
+    const int* tot = &L.total[fam * (1 + Ch)];
     float par[CPL];
 #pragma unroll
     for (int i = 0; i < CPL; ++i) par[i] = acc[0][i];
     int ncell = tot[0];
 #pragma unroll
-    for (int r = 1; r <= kChMax; ++r) {
+    for (int r = 1; r <= CHM; ++r) {
       if (r <= Ch) {
         if (vb) {
-          float4* dst =
-              reinterpret_cast<float4*>(vb + (size_t)(M0 + p * Ch + (r - 1)) * D + sub * CPL);
+          float* dst = vb + (size_t)(M0 + p * Ch + (r - 1)) * D + sub * CPL;
 #pragma unroll
-          for (int i = 0; i < CPL; i += 4)
-            dst[i / 4] = float4{acc[r][i], acc[r][i + 1], acc[r][i + 2], acc[r][i + 3]};
+          for (int i = 0; i < CPL; i += 2)
+            *reinterpret_cast<float2*>(dst + i) = float2{acc[r][i], acc[r][i + 1]};
         }
 #pragma unroll
         for (int i = 0; i < CPL; ++i) par[i] += acc[r][i];
@@ -252,19 +273,18 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       }
     }
     if (vb) {
-      float4* dst = reinterpret_cast<float4*>(vb + (size_t)p * D + sub * CPL);
+      float* dst = vb + (size_t)p * D + sub * CPL;
 #pragma unroll
-      for (int i = 0; i < CPL; i += 4)
-        dst[i / 4] = float4{par[i], par[i + 1], par[i + 2], par[i + 3]};
+      for (int i = 0; i < CPL; i += 2) *reinterpret_cast<float2*>(dst + i) = float2{par[i], par[i + 1]};
     }
     if (pk) {
       const float pinv = ncell > 0 ? 1.f / (float)ncell : 0.f;
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) pmean[quarter * D + sub * CPL + i] = par[i] * pinv;
-      if (sub == 0) pcell[quarter] = ncell;
+      for (int i = 0; i < CPL; ++i) pmean[fam * D + sub * CPL + i] = par[i] * pinv;
+      if (sub == 0) pcell[fam] = ncell;
       // this parent's child octets: [CO][D][8], and their info
 #pragma unroll
-      for (int j = 0; j < (kChMax + 7) / 8; ++j) {
+      for (int j = 0; j < (CHM + 7) / 8; ++j) {
         if (j < PL.CO) {
           const int o = PL.PO + p * PL.CO + j;
           float inv[8];
@@ -281,7 +301,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
             for (int sl = 0; sl < 8; ++sl) {
               float a = 0.f;
 #pragma unroll
-              for (int r = 1; r <= kChMax; ++r)
+              for (int r = 1; r <= CHM; ++r)
                 if (r == 1 + 8 * j + sl) a = acc[r][i];
               v[sl] = a * inv[sl];
             }
@@ -295,19 +315,21 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
               reinterpret_cast<float4*>(dst)[1] = float4{v[4], v[5], v[6], v[7]};
             }
           }
-          // lane sub writes info slot sub: n (slots 0..7), ln n (slots 8..15)
-          const int c = 8 * j + (sub & 7);
-          const int n = c < Ch ? tot[1 + c] : 0;
-          info[(size_t)o * 16 + sub] =
-              sub < 8 ? (float)n : (n > 0 ? log2_hw((float)n) * kLn2 : kNegInf);
+          // lane sub < 16 writes info slot sub: n (slots 0..7), ln n (8..15)
+          if (sub < 16) {
+            const int c = 8 * j + (sub & 7);
+            const int n = c < Ch ? tot[1 + c] : 0;
+            info[(size_t)o * 16 + sub] =
+                sub < 8 ? (float)n : (n > 0 ? log2_hw((float)n) * kLn2 : kNegInf);
+          }
         }
       }
     }
   }
   __syncthreads();
   if (pk) {
-    // the parent octets of this range (the last range also writes the
-    // padding octets, the first one the empty octet)
+    // the parent octets of this range (the last range also writes the padding
+    // octets, the first one the empty octet)
     const int o_begin = p0 / 8;
     const int o_end = (p0 + nfam >= M0) ? PL.PO : (p0 + nfam) / 8;
     const int nrow = (o_end - o_begin) * D;
@@ -351,31 +373,37 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   }
 }
 
+template <typename T, int D, int CHM>
+hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
+                               const int32_t* code_idx, float* Vbar, int32_t* counts,
+                               void* packed, hipStream_t stream) {
+  // one range of kFamilies parents per workgroup: ranges start at multiples
+  // of 8 parents, so each packed octet of parent means is written by one
+  // workgroup
+  static_assert(kFamilies % 8 == 0, "parent octets are assembled by one workgroup");
+  static_assert(kRound <= kQueueCap, "one round of codes fits the queue");
+  const int ranges = (M0 + kFamilies - 1) / kFamilies;
+  const int lds = (int)sizeof(AggLds);
+  hipError_t e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM>, lds,
+                                    (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0) + (CHM == 16 ? 1 : 0));
+  if (e != hipSuccess) return e;
+  const long long grid = (long long)BH * ranges;
+  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((aggregate_kernel<T, D, CHM>), dim3((unsigned)grid), dim3(kAggThreads), lds,
+                     stream, static_cast<const T*>(V), code_idx, Vbar, counts,
+                     static_cast<unsigned char*>(packed), N, M0, Ch, ranges);
+  return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
                               const int32_t* code_idx, float* Vbar, int32_t* counts,
                               void* packed, hipStream_t stream) {
-  DeviceInfo info;
-  hipError_t e = device_info(&info);
-  if (e != hipSuccess) return e;
-  if (Ch > kChMax) return hipErrorInvalidValue;
-  // families per workgroup: one per quarter wave, fewer while that leaves
-  // fewer workgroups than CUs. Every range but the last starts at a multiple
-  // of 8 parents, so that each packed octet of parent means is written by one
-  // workgroup: F stays a multiple of 8 whenever there is more than one range.
-  int F = kQuarters < M0 ? kQuarters : M0;
-  while (F > 8 && F % 16 == 0 && (long long)BH * ((M0 + F - 1) / F) < info.cus) F /= 2;
-  const int ranges = (M0 + F - 1) / F;
-  const int lds = (int)sizeof(AggLds);
-  e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D>, lds,
-                         (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0));
-  if (e != hipSuccess) return e;
-  const long long grid = (long long)BH * ranges;
-  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((aggregate_kernel<T, D>), dim3((unsigned)grid), dim3(kAggThreads), lds,
-                     stream, static_cast<const T*>(V), code_idx, Vbar, counts,
-                     static_cast<unsigned char*>(packed), N, M0, Ch, F, ranges);
-  return hipGetLastError();
+  if (Ch <= 8)
+    return launch_aggregate_dc<T, D, 8>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
+  if (Ch <= 16)
+    return launch_aggregate_dc<T, D, 16>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
+  return hipErrorInvalidValue;
 }
 
 template <typename T>

@@ -233,9 +233,9 @@ __global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-constexpr int kChildThreads = 256;
+constexpr int kChildThreads = 1024;
 constexpr int kChildWaves = kChildThreads / kWave;
-constexpr int kScanPerThread = 16;
+constexpr int kScanPerThread = 8;
 constexpr int kChildRound = kChildThreads * kScanPerThread;  // parent indices per round
 constexpr int kMaxFam = 32;
 
@@ -247,8 +247,11 @@ struct ChildLds {
   int start[kMaxFam + 1];
   int cursor[kMaxFam];
   int item_start[kMaxFam + 1];     // first group index of each family
-  int wave_count[kScanPerThread][kChildWaves];
+  int wave_count[kScanPerThread][kChildWaves];  // queued keys per (round slot, wave)
+  int wave_off[kScanPerThread][kChildWaves];    // their queue offsets
+  int qlen;
 };
+static_assert(kScanPerThread * kChildWaves <= 128, "one wave scans the slot offsets");
 
 template <typename T, int D>
 __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
@@ -349,23 +352,22 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     }
     if (tid < kMaxFam) L.hist[tid] = 0;
     __syncthreads();
-    int offset = 0;
+    if (wave == 0) {
+      const int tot = prefix128(&L.wave_count[0][0], &L.wave_off[0][0],
+                                kScanPerThread * kChildWaves, lane);
+      if (lane == 0) L.qlen = tot;
+    }
+    __syncthreads();
 #pragma unroll
     for (int k = 0; k < kScanPerThread; ++k) {
-      int before = offset, all = 0;
-      for (int wv = 0; wv < kChildWaves; ++wv) {
-        if (wv < wave) before += L.wave_count[k][wv];
-        all += L.wave_count[k][wv];
-      }
       if (cur[k] >= 0) {
-        const int slot = before + __popcll(mask[k] & ((1ull << lane) - 1ull));
+        const int slot = L.wave_off[k][wave] + __popcll(mask[k] & ((1ull << lane) - 1ull));
         L.qkey[slot] = base + k * kChildThreads + tid;
         L.qfam[slot] = (unsigned char)cur[k];
         atomicAdd(&L.hist[cur[k]], 1);
       }
-      offset += all;
     }
-    const int qlen = offset;
+    const int qlen = L.qlen;
     __syncthreads();
     if (qlen == 0) continue;  // uniform
     // 2. bucket by family; groups of 16 keys per family
@@ -476,7 +478,7 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   if (e != hipSuccess) return e;
 
   // child compare: F parents per workgroup
-  const int F = M0 <= 256 ? 8 : 16;
+  const int F = kMaxFam;
   const int ranges = (M0 + F - 1) / F;
   grid = (long long)BH * ranges;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;

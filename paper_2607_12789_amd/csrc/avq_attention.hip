@@ -60,7 +60,7 @@ namespace avq {
 template <typename T, int D, int MAXW>
 struct AttnCfg {
   static constexpr bool kB = Elem<T>::kBf16;
-  static constexpr int RPW = 32;                  // query rows per wave
+  static constexpr int RPW = 32;                  // query rows per wave (16 QS)
   static constexpr int QS = RPW / 16;             // query subtiles per wave
   static constexpr int CW = 64;                   // codeword rows per chunk
   static constexpr int TPC = CW / 16;             // 16-row tiles per chunk
@@ -71,7 +71,7 @@ struct AttnCfg {
   static constexpr int EPU = 16 / ESZ;            // elements per 16-byte unit
   static constexpr int U = D * ESZ / 16;          // 16-byte units per codeword row
   static constexpr int COPIES = CW * U / 64;      // wave copies per array per chunk
-  static constexpr int CPW = COPIES / MAXW;       // ... per wave
+  static constexpr int CPW = (COPIES + MAXW - 1) / MAXW;  // ... per wave, at most
   static constexpr int OCT_ELEMS = 8 * D;         // elements of one mean octet
   static constexpr int OCPY = OCT_ELEMS * ESZ / 1024;  // wave copies per mean octet
   static constexpr int M0MAX = 512;
@@ -93,7 +93,7 @@ struct AttnCfg {
   static constexpr int OFF_HIST = M0MAX * 4;           // [256] i32
   static constexpr int OFF_BMEM = OFF_HIST + 256 * 4;  // [M0MAX] i32
   static constexpr int kWavesPerEu = (kB && D == 64) ? 3 : 2;
-  static_assert(COPIES % MAXW == 0 && CPW >= 1, "copies split evenly over the waves");
+  static_assert(COPIES % MAXW == 0 || COPIES < MAXW, "copies split evenly over the waves");
   static_assert(OCPY >= 1 && (OCPY & (OCPY - 1)) == 0, "whole wave copies per octet");
   static_assert(OFF_BMEM + M0MAX * 4 <= BUF_BYTES, "top-P scratch fits one buffer");
 };
@@ -212,15 +212,18 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int j = wave + MAXW * i;
-      copy16_to_lds(row_of(crow[i] / 8, crow[i] % 8) + ccol[i], B + Cfg::OFF_C + 1024 * j);
+      if (j < Cfg::COPIES)
+        copy16_to_lds(row_of(crow[i] / 8, crow[i] % 8) + ccol[i], B + Cfg::OFF_C + 1024 * j);
     }
     if (with_values) {
 #pragma unroll
       for (int i = 0; i < CPW; ++i) {
         const int j = wave + MAXW * i;
-        const T* src = means + (size_t)octet_of(j / OCPY) * OCT_ELEMS +
-                       (j % OCPY) * 64 * EPU + lane * EPU;
-        copy16_to_lds(src, B + Cfg::OFF_V + 1024 * j);
+        if (j < Cfg::COPIES) {
+          const T* src = means + (size_t)octet_of(j / OCPY) * OCT_ELEMS +
+                         (j % OCPY) * 64 * EPU + lane * EPU;
+          copy16_to_lds(src, B + Cfg::OFF_V + 1024 * j);
+        }
       }
     }
     if (wave == MAXW - 1 && lane < 32)  // 8 octets x 64 bytes of count info

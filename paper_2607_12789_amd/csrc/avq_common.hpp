@@ -84,6 +84,27 @@ struct Elem<bf16> {
   static constexpr bool kBf16 = true;
 };
 
+// Exclusive prefix sums of n <= 128 counts (run by one whole wave): off[i] =
+// cnt[0] + ... + cnt[i-1]; returns the total to every lane.
+__device__ __forceinline__ int prefix128(const int* cnt, int* off, int n, int lane) {
+  const int a = lane < n ? cnt[lane] : 0;
+  const int b = lane + kWave < n ? cnt[lane + kWave] : 0;
+  int ia = a, ib = b;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int ya = __shfl_up(ia, o, kWave);
+    const int yb = __shfl_up(ib, o, kWave);
+    if (lane >= o) {
+      ia += ya;
+      ib += yb;
+    }
+  }
+  const int ta = __shfl(ia, kWave - 1, kWave);
+  if (lane < n) off[lane] = ia - a;
+  if (lane + kWave < n) off[lane + kWave] = ta + ib - b;
+  return ta + __shfl(ib, kWave - 1, kWave);
+}
+
 // Maps a linear workgroup index to a tile index so that consecutive tiles run
 // on the same XCD: workgroups are dispatched round-robin over the 8 XCDs, so
 // workgroup i lands on XCD i % 8. With the remap, XCD x processes the
