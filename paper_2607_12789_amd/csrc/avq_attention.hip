@@ -44,9 +44,9 @@
 //      parents fit one chunk) and takes exp(t - m - ln Z) directly; sums over
 //      the tile's queries by a reduce-scatter butterfly over lanes, then a
 //      fixed order over waves;
-//   3. top-P: histogram of the importance exponents finds the bin holding
-//      the P-th largest value; exact ranks (w desc, index asc) inside that bin
-//      decide the rest; the selected parents are listed in index order;
+//   3. top-P in one wave: a threshold on the importance bits, built bit by
+//      bit from the top, finds the P-th largest value; ties at it go to the
+//      lowest indices; the selected parents are listed in index order;
 //   4. child sweep over the child octets of the selected parents: logits,
 //      recovered parent logit, correcting weights, Xbar += Vmean^T dW;
 //   5. Y = Xbar / Z.
@@ -86,16 +86,10 @@ struct AttnCfg {
   static constexpr size_t OFF_LW = (size_t)NBUF * BUF_BYTES;    // [2][MAXW][CW] f32
   static constexpr size_t OFF_WF = OFF_LW + 2 * MAXW * CW * 4;  // [M0MAX] f32
   static constexpr size_t OFF_SEL = OFF_WF + M0MAX * 4;         // [M0MAX] i32
-  static constexpr size_t OFF_MISC = OFF_SEL + M0MAX * 4;       // [4] i32
-  static constexpr size_t LDS_BYTES = OFF_MISC + 16;
-  // top-P scratch in buffer 0 (no chunk is in flight during top-P)
-  static constexpr int OFF_FLAG = 0;                   // [M0MAX] i32
-  static constexpr int OFF_HIST = M0MAX * 4;           // [256] i32
-  static constexpr int OFF_BMEM = OFF_HIST + 256 * 4;  // [M0MAX] i32
+  static constexpr size_t LDS_BYTES = OFF_SEL + M0MAX * 4;
   static constexpr int kWavesPerEu = (kB && D == 64) ? 3 : 2;
   static_assert(COPIES % MAXW == 0 || COPIES < MAXW, "copies split evenly over the waves");
   static_assert(OCPY >= 1 && (OCPY & (OCPY - 1)) == 0, "whole wave copies per octet");
-  static_assert(OFF_BMEM + M0MAX * 4 <= BUF_BYTES, "top-P scratch fits one buffer");
 };
 
 struct AttnArgs {
@@ -145,10 +139,6 @@ void attention_kernel(AttnArgs args) {
   float* lw = reinterpret_cast<float*>(lds_raw + Cfg::OFF_LW);   // per-wave importance
   float* lwf = reinterpret_cast<float*>(lds_raw + Cfg::OFF_WF);  // importance
   int* lsel = reinterpret_cast<int*>(lds_raw + Cfg::OFF_SEL);    // selected, index order
-  int* lmisc = reinterpret_cast<int*>(lds_raw + Cfg::OFF_MISC);
-  int* lflag = reinterpret_cast<int*>(lds_raw + Cfg::OFF_FLAG);  // top-P only
-  int* lhist = reinterpret_cast<int*>(lds_raw + Cfg::OFF_HIST);
-  int* bmem = reinterpret_cast<int*>(lds_raw + Cfg::OFF_BMEM);
 
   const T* __restrict__ Q = static_cast<const T*>(args.Q);
   const T* __restrict__ Cp = static_cast<const T*>(args.Cp);
@@ -206,51 +196,63 @@ void attention_kernel(AttnArgs args) {
     ccol[i] = ((q % U) ^ row_swizzle<U>(q / U)) * EPU;
   }
   auto buffer = [&](int b) { return lds_raw + b * Cfg::BUF_BYTES; };
-  // octet_of(os): packed octet index of chunk octet os; row_of(os, r8):
-  // codebook row of row r8 (0..7) of chunk octet os.
-  auto issue = [&](unsigned char* B, bool with_values, auto octet_of, auto row_of) {
+  // Sources are a wave-uniform base plus a 32-bit byte offset per lane (the
+  // loads take the scalar-base form). row_off(r): offset of chunk row r
+  // (0..63) from cbase; octet_of(os): index of chunk octet os among the
+  // octets at mbase (means) and ibase (count info).
+  constexpr uint32_t RowB = D * Cfg::ESZ;
+  constexpr uint32_t OctB = OCT_ELEMS * Cfg::ESZ;
+  auto issue = [&](unsigned char* B, bool with_values, const char* cbase, const char* mbase,
+                   const char* ibase, auto octet_of, auto row_off) {
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int j = wave + MAXW * i;
       if (j < Cfg::COPIES)
-        copy16_to_lds(row_of(crow[i] / 8, crow[i] % 8) + ccol[i], B + Cfg::OFF_C + 1024 * j);
+        copy16_to_lds(cbase + (row_off(crow[i]) + (uint32_t)(ccol[i] * Cfg::ESZ)),
+                      B + Cfg::OFF_C + 1024 * j);
     }
     if (with_values) {
 #pragma unroll
       for (int i = 0; i < CPW; ++i) {
         const int j = wave + MAXW * i;
-        if (j < Cfg::COPIES) {
-          const T* src = means + (size_t)octet_of(j / OCPY) * OCT_ELEMS +
-                         (j % OCPY) * 64 * EPU + lane * EPU;
-          copy16_to_lds(src, B + Cfg::OFF_V + 1024 * j);
-        }
+        if (j < Cfg::COPIES)
+          copy16_to_lds(mbase + (octet_of(j / OCPY) * OctB + (uint32_t)((j % OCPY) * 1024 + 16 * lane)),
+                        B + Cfg::OFF_V + 1024 * j);
       }
     }
     if (wave == MAXW - 1 && lane < 32)  // 8 octets x 64 bytes of count info
-      copy16_to_lds(info + (size_t)octet_of(lane / 4) * 16 + (lane % 4) * 4, B + Cfg::OFF_I);
+      copy16_to_lds(ibase + (octet_of(lane / 4) * 64u + (uint32_t)(16 * (lane % 4))), B + Cfg::OFF_I);
   };
+  // parent chunk k: rows past M0 - 1 read row M0 - 1
   auto issue_parent = [&](int k, unsigned char* B, bool with_values) {
+    const int lim = M0 - 1 - 64 * k;
     issue(
-        B, with_values, [&](int os) { return 8 * k + os; },
-        [&](int os, int r8) { return cp_head + (size_t)min(64 * k + 8 * os + r8, M0 - 1) * D; });
+        B, with_values, reinterpret_cast<const char*>(cp_head) + (size_t)64 * k * RowB,
+        reinterpret_cast<const char*>(means) + (size_t)8 * k * OctB,
+        reinterpret_cast<const char*>(info) + (size_t)8 * k * 64,
+        [&](int os) { return (uint32_t)os; },
+        [&](int r) { return (uint32_t)min(r, lim) * RowB; });
   };
-  // child octet o belongs to selected parent o >> co_shift (CO is 1 or 2)
+  // child octet o belongs to selected parent o >> co_shift (CO is 1 or 2);
+  // octets past the last read the empty octet (and the last octet's rows),
+  // rows past Ch - 1 the last child
   const int n_child_oct = Ch > 1 ? P * CO : 0;
   const int co_shift = CO == 2 ? 1 : 0;
   auto issue_child = [&](int k, unsigned char* B) {
     issue(
-        B, true,
+        B, true, reinterpret_cast<const char*>(cc_head), reinterpret_cast<const char*>(means),
+        reinterpret_cast<const char*>(info),
         [&](int os) {
           const int o = 8 * k + os;
-          if (o >= n_child_oct) return ZO;
+          if (o >= n_child_oct) return (uint32_t)ZO;
           const int sl = o >> co_shift;
-          return PO + (lsel[sl] << co_shift) + (o - (sl << co_shift));
+          return (uint32_t)(PO + (lsel[sl] << co_shift) + (o - (sl << co_shift)));
         },
-        [&](int os, int r8) {
-          const int o = min(8 * k + os, n_child_oct - 1);
+        [&](int r) {
+          const int o = min(8 * k + r / 8, n_child_oct - 1);
           const int sl = o >> co_shift;
-          const int cc = min((o - (sl << co_shift)) * 8 + r8, Ch - 1);
-          return cc_head + ((size_t)lsel[sl] * Ch + cc) * D;
+          const int cc = min((o - (sl << co_shift)) * 8 + r % 8, Ch - 1);
+          return (uint32_t)(lsel[sl] * Ch + cc) * RowB;
         });
   };
   auto wait_chunk = [&]() {
@@ -619,70 +621,51 @@ void attention_kernel(AttnArgs args) {
   __syncthreads();
 
   // ---- phase 3: top-P (w desc, index asc) -------------------------------------
+  // One wave. Lane l holds the keys of parents 64 i + l: the importance bits
+  // plus one (importance is a non-negative float, so the integer order is the
+  // value order; padding gets 0, below every parent). A threshold kp is built
+  // bit by bit from the top, the largest with at least P keys >= kp (the P-th
+  // largest key), or the first with exactly P; every key above kp is
+  // selected, and of the keys equal to kp the lowest indices, as many as are
+  // still missing. The selected parents are listed in index order. With
+  // P >= M0 every parent is selected (all keys 1).
   if (P > 0) {
-    if (P < M0) {
-      for (int i = tid; i < 256; i += blockDim.x) lhist[i] = 0;
-      if (tid == 0) lmisc[2] = 0;
-      __syncthreads();
-      for (int a = tid; a < M0; a += blockDim.x)
-        atomicAdd(&lhist[(__float_as_uint(lwf[a]) >> 23) & 255], 1);
-      __syncthreads();
-      if (wave == 0) {
-        // lane l holds bins 255 - 4l - i (i = 0..3): lanes in descending bins
-        int cnt[4], local = 0;
+    if (wave == 0) {
+      constexpr int NV = Cfg::M0MAX / kWave;
+      unsigned key[NV];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          cnt[i] = lhist[255 - 4 * lane - i];
-          local += cnt[i];
-        }
-        int incl = local;
+      for (int i = 0; i < NV; ++i) {
+        const int a = kWave * i + lane;
+        const unsigned kv = P < M0 ? __float_as_uint(lwf[a < M0 ? a : 0]) + 1u : 1u;
+        key[i] = a < M0 ? kv : 0u;
+      }
+      auto count_ge = [&](unsigned v) {
+        int n = 0;
 #pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const int y = __shfl_up(incl, off, kWave);
-          if (lane >= off) incl += y;
-        }
-        int above = incl - local;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (above < P && P <= above + cnt[i]) {
-            lmisc[0] = 255 - 4 * lane - i;
-            lmisc[1] = above;
-          }
-          above += cnt[i];
+        for (int i = 0; i < NV; ++i) n += __popcll(__ballot(key[i] >= v));
+        return n;
+      };
+      unsigned kp = 0u;
+      for (int bit = 30; bit >= 0; --bit) {  // keys stay below 2^31
+        const unsigned cand = kp | (1u << bit);
+        const int cnt = count_ge(cand);
+        if (cnt >= P) {
+          kp = cand;
+          if (cnt == P) break;
         }
       }
-      __syncthreads();
-      const int bstar = lmisc[0], need = P - lmisc[1];
-      for (int a = tid; a < M0; a += blockDim.x) {
-        const int bin = (int)((__float_as_uint(lwf[a]) >> 23) & 255);
-        lflag[a] = bin > bstar ? 1 : 0;
-        if (bin == bstar) bmem[atomicAdd(&lmisc[2], 1)] = a;
-      }
-      __syncthreads();
-      const int nbm = lmisc[2];
-      for (int q = tid; q < nbm; q += blockDim.x) {
-        const int a = bmem[q];
-        const float wa = lwf[a];
-        int rank = 0;
-        for (int k = 0; k < nbm; ++k) {
-          const int b = bmem[k];
-          const float wb = lwf[b];
-          rank += (wb > wa) || (wb == wa && b < a);
-        }
-        if (rank < need) lflag[a] = 1;
-      }
-    } else {
-      for (int a = tid; a < M0; a += blockDim.x) lflag[a] = 1;
-    }
-    __syncthreads();
-    if (wave == 0) {  // selected parents in ascending index order
-      int filled = 0;
-      for (int a0 = 0; a0 < M0; a0 += kWave) {
-        const int a = a0 + lane;
-        const bool f = a < M0 && lflag[a] != 0;
-        const unsigned long long mask = __ballot(f);
-        if (f) lsel[filled + __popcll(mask & ((1ull << lane) - 1ull))] = a;
-        filled += __popcll(mask);
+      const int need = P - count_ge(kp + 1u);  // keys equal to kp still to take
+      const unsigned long long below = (1ull << lane) - 1ull;
+      int eq_before = 0, filled = 0;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const bool eq = key[i] == kp;
+        const unsigned long long me = __ballot(eq);
+        const bool sel = key[i] > kp || (eq && eq_before + __popcll(me & below) < need);
+        eq_before += __popcll(me);
+        const unsigned long long ms = __ballot(sel);
+        if (sel) lsel[filled + __popcll(ms & below)] = kWave * i + lane;
+        filled += __popcll(ms);
       }
     }
     __syncthreads();
@@ -699,7 +682,6 @@ void attention_kernel(AttnArgs args) {
         args.topp_idx[((size_t)bh * args.n_tiles + t) * P + rank] = a;
       }
     }
-    __syncthreads();  // the top-P scratch in buffer 0 is free again
 
     // ---- phase 4: child sweep ----------------------------------------------
     // The selected parents' child octets, 8 per chunk. With one child the
