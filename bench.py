@@ -10,7 +10,8 @@ children each, P=32, query block 128, bf16). Prints one JSON line:
 * value: query-token*heads per second of the whole step, B*H*N / t_step;
 * roofline: the fused attention kernel (the dominant one) against the bf16
   MFMA peak, its algorithmic flops 4 d (M0 + P Ch) per query-head divided by
-  its average launch time (HIP events on the launch stream); traffic is the
+  its average launch duration over the timed steps (HIP events bracketing
+  each launch, on the launch stream); traffic is the
   HBM bytes per launch from the committed rocprofv3 counter summary, or null
   if the kernel source changed since those counters were taken;
 * cpu_baseline: the fp64 oracle timed on the host cores, whole passes over
@@ -115,36 +116,33 @@ def main():
     counts = torch.empty((B, H, w.Mtot), dtype=torch.int32, device=dev)
     Y = torch.empty_like(xd["Q"])
 
-    def step():
+    def step(ev=None):
+        # ev: four events bracketing the three launches (HIP events on the
+        # stream the kernels are launched on, which is torch's current one)
+        if ev: ev[0].record()
         avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code)
+        if ev: ev[1].record()
         avq.aggregate(xd["V"], code, M0, Ch, packed, counts)
+        if ev: ev[2].record()
         avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, P, w.block_q, Y=Y)
+        if ev: ev[3].record()
 
     for _ in range(args.warmup):
         step()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for i in range(args.steps):
+        step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
 
-    # per-kernel average launch time, HIP events on the launch stream
-    def timed(fn, reps):
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s.record()
-        for _ in range(reps):
-            fn()
-        e.record()
-        e.synchronize()
-        return s.elapsed_time(e) / reps
+    # per-kernel average launch duration over the timed steps
+    def avg_ms(a, b):
+        return sum(ev[a].elapsed_time(ev[b]) for ev in evs) / max(len(evs), 1)
 
-    reps = max(args.steps, 1)
-    t_assign = timed(lambda: avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code), reps)
-    t_agg = timed(lambda: avq.aggregate(xd["V"], code, M0, Ch, packed, counts), reps)
-    t_attn = timed(lambda: avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, P,
-                                             w.block_q, Y=Y), reps)
+    t_assign, t_agg, t_attn = avg_ms(0, 1), avg_ms(1, 2), avg_ms(2, 3)
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
