@@ -14,8 +14,8 @@
 //   2. when the queue is full or the codes are exhausted, buckets the queued
 //      keys by their row (stay row of the parent, or one of its children) with
 //      integer LDS atomics: histogram, prefix sum, scatter;
-//   3. lets each half wave walk its family's keys in bucket order, 16 value
-//      rows in flight at a time whatever rows they belong to (lane l holds
+//   3. lets each half wave walk its family's keys in bucket order, 8 value
+//      rows (4 for Ch = 16) in flight at a time whatever rows they belong to (lane l holds
 //      columns l*CPL .. l*CPL+CPL-1), summing in fp32 into a running row sum
 //      that is added to the family's register table when the row ends.
 // At the end the parent row is the stay row plus the children (the whole
@@ -37,7 +37,10 @@ constexpr int kCodesPerThread = 8;                     // codes scanned per thre
 constexpr int kRound = kAggThreads * kCodesPerThread;
 constexpr int kQueueCap = 8192;                        // queued keys per flush
 constexpr int kMaxRows = kFamilies * 17;               // families x (1 + Ch), Ch <= 16
-constexpr int kInFlight = 16;                          // value rows in flight per family
+// value rows in flight per family: as many as the registers beside the
+// family table (1 + CHM rows of D / 32 sums per lane) allow
+template <int CHM>
+constexpr int kInFlight = CHM > 8 ? 4 : 8;
 
 struct AggLds {
   int qkey[kQueueCap];       // queued keys, key order
@@ -181,7 +184,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         L.skey[atomicAdd(&L.cursor[L.qrow[e]], 1)] = L.qkey[e];
       __syncthreads();
       if (fam < nfam) {
-        // the family's keys, bucketed by row, in kInFlight batches; the
+        // the family's keys, bucketed by row, in kInFlight<CHM> batches; the
         // running row sum goes into the table when its row ends
         const int r_begin = fam * (1 + Ch);
         const int kb = L.start[r_begin], ke = L.start[r_begin + 1 + Ch];
@@ -190,24 +193,27 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         float cur[CPL];
 #pragma unroll
         for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
+        // every table row takes cur or zero: a plain add per row keeps the
+        // table in registers (a conditional add on rr alone is turned into an
+        // indexed access to scratch memory)
         auto close_row = [&]() {
 #pragma unroll
           for (int r = 0; r <= CHM; ++r)
-            if (r == rr)
 #pragma unroll
-              for (int i = 0; i < CPL; ++i) acc[r][i] += cur[i];
+            for (int i = 0; i < CPL; ++i) acc[r][i] += r == rr ? cur[i] : 0.f;
 #pragma unroll
           for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
         };
-        for (int k0 = kb; k0 < ke; k0 += kInFlight) {
-          Raw raw[kInFlight];
+        constexpr int kIF = kInFlight<CHM>;
+        for (int k0 = kb; k0 < ke; k0 += kIF) {
+          Raw raw[kIF];
 #pragma unroll
-          for (int u = 0; u < kInFlight; ++u) {
+          for (int u = 0; u < kIF; ++u) {
             const int k = min(k0 + u, ke - 1);
             raw[u] = *reinterpret_cast<const Raw*>(vhead + (size_t)L.skey[k] * D + sub * CPL);
           }
 #pragma unroll
-          for (int u = 0; u < kInFlight; ++u) {
+          for (int u = 0; u < kIF; ++u) {
             if (k0 + u < ke) {
               while (k0 + u >= row_end) {  // uniform within the half wave
                 close_row();
@@ -244,7 +250,15 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   //    together through LDS (the queue area is free now).
   const PackedLayout PL = packed_layout(M0, Ch, D, (int)sizeof(T));
   float* pmean = reinterpret_cast<float*>(L.qkey);  // [kFamilies][D]
-  int* pcell = reinterpret_cast<int*>(L.skey);      // [kFamilies] cell sizes
+  int* pcell = reinterpret_cast<int*>(pmean + kFamilies * D);  // [kFamilies] cell sizes
+  static_assert((kFamilies * D + kFamilies) * 4 <= sizeof(L.qkey), "parent means fit the key queue");
+  // child octets leave through a 1 KB staging area per family (in the free
+  // row and bucket queues), so that each store writes 16 consecutive bytes
+  // per lane, contiguous over the half wave
+  constexpr int kStageRows = 1024 / (8 * (int)sizeof(T));  // octet d-rows per pass
+  static_assert(kFamilies * 1024 <= sizeof(L.qrow) + sizeof(L.skey), "staging fits the queues");
+  static_assert(kStageRows % kFamLanes == 0 && D % kStageRows == 0, "whole passes");
+  T* stage = reinterpret_cast<T*>(reinterpret_cast<unsigned char*>(L.qrow) + fam * 1024);
   float* vb = Vbar ? Vbar + (size_t)bh * Mtot * D : nullptr;
   unsigned char* pk = packed ? packed + (size_t)bh * PL.bytes : nullptr;
   T* means = reinterpret_cast<T*>(pk);
@@ -294,26 +308,50 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
             const int n = c < Ch ? tot[1 + c] : 0;
             inv[sl] = n > 0 ? 1.f / (float)n : 0.f;
           }
+          // pass q: the lanes holding d-rows q R .. q R + R - 1 (R =
+          // kStageRows) put them in the staging area, then lane sub stores
+          // d-rows q R + sub + 32 t
 #pragma unroll
-          for (int i = 0; i < CPL; ++i) {
-            float v[8];
+          for (int q = 0; q < D / kStageRows; ++q) {
 #pragma unroll
-            for (int sl = 0; sl < 8; ++sl) {
-              float a = 0.f;
+            for (int i = 0; i < CPL; ++i) {
+              const int dr = sub * CPL + i - q * kStageRows;
+              if (dr < 0 || dr >= kStageRows) continue;
+              float v[8];
 #pragma unroll
-              for (int r = 1; r <= CHM; ++r)
-                if (r == 1 + 8 * j + sl) a = acc[r][i];
-              v[sl] = a * inv[sl];
+              for (int sl = 0; sl < 8; ++sl) {
+                float a = 0.f;
+#pragma unroll
+                for (int r = 1; r <= CHM; ++r)
+                  if (r == 1 + 8 * j + sl) a = acc[r][i];
+                v[sl] = a * inv[sl];
+              }
+              T* sd = stage + dr * 8;
+              if constexpr (Elem<T>::kBf16) {
+                bf16x8 w = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
+                            (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+                *reinterpret_cast<bf16x8*>(sd) = w;
+              } else {
+                reinterpret_cast<float4*>(sd)[0] = float4{v[0], v[1], v[2], v[3]};
+                reinterpret_cast<float4*>(sd)[1] = float4{v[4], v[5], v[6], v[7]};
+              }
             }
-            T* dst = means + ((size_t)o * D + sub * CPL + i) * 8;
-            if constexpr (Elem<T>::kBf16) {
-              bf16x8 w = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
-                          (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
-              *reinterpret_cast<bf16x8*>(dst) = w;
-            } else {
-              reinterpret_cast<float4*>(dst)[0] = float4{v[0], v[1], v[2], v[3]};
-              reinterpret_cast<float4*>(dst)[1] = float4{v[4], v[5], v[6], v[7]};
+            // the half wave's own LDS writes and reads stay in order
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int t = 0; t < kStageRows / kFamLanes; ++t) {
+              const int dr = sub + kFamLanes * t;
+              T* dst = means + ((size_t)o * D + q * kStageRows + dr) * 8;
+              if constexpr (Elem<T>::kBf16) {
+                *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(stage + dr * 8);
+              } else {
+                reinterpret_cast<float4*>(dst)[0] = reinterpret_cast<const float4*>(stage + dr * 8)[0];
+                reinterpret_cast<float4*>(dst)[1] = reinterpret_cast<const float4*>(stage + dr * 8)[1];
+              }
             }
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
           }
           // lane sub < 16 writes info slot sub: n (slots 0..7), ln n (8..15)
           if (sub < 16) {
