@@ -233,6 +233,199 @@ __global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict_
 }
 
 // ---------------------------------------------------------------------------
+// parent_stream_kernel: the same argmin when the head's whole parent codebook
+// fits half the LDS. Two workgroups per CU, each persistent over a run of
+// consecutive 256-key steps (normally of one (batch, head)): the codebook and
+// its norms are staged once per head, and the key fragments of the next step
+// load while the current step runs, so K streams from HBM without the gaps of
+// a one-shot workgroup. It keeps the keys unscaled and maximises
+// k.c - ||c||^2 / 2, which is the distance times -1/2 exactly.
+template <typename T, int D>
+struct StreamCfg {
+  static constexpr bool kB = Elem<T>::kBf16;
+  static constexpr int kWaves = 4;
+  static constexpr int KS = 4;                    // key subtiles (of 16) per wave
+  static constexpr int kKeysPerStep = kWaves * KS * 16;
+  static constexpr int KQ = kB ? D / 32 : D / 4;
+  static constexpr int ESZ = sizeof(T);
+  static constexpr int EPU = 16 / ESZ;
+  static constexpr int U = D * ESZ / 16;
+  static constexpr int ROW_BYTES = D * ESZ;
+  static constexpr int LDS_HALF = 80 * 1024;      // two workgroups per CU
+  // codebook rows padded to whole pairs of 16-row tiles, then the norms
+  static int lds_bytes(int M0) { return ((M0 + 31) / 32 * 32) * (ROW_BYTES + 4); }
+  static bool fits(int M0) { return lds_bytes(M0) <= LDS_HALF; }
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void parent_stream_kernel(const T* __restrict__ K,
+                                                            const T* __restrict__ Cp,
+                                                            int32_t* __restrict__ parent_idx,
+                                                            int H, int N, int M0, int steps_per_bh,
+                                                            int n_steps) {
+  using Cfg = StreamCfg<T, D>;
+  constexpr bool kB = Cfg::kB;
+  constexpr int KS = Cfg::KS, KQ = Cfg::KQ, U = Cfg::U, EPU = Cfg::EPU;
+  using Frag = typename std::conditional<kB, bf16x8, float>::type;
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
+
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = tid % kWave;
+  const int g = lane / 16, c = lane % 16;
+  const int M16 = (M0 + 31) / 32 * 32;  // whole pairs of 16-row tiles
+  const T* lc = reinterpret_cast<const T*>(lds_raw);                           // [M16][D]
+  float* lnorm = reinterpret_cast<float*>(lds_raw + (size_t)M16 * Cfg::ROW_BYTES);  // [M16]
+
+  // a contiguous run of steps per workgroup
+  const int wg = xcd_remap(blockIdx.x, gridDim.x);
+  const int per = (n_steps + gridDim.x - 1) / gridDim.x;
+  const int s_begin = wg * per, s_end = min(s_begin + per, n_steps);
+  if (s_begin >= s_end) return;  // whole workgroup
+
+  // raw key fragments of step st: subtile s holds key key0 + 16 s + c, lane
+  // group g the d values of k-step kq at 32 kq + 8 g (bf16) or 4 kq + g (fp32);
+  // keys past N read key N - 1
+  auto load_keys = [&](int st, Frag (&dst)[KS][KQ]) {
+    const int bh = st / steps_per_bh;
+    const int key0 = (st % steps_per_bh) * Cfg::kKeysPerStep + wave * KS * 16;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int j = min(key0 + 16 * s + c, N - 1);
+      const T* row = K + ((size_t)bh * N + j) * D;
+#pragma unroll
+      for (int kq = 0; kq < KQ; ++kq) {
+        if constexpr (kB)
+          dst[s][kq] = *reinterpret_cast<const bf16x8*>(row + 32 * kq + 8 * g);
+        else
+          dst[s][kq] = row[4 * kq + g];
+      }
+    }
+  };
+
+  Frag kn[KS][KQ];
+  load_keys(s_begin, kn);
+  int cur_h = -1;
+  for (int st = s_begin; st < s_end; ++st) {
+    const int bh = st / steps_per_bh, h = bh % H;
+    if (h != cur_h) {
+      // stage head h's codebook: row r's 16-byte unit u at unit u ^ swizzle(r)
+      __syncthreads();  // every wave is done with the previous head
+      const T* cp_head = Cp + (size_t)h * M0 * D;
+      const int copies = M16 * U / 64;
+      for (int j = wave; j < copies; j += Cfg::kWaves) {
+        const int q = 64 * j + lane;
+        const int r = q / U, pu = q % U;
+        copy16_lds(cp_head + (size_t)min(r, M0 - 1) * D + (pu ^ assign_swizzle<U>(r)) * EPU,
+                   lds_raw + 1024 * j);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      // norms in one fixed order (consecutive units), +inf past M0 - 1
+      for (int r = tid; r < M16; r += blockDim.x) {
+        const int sw = assign_swizzle<U>(r);
+        float acc = 0.f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if constexpr (kB) {
+            acc = frag_sq<T>(*reinterpret_cast<const bf16x8*>(&lc[r * D + (u ^ sw) * EPU]), acc);
+          } else {
+            const float4 v = *reinterpret_cast<const float4*>(&lc[r * D + (u ^ sw) * EPU]);
+            acc = fmaf(v.x, v.x, acc);
+            acc = fmaf(v.y, v.y, acc);
+            acc = fmaf(v.z, v.z, acc);
+            acc = fmaf(v.w, v.w, acc);
+          }
+        }
+        // the products below give k.c - ||c||^2 / 2 = -(||c||^2 - 2 k.c) / 2
+        // exactly (power-of-two scales), so the nearest row is the largest
+        lnorm[r] = r < M0 ? -0.5f * acc : -__builtin_inff();
+      }
+      __syncthreads();
+      cur_h = h;
+    }
+
+    // this step's keys and the next step's loads
+    Frag kf[KS][KQ];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int kq = 0; kq < KQ; ++kq) kf[s][kq] = kn[s][kq];
+    if (st + 1 < s_end) load_keys(st + 1, kn);
+
+    float best[KS];
+    int bidx[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      best[s] = -__builtin_inff();
+      bidx[s] = 0;
+    }
+    // two 16-row tiles per step: all their row fragments are read before
+    // the products, and the second tile's products overlap the first
+    // tile's comparisons
+    for (int tt = 0; tt < M16 / 16; tt += 2) {
+      f32x4 acc[2][KS];
+      Frag a[2][KQ];
+      f32x4 nr[2];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int r = 16 * (tt + h2) + c;
+        const int sw = assign_swizzle<U>(r);
+        // the accumulator starts at -||c||^2 / 2 of the lane's rows
+        nr[h2] = *reinterpret_cast<const f32x4*>(&lnorm[16 * (tt + h2) + 4 * g]);
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) {
+          if constexpr (kB)
+            a[h2][kq] = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
+          else
+            a[h2][kq] = lc[r * D + (kq ^ sw) * EPU + g];
+        }
+      }
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq)
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            if constexpr (kB)
+              acc[h2][s] = mfma_bf16(a[h2][kq], kf[s][kq], kq == 0 ? nr[h2] : acc[h2][s]);
+            else
+              acc[h2][s] = mfma_f32(a[h2][kq], kf[s][kq], kq == 0 ? nr[h2] : acc[h2][s]);
+          }
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = 16 * (tt + h2) + 4 * g + q;
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            const float v = acc[h2][s][q];
+            if (v > best[s]) {  // strict: the first (lowest) row keeps a tie
+              best[s] = v;
+              bidx[s] = row;
+            }
+          }
+        }
+    }
+    // merge the four lane groups: largest value, lowest index on ties
+    const int key0 = (st % steps_per_bh) * Cfg::kKeysPerStep + wave * KS * 16;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+      for (int m = 16; m <= 32; m <<= 1) {
+        const float ob = shfl_xor(best[s], m);
+        const int oi = shfl_xor(bidx[s], m);
+        if (ob > best[s] || (ob == best[s] && oi < bidx[s])) {
+          best[s] = ob;
+          bidx[s] = oi;
+        }
+      }
+      const int j = key0 + 16 * s + c;
+      if (g == 0 && j < N) parent_idx[(size_t)bh * N + j] = bidx[s];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 constexpr int kChildThreads = 1024;
 constexpr int kChildWaves = kChildThreads / kWave;
 constexpr int kScanPerThread = 8;
@@ -464,16 +657,38 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
                          const void* Cc, int32_t* parent_idx, int32_t* code_idx,
                          hipStream_t stream) {
   using Cfg = AssignCfg<T, D>;
-  const int per_bh = (N + Cfg::kKeysPerBlock - 1) / Cfg::kKeysPerBlock;
-  long long grid = (long long)BH * per_bh;
-  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  constexpr int slot_a = 24 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
-  hipError_t e = ensure_dynamic_lds((const void*)parent_assign_kernel<T, D>, Cfg::LDS_BYTES,
-                                    slot_a);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid), dim3(256),
-                     Cfg::LDS_BYTES, stream, static_cast<const T*>(K),
-                     static_cast<const T*>(Cp), parent_idx, H, N, M0, per_bh);
+  using SCfg = StreamCfg<T, D>;
+  long long grid;
+  hipError_t e;
+  if (SCfg::fits(M0)) {
+    // persistent: two workgroups per CU, each a run of whole steps
+    DeviceInfo dev;
+    e = device_info(&dev);
+    if (e != hipSuccess) return e;
+    const int per_bh = (N + SCfg::kKeysPerStep - 1) / SCfg::kKeysPerStep;
+    const long long n_steps = (long long)BH * per_bh;
+    if (n_steps > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const long long slots = 2LL * (dev.cus > 0 ? dev.cus : 1);
+    const long long per = (n_steps + slots - 1) / slots;
+    grid = (n_steps + per - 1) / per;
+    const int lds = SCfg::lds_bytes(M0);
+    constexpr int slot_s = 32 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
+    e = ensure_dynamic_lds((const void*)parent_stream_kernel<T, D>, SCfg::LDS_HALF, slot_s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid), dim3(256), lds, stream,
+                       static_cast<const T*>(K), static_cast<const T*>(Cp), parent_idx, H, N,
+                       M0, per_bh, (int)n_steps);
+  } else {
+    const int per_bh = (N + Cfg::kKeysPerBlock - 1) / Cfg::kKeysPerBlock;
+    grid = (long long)BH * per_bh;
+    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    constexpr int slot_a = 24 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
+    e = ensure_dynamic_lds((const void*)parent_assign_kernel<T, D>, Cfg::LDS_BYTES, slot_a);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid), dim3(256),
+                       Cfg::LDS_BYTES, stream, static_cast<const T*>(K),
+                       static_cast<const T*>(Cp), parent_idx, H, N, M0, per_bh);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
 
