@@ -1,6 +1,7 @@
 """Throughput of the AVQ-Attention forward pass on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
+    python bench.py --sweep [--steps K] [--warmup W]
 
 One step is the whole forward pass over one batch of synthetic inputs
 already resident in HBM: avq_assign -> avq_aggregate -> avq_attention_fwd.
@@ -16,6 +17,12 @@ children each, P=32, query block 128, bf16). Prints one JSON line:
   if the kernel source changed since those counters were taken;
 * cpu_baseline: the fp64 oracle timed on the host cores, whole passes over
   the same workload repeated for at least --cpu-seconds.
+
+--sweep runs the sequence-length sweep of the scaling analysis instead
+(Sec. 5: B=4, H=12, d=64, N from 1k to 64k, flat and tree codebooks): one
+JSON line per workload with the median step time and the per-kernel medians,
+then one line with the fitted log-log slopes of step time against N and
+against the effective codebook size (linear scaling is slope 1).
 """
 from __future__ import annotations
 
@@ -78,6 +85,111 @@ def cpu_baseline(x, w, min_seconds: float, max_passes: int):
                       f"each, assign + aggregate + attention in fp64) in {dt:.1f} s wall"}
 
 
+class Runner:
+    """Device buffers of one workload and its timed step (the three entry
+    points on torch's current stream)."""
+
+    def __init__(self, w, x, dev):
+        import torch
+        from paper_2607_12789_amd import avq
+        self.avq, self.w = avq, w
+        self.xd = {k: v.to(dev) for k, v in x.items()}
+        B, H, N, d = w.B, w.H, w.N, w.d
+        self.par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
+        self.code = torch.empty_like(self.par)
+        self.packed = torch.empty((B, H, avq.packed_bytes(w.torch_dtype, w.M0, w.Ch, d)),
+                                  dtype=torch.uint8, device=dev)
+        self.counts = torch.empty((B, H, w.Mtot), dtype=torch.int32, device=dev)
+        self.Y = torch.empty_like(self.xd["Q"])
+
+    def step(self, ev=None):
+        # ev: four events bracketing the three launches (HIP events on the
+        # stream the kernels are launched on, which is torch's current one)
+        avq, w, xd = self.avq, self.w, self.xd
+        if ev: ev[0].record()
+        avq.assign(xd["K"], xd["Cp"], xd["Cc"], self.par, self.code)
+        if ev: ev[1].record()
+        avq.aggregate(xd["V"], self.code, w.M0, w.Ch, self.packed, self.counts)
+        if ev: ev[2].record()
+        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], self.packed, w.P, w.block_q, Y=self.Y)
+        if ev: ev[3].record()
+
+    def timed(self, steps: int, warmup: int):
+        """Runs warmup + steps steps; returns (wall ms per step, per-step event
+        durations [steps][3] in ms: assign, aggregate, attention)."""
+        import torch
+        for _ in range(warmup):
+            self.step()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(evs[i])
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / steps
+        return wall, [[ev[k].elapsed_time(ev[k + 1]) for k in range(3)] for ev in evs]
+
+
+def _median(v):
+    v = sorted(v)
+    n = len(v)
+    return v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2])
+
+
+def _slope(xs, ys):
+    """Least-squares slope of log y against log x."""
+    lx = [math.log(a) for a in xs]
+    ly = [math.log(b) for b in ys]
+    mx, my = sum(lx) / len(lx), sum(ly) / len(ly)
+    num = sum((a - mx) * (b - my) for a, b in zip(lx, ly))
+    den = sum((a - mx) ** 2 for a in lx)
+    return num / den if den > 0 else float("nan")
+
+
+def sweep(args):
+    import torch
+    from paper_2607_12789_amd import inputs
+    dev = torch.device("cuda:0")
+    rows = []
+    for w in inputs.scaling_workloads():
+        x = inputs.generate(w)
+        r = Runner(w, x, dev)
+        wall, per = r.timed(args.steps, args.warmup)
+        step_ms = _median([sum(p) for p in per])
+        k = [_median([p[i] for p in per]) for i in range(3)]
+        qh = w.B * w.H * w.N
+        row = {"sweep": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "M0": w.M0, "Ch": w.Ch,
+               "P": w.P, "block_q": w.block_q, "dtype": w.dtype,
+               "codes_precompute": w.M0 * (1 + w.Ch), "codes_attention": w.M0 + w.P * w.Ch,
+               "ms_median": step_ms, "ms_wall_mean": wall, "qh_per_s": qh / (step_ms * 1e-3),
+               "kernels_ms_median": {"assign": k[0], "aggregate": k[1], "attention_fwd": k[2]},
+               "steps": args.steps, "warmup": args.warmup}
+        rows.append(row)
+        print(json.dumps(row), flush=True)
+        del r, x
+        torch.cuda.empty_cache()
+    # slopes against N for each codebook, and against the attention's
+    # effective codebook size M0 + P Ch at each N
+    by_cb, by_n = {}, {}
+    for row in rows:
+        by_cb.setdefault(row["sweep"].split("@")[0], []).append(row)
+        by_n.setdefault(row["N"], []).append(row)
+    summary = {
+        "sweep_summary": "log-log slopes of median step time (1 = linear)",
+        "slope_vs_N": {cb: round(_slope([r["N"] for r in v], [r["ms_median"] for r in v]), 3)
+                       for cb, v in by_cb.items()},
+        "slope_vs_N_16k_64k": {
+            cb: round(_slope([r["N"] for r in v if r["N"] >= 16384],
+                             [r["ms_median"] for r in v if r["N"] >= 16384]), 3)
+            for cb, v in by_cb.items()},
+        "attention_slope_vs_codes": {
+            str(n): round(_slope([r["codes_attention"] for r in v],
+                                 [r["kernels_ms_median"]["attention_fwd"] for r in v]), 3)
+            for n, v in by_n.items()},
+    }
+    print(json.dumps(summary), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -90,6 +202,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also launch one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="run the sequence-length scaling sweep instead")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -104,45 +218,16 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.sweep:
+        sweep(args)
+        return
     w = inputs.WORKLOADS[args.workload]
     x = inputs.generate(w)
     dev = torch.device("cuda:0")
-    xd = {k: v.to(dev) for k, v in x.items()}
     B, H, N, d, M0, Ch, P = w.B, w.H, w.N, w.d, w.M0, w.Ch, w.P
-    par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
-    code = torch.empty_like(par)
-    packed = torch.empty((B, H, avq.packed_bytes(w.torch_dtype, M0, Ch, d)), dtype=torch.uint8,
-                         device=dev)
-    counts = torch.empty((B, H, w.Mtot), dtype=torch.int32, device=dev)
-    Y = torch.empty_like(xd["Q"])
-
-    def step(ev=None):
-        # ev: four events bracketing the three launches (HIP events on the
-        # stream the kernels are launched on, which is torch's current one)
-        if ev: ev[0].record()
-        avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code)
-        if ev: ev[1].record()
-        avq.aggregate(xd["V"], code, M0, Ch, packed, counts)
-        if ev: ev[2].record()
-        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, P, w.block_q, Y=Y)
-        if ev: ev[3].record()
-
-    for _ in range(args.warmup):
-        step()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-
+    ms_per_step, per = Runner(w, x, dev).timed(args.steps, args.warmup)
     # per-kernel average launch duration over the timed steps
-    def avg_ms(a, b):
-        return sum(ev[a].elapsed_time(ev[b]) for ev in evs) / max(len(evs), 1)
-
-    t_assign, t_agg, t_attn = avg_ms(0, 1), avg_ms(1, 2), avg_ms(2, 3)
+    t_assign, t_agg, t_attn = (sum(p[i] for p in per) / max(len(per), 1) for i in range(3))
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)

@@ -36,9 +36,12 @@
  *     non-OK status means nothing was enqueued (AVQ_ERR_DEVICE: a launch was
  *     rejected). avq_last_error() then returns a message for the calling
  *     thread. Non-finite inputs are not checked; they propagate.
- *   - Supported: d in {64, 128}; Ch in {1, 2, 4, 8, 16}; 1 <= M0 <= 512;
+ *   - Supported: d in {64, 128}; Ch in {0, 1, 2, 4, 8, 16}; 1 <= M0 <= 512;
  *     1 <= N <= 2^24, B >= 1, H >= 1 and B*H*N*d < 2^31. Other shapes return
  *     AVQ_ERR_UNSUPPORTED.
+ *   - Ch = 0 is a flat codebook of M0 codewords (plain vector quantisation,
+ *     Sec. 3.2): Cc may then be NULL, every code is a parent (Mtot = M0),
+ *     and avq_attention_fwd needs P = 0, which is VQ attention (Sec. 3.2).
  */
 #ifndef AVQ_H
 #define AVQ_H
@@ -73,12 +76,12 @@ const char* avq_last_error(void);
  *   parent_idx = p* = argmin_p ||K_j - Cp[h][p]||^2, lowest p on exact ties;
  *   c*            = argmin_c ||K_j - Cc[h][p*][c]||^2, lowest c on exact ties;
  *   code_idx      = M0 + p* * Ch + c* if that child distance is strictly below
- *                   the parent distance, else p*.
+ *                   the parent distance, else p* (always p* when Ch = 0).
  * Distances are evaluated in fp32 from the stored inputs.
  *
  *   K            [B][H][N][d]   dtype
  *   Cp           [H][M0][d]     dtype
- *   Cc           [H][M0][Ch][d] dtype
+ *   Cc           [H][M0][Ch][d] dtype (NULL allowed when Ch = 0)
  *   parent_idx   [B][H][N]      int32, out
  *   code_idx     [B][H][N]      int32, out
  */
@@ -90,7 +93,7 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
 /*
  * Bytes of the packed aggregates of one (batch, head) (see avq_aggregate) for
  * the given dtype and sizes. Returns -1 for an unknown dtype or sizes outside
- * 1 <= M0 <= 512, 1 <= Ch <= 16, 1 <= d <= 128.
+ * 1 <= M0 <= 512, 0 <= Ch <= 16, 1 <= d <= 128.
  */
 int64_t avq_packed_bytes(avq_dtype_t dtype, int32_t M0, int32_t Ch, int32_t d);
 
@@ -122,8 +125,8 @@ int64_t avq_packed_bytes(avq_dtype_t dtype, int32_t M0, int32_t Ch, int32_t d);
  *             means first, info right after it.
  * At least one of Vbar and packed must be given.
  *
- * Every sum is accumulated in fp32 by the one quarter wave that owns the
- * parent family, keys in bucket order; counts are exact.
+ * Every sum is accumulated in fp32 by the one half wave that owns the parent
+ * family, keys in bucket order; counts are exact.
  */
 avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
                            int32_t M0, int32_t Ch, const void* V, const int32_t* code_idx,
@@ -150,11 +153,11 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
  *   output       Y_i = Xbar_i / Zbar_i.
  * P = 0 gives plain VQ attention over the parents (Sec. 3.2).
  *
- *   P            0 <= P <= M0
+ *   P            0 <= P <= M0; P = 0 when Ch = 0
  *   block_q      query tile size, 1 <= block_q <= 256 (semantic: importance
  *                and top-P are computed per tile of block_q tokens)
  *   Q            [B][H][N][d]    dtype
- *   Cp, Cc       as in avq_assign
+ *   Cp, Cc       as in avq_assign (Cc NULL allowed when Ch = 0)
  *   packed       the packed aggregates written by avq_aggregate (required)
  *   Y            [B][H][N][d]    dtype, out
  *   topp_idx     [B][H][T][P]    int32, out, nullable; T = ceil(N / block_q);

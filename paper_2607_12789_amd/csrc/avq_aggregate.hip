@@ -39,8 +39,8 @@ constexpr int kQueueCap = 8192;                        // queued keys per flush
 constexpr int kMaxRows = kFamilies * 17;               // families x (1 + Ch), Ch <= 16
 // value rows in flight per family: as many as the registers beside the
 // family table (1 + CHM rows of D / 32 sums per lane) allow
-template <int CHM>
-constexpr int kInFlight = CHM > 8 ? 4 : 8;
+template <int CHM, typename T>
+constexpr int kInFlight = CHM > 8 ? 4 : (CHM == 0 && sizeof(T) == 2) ? 16 : 8;
 
 struct AggLds {
   int qkey[kQueueCap];       // queued keys, key order
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   const int rows = nfam * (1 + Ch);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int sub = lane % kFamLanes, fam = tid / kFamLanes;
-  const int ch_shift = 31 - __builtin_clz(Ch);
+  const int ch_shift = Ch > 0 ? 31 - __builtin_clz(Ch) : 0;  // Ch = 0: a flat codebook
 
   for (int r = tid; r < kMaxRows; r += kAggThreads) L.total[r] = 0;
 
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         L.skey[atomicAdd(&L.cursor[L.qrow[e]], 1)] = L.qkey[e];
       __syncthreads();
       if (fam < nfam) {
-        // the family's keys, bucketed by row, in kInFlight<CHM> batches; the
+        // the family's keys, bucketed by row, in kInFlight<CHM, T> batches; the
         // running row sum goes into the table when its row ends
         const int r_begin = fam * (1 + Ch);
         const int kb = L.start[r_begin], ke = L.start[r_begin + 1 + Ch];
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
 #pragma unroll
           for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
         };
-        constexpr int kIF = kInFlight<CHM>;
+        constexpr int kIF = kInFlight<CHM, T>;
         for (int k0 = kb; k0 < ke; k0 += kIF) {
           Raw raw[kIF];
 #pragma unroll
@@ -422,8 +422,8 @@ hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
   static_assert(kRound <= kQueueCap, "one round of codes fits the queue");
   const int ranges = (M0 + kFamilies - 1) / kFamilies;
   const int lds = (int)sizeof(AggLds);
-  hipError_t e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM>, lds,
-                                    (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0) + (CHM == 16 ? 1 : 0));
+  constexpr int slot = (CHM == 0 ? 40 : CHM == 16 ? 1 : 0) + (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0);
+  hipError_t e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM>, lds, slot);
   if (e != hipSuccess) return e;
   const long long grid = (long long)BH * ranges;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
@@ -437,6 +437,8 @@ template <typename T, int D>
 hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
                               const int32_t* code_idx, float* Vbar, int32_t* counts,
                               void* packed, hipStream_t stream) {
+  if (Ch == 0)  // flat codebook: a family is one parent
+    return launch_aggregate_dc<T, D, 0>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
   if (Ch <= 8)
     return launch_aggregate_dc<T, D, 8>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
   if (Ch <= 16)

@@ -96,12 +96,13 @@ avq_status_t check_common(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, in
                           int32_t M0, int32_t Ch) {
   if (dtype != AVQ_F32 && dtype != AVQ_BF16)
     return fail(AVQ_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
-  if (B < 1 || H < 1 || N < 1 || d < 1 || M0 < 1 || Ch < 1)
-    return fail(AVQ_ERR_INVALID_ARG, "sizes must be positive (B=%d H=%d N=%d d=%d M0=%d Ch=%d)",
-                B, H, N, d, M0, Ch);
+  if (B < 1 || H < 1 || N < 1 || d < 1 || M0 < 1 || Ch < 0)
+    return fail(AVQ_ERR_INVALID_ARG,
+                "sizes must be positive, Ch not negative (B=%d H=%d N=%d d=%d M0=%d Ch=%d)", B, H,
+                N, d, M0, Ch);
   if (d != 64 && d != 128) return fail(AVQ_ERR_UNSUPPORTED, "d=%d: only 64 and 128", d);
-  if (Ch != 1 && Ch != 2 && Ch != 4 && Ch != 8 && Ch != 16)
-    return fail(AVQ_ERR_UNSUPPORTED, "Ch=%d: only 1, 2, 4, 8, 16", Ch);
+  if (Ch != 0 && Ch != 1 && Ch != 2 && Ch != 4 && Ch != 8 && Ch != 16)
+    return fail(AVQ_ERR_UNSUPPORTED, "Ch=%d: only 0 (flat codebook), 1, 2, 4, 8, 16", Ch);
   if (M0 > 512) return fail(AVQ_ERR_UNSUPPORTED, "M0=%d: at most 512", M0);
   if (N > (1 << 24)) return fail(AVQ_ERR_UNSUPPORTED, "N=%d: at most 2^24 keys per head", N);
   const long long elems = (long long)B * H * N * d;
@@ -116,13 +117,13 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 extern "C" {
 
-int avq_version(void) { return 200; }
+int avq_version(void) { return 201; }
 
 const char* avq_last_error(void) { return g_err; }
 
 int64_t avq_packed_bytes(avq_dtype_t dtype, int32_t M0, int32_t Ch, int32_t d) {
   if (dtype != AVQ_F32 && dtype != AVQ_BF16) return -1;
-  if (M0 < 1 || Ch < 1 || d < 1 || M0 > 512 || Ch > 16 || d > 128) return -1;
+  if (M0 < 1 || Ch < 0 || d < 1 || M0 > 512 || Ch > 16 || d > 128) return -1;
   return (int64_t)avq::packed_layout(M0, Ch, d, dtype == AVQ_BF16 ? 2 : 4).bytes;
 }
 
@@ -131,7 +132,7 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
                         int32_t* parent_idx, int32_t* code_idx, void* stream) {
   avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
   if (st != AVQ_OK) return st;
-  if (!K || !Cp || !Cc || !parent_idx || !code_idx)
+  if (!K || !Cp || (!Cc && Ch > 0) || !parent_idx || !code_idx)
     return fail(AVQ_ERR_INVALID_ARG, "avq_assign: null pointer argument");
   if (!aligned16(K) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(parent_idx) ||
       !aligned16(code_idx))
@@ -177,9 +178,11 @@ avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t 
   avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
   if (st != AVQ_OK) return st;
   if (P < 0 || P > M0) return fail(AVQ_ERR_INVALID_ARG, "P=%d outside [0, M0=%d]", P, M0);
+  if (Ch == 0 && P != 0)
+    return fail(AVQ_ERR_INVALID_ARG, "P=%d with a flat codebook (Ch=0): must be 0", P);
   if (block_q < 1) return fail(AVQ_ERR_INVALID_ARG, "block_q=%d must be positive", block_q);
   if (block_q > 256) return fail(AVQ_ERR_UNSUPPORTED, "block_q=%d: at most 256", block_q);
-  if (!Q || !Cp || !Cc || !packed || !Y)
+  if (!Q || !Cp || (!Cc && Ch > 0) || !packed || !Y)
     return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: null pointer argument");
   if (!aligned16(Q) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(packed) ||
       !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance))

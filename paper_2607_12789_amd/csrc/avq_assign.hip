@@ -112,7 +112,8 @@ __device__ __forceinline__ float row_norm(const T* row) {
 template <typename T, int D>
 __global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict__ K,
                                                             const T* __restrict__ Cp,
-                                                            int32_t* __restrict__ parent_idx, int H,
+                                                            int32_t* __restrict__ parent_idx,
+                                                            int32_t* __restrict__ code_idx, int H,
                                                             int N, int M0, int blocks_per_bh) {
   using Cfg = AssignCfg<T, D>;
   constexpr bool kB = Cfg::kB;
@@ -228,7 +229,10 @@ __global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict_
       }
     }
     const int j = key0 + 16 * s + c;
-    if (g == 0 && j < N) parent_idx[(size_t)bh * N + j] = bidx[s];
+    if (g == 0 && j < N) {
+      parent_idx[(size_t)bh * N + j] = bidx[s];
+      if (code_idx) code_idx[(size_t)bh * N + j] = bidx[s];  // flat codebook
+    }
   }
 }
 
@@ -261,7 +265,8 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void parent_stream_kernel(const T* __restrict__ K,
                                                             const T* __restrict__ Cp,
                                                             int32_t* __restrict__ parent_idx,
-                                                            int H, int N, int M0, int steps_per_bh,
+                                                            int32_t* __restrict__ code_idx, int H,
+                                                            int N, int M0, int steps_per_bh,
                                                             int n_steps) {
   using Cfg = StreamCfg<T, D>;
   constexpr bool kB = Cfg::kB;
@@ -420,7 +425,10 @@ __global__ __launch_bounds__(256) void parent_stream_kernel(const T* __restrict_
         }
       }
       const int j = key0 + 16 * s + c;
-      if (g == 0 && j < N) parent_idx[(size_t)bh * N + j] = bidx[s];
+      if (g == 0 && j < N) {
+        parent_idx[(size_t)bh * N + j] = bidx[s];
+        if (code_idx) code_idx[(size_t)bh * N + j] = bidx[s];  // flat codebook
+      }
     }
   }
 }
@@ -676,8 +684,8 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
     e = ensure_dynamic_lds((const void*)parent_stream_kernel<T, D>, SCfg::LDS_HALF, slot_s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid), dim3(256), lds, stream,
-                       static_cast<const T*>(K), static_cast<const T*>(Cp), parent_idx, H, N,
-                       M0, per_bh, (int)n_steps);
+                       static_cast<const T*>(K), static_cast<const T*>(Cp), parent_idx,
+                       Ch == 0 ? code_idx : nullptr, H, N, M0, per_bh, (int)n_steps);
   } else {
     const int per_bh = (N + Cfg::kKeysPerBlock - 1) / Cfg::kKeysPerBlock;
     grid = (long long)BH * per_bh;
@@ -687,10 +695,12 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid), dim3(256),
                        Cfg::LDS_BYTES, stream, static_cast<const T*>(K),
-                       static_cast<const T*>(Cp), parent_idx, H, N, M0, per_bh);
+                       static_cast<const T*>(Cp), parent_idx, Ch == 0 ? code_idx : nullptr, H, N,
+                       M0, per_bh);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (Ch == 0) return hipSuccess;  // flat codebook: the parent is the code
 
   // child compare: F parents per workgroup
   const int F = kMaxFam;

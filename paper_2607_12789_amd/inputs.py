@@ -18,6 +18,9 @@ Workload recipe (one generator, NumPy PCG64, fp64 draws, fixed draw order):
 6. Every tensor is rounded to the storage dtype (fp64 -> fp32 -> bf16, each
    step round-to-nearest-even). Both sides receive the same rounded tensors.
 
+A flat codebook (``Ch = 0``) skips step 2 (``Cc`` is ``[H, M0, 0, d]``) and
+draws the key components over the parents in step 3.
+
 The paper's own workloads (keys of trained ViT-B / DPT-L models, Sec. 5)
 are not available; these Gaussian-mixture keys stand in for them.
 """
@@ -68,8 +71,9 @@ class Workload:
         return dataclasses.replace(self, **kw)
 
     def describe(self) -> str:
-        mix = ("uniform children" if self.dirichlet_alpha is None
-               else f"Dirichlet({self.dirichlet_alpha}) children")
+        unit = "children" if self.Ch > 0 else "parents (flat codebook)"
+        mix = (f"uniform {unit}" if self.dirichlet_alpha is None
+               else f"Dirichlet({self.dirichlet_alpha}) {unit}")
         return (f"B={self.B} H={self.H} N={self.N} d={self.d} {self.dtype} "
                 f"M0={self.M0} Ch={self.Ch} P={self.P} Bq={self.block_q}; "
                 f"keys: {mix}, sigma_c={self.sigma_c}, sigma_k={self.sigma_k}; "
@@ -91,6 +95,21 @@ WORKLOADS = {
                    dirichlet_alpha=0.3),
 }
 
+# The sequence-length sweep of the scaling analysis (Sec. 5, scaling table):
+# B=4, H=12, d=64, N in {1k, 4k, 16k, 64k}; flat codebooks of M = 256 and 512
+# codewords (P = 0) and tree codebooks M0/P/Ch = 64/8/8, 64/16/8, 128/8/8,
+# 128/16/8. The query block is not given there; 128 is used throughout.
+SCALING_N = (1024, 4096, 16384, 65536)
+SCALING_CODEBOOKS = (("vq256", 256, 0, 0), ("vq512", 512, 0, 0), ("avq64/8/8", 64, 8, 8),
+                     ("avq64/16/8", 64, 8, 16), ("avq128/8/8", 128, 8, 8),
+                     ("avq128/16/8", 128, 8, 16))
+
+
+def scaling_workloads(ns=SCALING_N):
+    """The sweep's workloads, codebook-major (name, M0, Ch, P per codebook)."""
+    return [Workload(f"{name}@N={n}", B=4, H=12, N=n, d=64, M0=M0, Ch=Ch, P=P, block_q=128)
+            for name, M0, Ch, P in SCALING_CODEBOOKS for n in ns]
+
 
 def _round(x: np.ndarray, dtype: str) -> torch.Tensor:
     t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64)).to(torch.float32)
@@ -109,19 +128,24 @@ def generate(w: Workload) -> dict:
     rng = np.random.default_rng(w.seed)
     B, H, N, d, M0, Ch = w.B, w.H, w.N, w.d, w.M0, w.Ch
     cp = rng.standard_normal((H, M0, d))
-    eps = w.sigma_c * rng.standard_normal((H, M0, Ch, d))
-    eps -= eps.mean(axis=2, keepdims=True)
-    cc = cp[:, :, None, :] + eps
-    cc_flat = cc.reshape(H, M0 * Ch, d)
+    if Ch > 0:
+        eps = w.sigma_c * rng.standard_normal((H, M0, Ch, d))
+        eps -= eps.mean(axis=2, keepdims=True)
+        cc = cp[:, :, None, :] + eps
+        comps = cc.reshape(H, M0 * Ch, d)
+    else:  # flat codebook: keys around the parents
+        cc = np.zeros((H, M0, 0, d))
+        comps = cp
+    n_comp = comps.shape[1]
     k = np.empty((B, H, N, d))
     for b in range(B):
         for h in range(H):
             if w.dirichlet_alpha is None:
-                comp = rng.integers(0, M0 * Ch, size=N)
+                comp = rng.integers(0, n_comp, size=N)
             else:
-                pi = rng.dirichlet(np.full(M0 * Ch, w.dirichlet_alpha))
-                comp = rng.choice(M0 * Ch, size=N, p=pi)
-            k[b, h] = cc_flat[h, comp] + w.sigma_k * rng.standard_normal((N, d))
+                pi = rng.dirichlet(np.full(n_comp, w.dirichlet_alpha))
+                comp = rng.choice(n_comp, size=N, p=pi)
+            k[b, h] = comps[h, comp] + w.sigma_k * rng.standard_normal((N, d))
     q = (w.q_scale / math.sqrt(d)) * rng.standard_normal((B, H, N, d))
     v = rng.standard_normal((B, H, N, d))
     return {

@@ -118,6 +118,8 @@ def check_assign(x, w, g, o) -> tuple:
     op, oc = o["parent_idx"], o["code_idx"]
     bad = par_cert & (gp != op)
     assert not bad.any(), f"{bad.sum()} certified parent decisions differ, e.g. at {np.argwhere(bad)[:5]}"
+    if w.Ch == 0:
+        return _check_flat_assign(K, Cp, w, gp, gc, op, err_p, par_cert)
 
     # child compare: bound both the direct form and ||c||^2 - 2 k.c (bf16)
     cn = np.maximum(np.linalg.norm(Cc, axis=-1).max(axis=(-1, -2)),
@@ -152,6 +154,20 @@ def check_assign(x, w, g, o) -> tuple:
     rep = Report(keys=int(diff.size), uncertified=int((~code_cert).sum()),
                  differing=int(diff.sum()), heads_excluded=int((~clean).sum()),
                  moved_frac=round(float((oc >= w.M0).mean()), 4))
+    return clean, rep
+
+
+def _check_flat_assign(K, Cp, w, gp, gc, op, err_p, par_cert) -> tuple:
+    """Flat codebook: the code is the parent, exactly; an uncertified parent
+    that differs from the oracle's must be within the bound of the nearest."""
+    np.testing.assert_array_equal(gc, gp)
+    diff = gp != op
+    for b, h, j in np.argwhere(diff):
+        dp = ((Cp[h] - K[b, h, j]) ** 2).sum(-1)
+        assert dp[gp[b, h, j]] <= dp.min() + 4 * err_p[b, h, j], "invalid parent choice"
+    clean = ~diff.any(axis=-1)
+    rep = Report(keys=int(diff.size), uncertified=int((~par_cert).sum()),
+                 differing=int(diff.sum()), heads_excluded=int((~clean).sum()), moved_frac=0.0)
     return clean, rep
 
 

@@ -37,7 +37,7 @@ def test_header_declares_the_entry_points():
 def test_library_exports_every_declared_symbol(L):
     for name in declared_functions():
         assert hasattr(L, name), name
-    assert L.avq_version() == 200
+    assert L.avq_version() == 201
 
 
 NULL = None
@@ -59,7 +59,7 @@ def attn(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,
 @pytest.mark.parametrize("kw,status", [
     (dict(dtype=7), INVALID),
     (dict(B=0), INVALID), (dict(H=-1), INVALID), (dict(N=0), INVALID), (dict(M0=0), INVALID),
-    (dict(Ch=0), INVALID),
+    (dict(Ch=-1), INVALID),
     (dict(d=96), UNSUPPORTED), (dict(d=32), UNSUPPORTED), (dict(Ch=3), UNSUPPORTED),
     (dict(Ch=32), UNSUPPORTED), (dict(M0=513), UNSUPPORTED),
     (dict(B=1 << 14, H=1 << 10, N=1 << 10, d=128), UNSUPPORTED),
@@ -99,6 +99,8 @@ def test_packed_size(L):
     assert L.avq_packed_bytes(BF16, 256, 8, 128) == (32 + 256 + 1) * (2048 + 64)
     assert L.avq_packed_bytes(F32, 37, 16, 64) == expect(37, 16, 64, 4)
     assert L.avq_packed_bytes(BF16, 5, 2, 64) == expect(5, 2, 64, 2)
+    assert L.avq_packed_bytes(BF16, 100, 0, 64) == expect(100, 0, 64, 2)  # flat codebook
+    assert L.avq_packed_bytes(BF16, 4, -1, 64) == -1
     assert L.avq_packed_bytes(BF16, 0, 2, 64) == -1
     assert L.avq_packed_bytes(BF16, 4, 2, -1) == -1
     assert L.avq_packed_bytes(7, 4, 2, 64) == -1
@@ -116,6 +118,22 @@ def test_misaligned_pointers_are_rejected(L):
                                          (1, 257, UNSUPPORTED)])
 def test_attention_argument_validation(L, P, bq, status):
     assert attn(L, P=P, bq=bq) == status
+
+
+def test_flat_codebook_arguments(L):
+    # Ch = 0: no children to select, so P must be 0
+    assert attn(L, Ch=0, P=1) == INVALID
+    assert "flat" in L.avq_last_error().decode()
+    # Cc may be NULL: validation goes on to the next problem (here a
+    # misaligned output), which also proves nothing was launched
+    odd = ctypes.c_void_p(24)
+    assert assign(L, Ch=0, ptrs=(FAKE, FAKE, NULL, odd, FAKE)) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
+    assert attn(L, Ch=0, P=0, ptrs=(FAKE, FAKE, NULL, FAKE, odd)) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
+    # with children, Cc is required
+    assert assign(L, Ch=2, ptrs=(FAKE, FAKE, NULL, FAKE, FAKE)) == INVALID
+    assert "null" in L.avq_last_error().decode()
 
 
 def test_binding_refuses_cpu_tensors():

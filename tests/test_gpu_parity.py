@@ -70,6 +70,13 @@ EDGE = {
     "m0_24_split": small(M0=24, Ch=2, P=5, B=1, H=1, N=700),
     "m0_44_split": small(M0=44, Ch=4, P=5, B=1, H=1, N=700),
     "fp32_ch16_d64": small(dtype="f32", M0=70, Ch=16, P=9, N=600),
+    # flat codebook (Ch = 0): VQ attention over the parents alone
+    "flat": small(Ch=0, P=0),
+    "flat_n_one": small(Ch=0, P=0, N=1, B=1, H=1),
+    "flat_fp32_ragged": small(Ch=0, P=0, dtype="f32", N=777, block_q=100),
+    "flat_fp32_d128": small(Ch=0, P=0, dtype="f32", d=128, block_q=64),
+    "flat_m0_300_split": small(Ch=0, P=0, M0=300, B=1, H=1, N=2000),
+    "flat_m0_512_d128": small(Ch=0, P=0, M0=512, d=128, N=1536, B=1, H=2, block_q=256),
 }
 
 

@@ -161,6 +161,31 @@ def test_p0_is_vq_attention():
                                        rtol=1e-10, atol=1e-12)
 
 
+def test_flat_codebook_is_vq_attention():
+    """Ch = 0 (a flat codebook, the VQ attention of Sec. 3.2): every key takes
+    its nearest parent (scipy cdist), the aggregates are a bincount, and the
+    output is per-key softmax attention with each key replaced by that
+    codeword (SDPA route). It also equals the P = 0 output of the same keys
+    and parents under a tree codebook, whose children P = 0 never reads."""
+    w = small(Ch=0, P=0, N=130, block_q=32)
+    x = inputs.generate(w)
+    assert x["Cc"].shape == (w.H, w.M0, 0, w.d)
+    o = run(x, w)
+    Q, K, V, Cp = np64(x["Q"]), np64(x["K"]), np64(x["V"]), np64(x["Cp"])
+    for b in range(w.B):
+        for h in range(w.H):
+            idx, _ = ref.nearest(K[b, h], Cp[h])
+            np.testing.assert_array_equal(o["parent_idx"][b, h], idx)
+            np.testing.assert_array_equal(o["code_idx"][b, h], idx)
+            np.testing.assert_array_equal(o["counts"][b, h], np.bincount(idx, minlength=w.M0))
+            np.testing.assert_allclose(o["Y"][b, h], ref.sdpa(Q[b, h], Cp[h][idx], V[b, h]),
+                                       rtol=1e-10, atol=1e-12)
+    tree = dict(x, Cc=x["Cp"][:, :, None, :].repeat(1, 1, 3, 1) * 1.5)
+    ot = oracle.forward(tree["Q"], tree["K"], tree["V"], tree["Cp"], tree["Cc"], 0, w.block_q)
+    np.testing.assert_allclose(o["Y"], ot["Y"], rtol=1e-12, atol=1e-14)
+    assert o["selection"].shape[-1] == 0
+
+
 def test_one_codeword_per_key_is_exact_attention():
     """Codebook = the keys (M0 = N, distinct keys) and P = 0: exact softmax
     attention, Eq. (standardattention), through torch SDPA."""
