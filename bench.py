@@ -89,10 +89,10 @@ class Runner:
     """Device buffers of one workload and its timed step (the three entry
     points on torch's current stream)."""
 
-    def __init__(self, w, x, dev):
+    def __init__(self, w, x, dev, tiled=False):
         import torch
         from paper_2607_12789_amd import avq
-        self.avq, self.w = avq, w
+        self.avq, self.w, self.tiled = avq, w, tiled
         self.xd = {k: v.to(dev) for k, v in x.items()}
         B, H, N, d = w.B, w.H, w.N, w.d
         self.par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
@@ -111,7 +111,8 @@ class Runner:
         if ev: ev[1].record()
         avq.aggregate(xd["V"], self.code, w.M0, w.Ch, self.packed, self.counts)
         if ev: ev[2].record()
-        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], self.packed, w.P, w.block_q, Y=self.Y)
+        avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], self.packed, w.P, w.block_q, Y=self.Y,
+                          tiled_importance=self.tiled)
         if ev: ev[3].record()
 
     def timed(self, steps: int, warmup: int):
@@ -137,7 +138,9 @@ def _median(v):
 
 
 def _slope(xs, ys):
-    """Least-squares slope of log y against log x."""
+    """Least-squares slope of log y against log x (nan below two points)."""
+    if len(xs) < 2:
+        return float("nan")
     lx = [math.log(a) for a in xs]
     ly = [math.log(b) for b in ys]
     mx, my = sum(lx) / len(lx), sum(ly) / len(ly)
@@ -152,6 +155,9 @@ def sweep(args):
     dev = torch.device("cuda:0")
     rows = []
     for w in inputs.scaling_workloads():
+        if args.sweep_only and not any(f == w.name or f == w.name.split("@")[0]
+                                       for f in args.sweep_only.split(",")):
+            continue
         x = inputs.generate(w)
         r = Runner(w, x, dev)
         wall, per = r.timed(args.steps, args.warmup)
@@ -202,8 +208,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also launch one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--tiled-importance", action="store_true",
+                    help="use the App. B importance (one parent sweep) instead of the exact one")
     ap.add_argument("--sweep", action="store_true",
                     help="run the sequence-length scaling sweep instead")
+    ap.add_argument("--sweep-only", default="",
+                    help="comma-separated sweep workloads (e.g. vq256@N=65536) or codebooks "
+                         "(e.g. avq64/8/8) to run")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -225,7 +236,7 @@ def main():
     x = inputs.generate(w)
     dev = torch.device("cuda:0")
     B, H, N, d, M0, Ch, P = w.B, w.H, w.N, w.d, w.M0, w.Ch, w.P
-    ms_per_step, per = Runner(w, x, dev).timed(args.steps, args.warmup)
+    ms_per_step, per = Runner(w, x, dev, args.tiled_importance).timed(args.steps, args.warmup)
     # per-kernel average launch duration over the timed steps
     t_assign, t_agg, t_attn = (sum(p[i] for p in per) / max(len(per), 1) for i in range(3))
     if args.calib_copy_mib > 0:
@@ -238,7 +249,7 @@ def main():
     qh = B * H * N
     flops_attn = 4.0 * d * (M0 + P * Ch) * qh
     achieved = flops_attn / (t_attn * 1e-3) / 1e12
-    traffic = read_traffic()
+    traffic = None if args.tiled_importance else read_traffic()
     line = {
         "metric": METRIC,
         "value": qh / (ms_per_step * 1e-3),
@@ -253,9 +264,12 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.describe()}", "B": B, "H": H, "N": N, "d": d,
-                   "M0": M0, "Ch": Ch, "P": P, "block_q": w.block_q},
+                   "M0": M0, "Ch": Ch, "P": P, "block_q": w.block_q,
+                   "importance": "tiled (App. B, 64-parent tiles)" if args.tiled_importance
+                   else "exact"},
         "kernels_ms": {"assign": t_assign, "aggregate": t_agg, "attention_fwd": t_attn},
-        "roofline": {"kernel": "avq_attention_fwd", "bound": "mfma", "achieved": achieved,
+        "roofline": {"kernel": "avq_attention_fwd_tiled" if args.tiled_importance
+                     else "avq_attention_fwd", "bound": "mfma", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                      "flops_per_launch": flops_attn},

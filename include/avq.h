@@ -15,6 +15,8 @@
  *                      attention and normalisation (Sec. 4.3,
  *                      Eq. (vqflashattention), (importance),
  *                      (parent_recovery), (correcting_attention), Alg. 2)
+ *   avq_attention_fwd_tiled  the same with the tiled-codeword importance of
+ *                      App. B (Eq. (aproxdenom), (codewordimportance))
  *
  * Conventions shared by every call:
  *   - Every array argument is a DEVICE pointer owned by the caller, contiguous,
@@ -179,6 +181,33 @@ avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t 
                                const void* Cc, const void* packed, void* Y,
                                int32_t* topp_idx, float* importance,
                                void* stream);
+
+/* Parents per codeword tile of avq_attention_fwd_tiled. */
+#define AVQ_IMPORTANCE_TILE 64
+
+/*
+ * avq_attention_fwd_tiled - avq_attention_fwd with the importance of App. B
+ * (computing importance with tiled codewords), in one parent sweep.
+ *
+ * The parents are visited in tiles of AVQ_IMPORTANCE_TILE (parents
+ * 64t .. 64t+63). After tile J the partial denominator of query i, the sum of
+ * A_ip n_p over the parents of tiles up to J, is extrapolated to all keys
+ * (Eq. (aproxdenom)): Ztilde_i(J) = N / N_seen(J) * partial, N_seen(J) being
+ * the number of keys whose parent lies in those tiles; the importance of each
+ * parent p of tile J is w_p(I) = sum_{i in I} A_ip n_p / Ztilde_i(J)
+ * (Eq. (codewordimportance)). A tile whose parents hold no key adds nothing.
+ * The last tile has N_seen = N, so with M0 <= AVQ_IMPORTANCE_TILE this is
+ * Eq. (importance) and the call equals avq_attention_fwd. Top-P, the child
+ * pass and the output are as in avq_attention_fwd, on this importance.
+ *
+ * Arguments, layouts, ownership, arithmetic and errors as avq_attention_fwd
+ * (importance, when given, receives this w).
+ */
+avq_status_t avq_attention_fwd_tiled(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                                     int32_t d, int32_t M0, int32_t Ch, int32_t P,
+                                     int32_t block_q, const void* Q, const void* Cp,
+                                     const void* Cc, const void* packed, void* Y,
+                                     int32_t* topp_idx, float* importance, void* stream);
 
 #ifdef __cplusplus
 }

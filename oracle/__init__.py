@@ -56,6 +56,8 @@ def open_library(path):
                                 _f64p, _f64p, _f64p, _f64p]
     lib.avqo_aggregate.argtypes = [i, i, i, i, i, _f64p, _i32p, _i32p, _f64p, _i64p]
     lib.avqo_importance.argtypes = [i, i, i, i, i, i, i, _f64p, _f64p, _i64p, _u8p, _f64p]
+    lib.avqo_importance_tiled.argtypes = [i, i, i, i, i, i, i, i, _f64p, _f64p, _i64p, _u8p,
+                                          _f64p]
     lib.avqo_topp.argtypes = [ctypes.c_longlong, i, i, _f64p, _u8p, _i32p]
     lib.avqo_output.argtypes = [i, i, i, i, i, i, i, i, _f64p, _f64p, _f64p, _f64p,
                                 _i64p, _i32p, i, _u8p, _f64p, _f64p]
@@ -140,6 +142,60 @@ def importance(Q, Cp, counts, Ch: int, block_q: int, tile_mask=None) -> np.ndarr
     return w
 
 
+def importance_tiled(Q, Cp, counts, Ch: int, block_q: int, tile_c: int,
+                     tile_mask=None) -> np.ndarray:
+    """App. B importance (count-extrapolated denominator, parents in tiles of
+    tile_c): w [B, H, T, M0] (rows outside tile_mask: 0)."""
+    Q, Cp = f64(Q), f64(Cp)
+    B, H, N, d = Q.shape
+    M0 = Cp.shape[1]
+    if tile_c < 1:
+        raise ValueError("tile_c must be positive")
+    n = np.ascontiguousarray(counts, dtype=np.int64)
+    T = (N + block_q - 1) // block_q
+    w = np.zeros((B, H, T, M0), np.float64)
+    m = _mask(tile_mask, B * H * T)
+    _load().avqo_importance_tiled(B * H, H, N, d, M0, Ch, block_q, tile_c, _p(Q, _f64p),
+                                  _p(Cp, _f64p), _p(n, _i64p), _p(m, _u8p), _p(w, _f64p))
+    return w
+
+
+def capture(Q, K, parent_idx, sel, block_q: int, tile_mask=None) -> dict:
+    """Top-P capture (App. B, tab. tiled_capture): the fraction of the exact
+    softmax attention mass of each query (over the original keys, Eq.
+    (standardattention)) that falls on keys whose parent is in its tile's
+    selection sel [B, H, T, P]. Also the capture of the best possible
+    selection: per tile, the P parents whose keys receive the most mass.
+
+    Returns mean capture over the queries of the evaluated tiles for the
+    given selection ("selected") and the best one ("exact")."""
+    Q, K = f64(Q), f64(K)
+    B, H, N, d = Q.shape
+    T = (N + block_q - 1) // block_q
+    par = np.asarray(parent_idx)
+    sel = np.asarray(sel)
+    P = sel.shape[-1]
+    M0 = int(par.max()) + 1 if P == 0 else max(int(par.max()), int(sel.max())) + 1
+    got, best, count = 0.0, 0.0, 0
+    for b in range(B):
+        for h in range(H):
+            onehot = np.zeros((N, M0))
+            onehot[np.arange(N), par[b, h]] = 1.0
+            for t in range(T):
+                if tile_mask is not None and not tile_mask[b, h, t]:
+                    continue
+                i0, i1 = t * block_q, min(N, (t + 1) * block_q)
+                S = Q[b, h, i0:i1] @ K[b, h].T
+                A = np.exp(S - S.max(axis=1, keepdims=True))
+                A /= A.sum(axis=1, keepdims=True)
+                mass = A @ onehot  # [queries, M0]: attention mass per parent
+                got += mass[:, sel[b, h, t]].sum()
+                top = np.argsort(-mass.sum(axis=0), kind="stable")[:P]
+                best += mass[:, top].sum()
+                count += i1 - i0
+    return {"selected": got / count, "exact": best / count}
+
+
 def topp(w, P: int, row_mask=None) -> np.ndarray:
     """Top-P parents per row of w, canonical order (w desc, index asc): int32 [..., P]."""
     w = np.ascontiguousarray(w, dtype=np.float64)
@@ -181,14 +237,19 @@ def output(Q, Cp, Cc, Vbar, counts, sel, block_q: int, recovered: bool = True,
 
 
 def forward(Q, K, V, Cp, Cc, P: int, block_q: int, recovered: bool = True,
-            tile_mask=None) -> dict:
+            tile_mask=None, importance_tile=None) -> dict:
     """The whole forward pass (Fig. pipeline): assign, aggregate, importance,
-    top-P, refined output. Returns every intermediate as NumPy arrays."""
+    top-P, refined output. Returns every intermediate as NumPy arrays.
+    importance_tile: None for Eq. (importance), or the codeword tile size of
+    the App. B approximation."""
     Cc64 = f64(Cc)
     M0, Ch = Cc64.shape[1], Cc64.shape[2]
     a = assign(K, Cp, Cc64)
     Vbar, counts = aggregate(V, a["parent_idx"], a["code_idx"], M0, Ch)
-    w = importance(Q, Cp, counts, Ch, block_q, tile_mask)
+    if importance_tile is None:
+        w = importance(Q, Cp, counts, Ch, block_q, tile_mask)
+    else:
+        w = importance_tiled(Q, Cp, counts, Ch, block_q, importance_tile, tile_mask)
     sel = topp(w, P, tile_mask)
     Y, zr = output(Q, Cp, Cc64, Vbar, counts, sel, block_q, recovered, tile_mask)
     a.update(Vbar=Vbar, counts=counts, importance=w, selection=sel, Y=Y, zratio=zr)

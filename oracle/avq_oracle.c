@@ -206,6 +206,57 @@ void avqo_importance(int BH, int H, int N, int d, int M0, int Ch, int block_q,
 }
 
 /*
+ * Importance with tiled codewords (App. B, Eq. (aproxdenom) and
+ * Eq. (codewordimportance)): the parents are visited in consecutive tiles of
+ * tile_c. After tile J, the partial denominator of query i (the sum of
+ * n_a exp(S_ia) over the non-empty parents of tiles up to J) is scaled by
+ * N / N_seen(J), N_seen(J) being the number of keys in the parents of those
+ * tiles, and the importance of every parent a of tile J is
+ * w_a += n_a exp(S_ia) / Ztilde_i(J). For the last tile N_seen = N and the
+ * result is Eq. (importance); a tile with N_seen = 0 holds only empty parents,
+ * which get w = 0. The shift mu_i cancels in each ratio.
+ */
+void avqo_importance_tiled(int BH, int H, int N, int d, int M0, int Ch, int block_q, int tile_c,
+                           const double* Q, const double* Cp, const int64_t* counts,
+                           const uint8_t* tile_mask, double* w) {
+  int T = (N + block_q - 1) / block_q;
+  int Mtot = M0 * (1 + Ch);
+  long long total = (long long)BH * T;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long long bt = 0; bt < total; ++bt) {
+    if (tile_mask && !tile_mask[bt]) continue;
+    int bh = (int)(bt / T), t = (int)(bt % T), h = bh % H;
+    const int64_t* n = counts + (long long)bh * Mtot;
+    double* wt = w + bt * M0;
+    double* S = (double*)malloc(sizeof(double) * M0);
+    for (int a = 0; a < M0; ++a) wt[a] = 0.0;
+    int i_end = (t + 1) * block_q < N ? (t + 1) * block_q : N;
+    for (int i = t * block_q; i < i_end; ++i) {
+      const double* q = Q + ((long long)bh * N + i) * d;
+      double mu = -INFINITY;
+      for (int a = 0; a < M0; ++a) {
+        S[a] = dot(q, Cp + ((long long)h * M0 + a) * d, d);
+        if (n[a] > 0 && S[a] > mu) mu = S[a];
+      }
+      double zsum = 0.0;
+      long long seen = 0;
+      for (int a0 = 0; a0 < M0; a0 += tile_c) {
+        int a1 = a0 + tile_c < M0 ? a0 + tile_c : M0;
+        for (int a = a0; a < a1; ++a) {
+          seen += n[a];
+          if (n[a] > 0) zsum += (double)n[a] * exp(S[a] - mu);
+        }
+        if (seen == 0) continue;
+        double zt = (double)N / (double)seen * zsum;
+        for (int a = a0; a < a1; ++a)
+          if (n[a] > 0) wt[a] += (double)n[a] * exp(S[a] - mu) / zt;
+      }
+    }
+    free(S);
+  }
+}
+
+/*
  * Top-P (Sec. 4.3, child spawning): for every row of w (length M0), the P
  * parents of largest importance, listed in the canonical order
  * (importance descending, index ascending on equal importance).

@@ -21,7 +21,8 @@ AVQ_OK, AVQ_ERR_INVALID_ARG, AVQ_ERR_UNSUPPORTED, AVQ_ERR_DEVICE = 0, 1, 2, 3
 AVQ_F32, AVQ_BF16 = 0, 1
 _DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
 SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_bytes", "avq_assign",
-           "avq_aggregate", "avq_attention_fwd")
+           "avq_aggregate", "avq_attention_fwd", "avq_attention_fwd_tiled")
+IMPORTANCE_TILE = 64  # parents per codeword tile of attention_fwd(tiled_importance=True)
 
 
 class AvqError(RuntimeError):
@@ -50,9 +51,11 @@ def lib():
         L.avq_assign.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         L.avq_aggregate.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32,
                                     vp, vp, vp, vp, vp, vp]
-        L.avq_attention_fwd.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32, i32,
-                                        vp, vp, vp, vp, vp, vp, vp, vp]
-        for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd"):
+        for name in ("avq_attention_fwd", "avq_attention_fwd_tiled"):
+            getattr(L, name).argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32, i32,
+                                         vp, vp, vp, vp, vp, vp, vp, vp]
+        for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd",
+                     "avq_attention_fwd_tiled"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -147,8 +150,11 @@ def aggregate(V, code_idx, M0: int, Ch: int, packed=None, counts=None, Vbar=None
 
 
 def attention_fwd(Q, Cp, Cc, packed, P: int, block_q: int, Y=None, topp_idx=None,
-                  importance=None, debug: bool = False, stream=None):
-    """Refined-codebook attention (``avq_attention_fwd``).
+                  importance=None, debug: bool = False, tiled_importance: bool = False,
+                  stream=None):
+    """Refined-codebook attention (``avq_attention_fwd``, or
+    ``avq_attention_fwd_tiled`` with ``tiled_importance``: the importance of
+    App. B over tiles of IMPORTANCE_TILE parents).
 
     Returns Y, or (Y, topp_idx, importance) when ``debug`` is set (the two
     debug outputs are then allocated if not given).
@@ -172,9 +178,9 @@ def attention_fwd(Q, Cp, Cc, packed, P: int, block_q: int, Y=None, topp_idx=None
         _dev(topp_idx, "topp_idx", torch.int32, (B, H, T, P))
     if importance is not None:
         _dev(importance, "importance", torch.float32, (B, H, T, M0))
-    _check(lib().avq_attention_fwd(_dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(Q),
-                                   _ptr(Cp), _ptr(Cc), _ptr(packed), _ptr(Y),
-                                   _ptr(topp_idx), _ptr(importance), _stream(stream)))
+    fn = lib().avq_attention_fwd_tiled if tiled_importance else lib().avq_attention_fwd
+    _check(fn(_dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(Q), _ptr(Cp), _ptr(Cc),
+              _ptr(packed), _ptr(Y), _ptr(topp_idx), _ptr(importance), _stream(stream)))
     if debug:
         return Y, topp_idx, importance
     return Y

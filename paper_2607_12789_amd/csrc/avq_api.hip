@@ -23,7 +23,7 @@ template <typename T, int D>
 hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
                             const void* Q, const void* Cp, const void* Cc, const void* packed,
                             void* Y, int32_t* topp_idx,
-                            float* importance, hipStream_t stream);
+                            float* importance, bool tiled, hipStream_t stream);
 }  // namespace avq
 
 namespace avq {
@@ -117,7 +117,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 extern "C" {
 
-int avq_version(void) { return 201; }
+int avq_version(void) { return 202; }
 
 const char* avq_last_error(void) { return g_err; }
 
@@ -170,11 +170,16 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
   return from_hip(e, "avq_aggregate launch");
 }
 
-avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
-                               int32_t M0, int32_t Ch, int32_t P, int32_t block_q,
-                               const void* Q, const void* Cp, const void* Cc,
-                               const void* packed, void* Y,
-                               int32_t* topp_idx, float* importance, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// avq_attention_fwd and avq_attention_fwd_tiled: the same checks and launch;
+// tiled selects the App. B importance.
+avq_status_t attention(const char* name, bool tiled, avq_dtype_t dtype, int32_t B, int32_t H,
+                       int32_t N, int32_t d, int32_t M0, int32_t Ch, int32_t P, int32_t block_q,
+                       const void* Q, const void* Cp, const void* Cc, const void* packed, void* Y,
+                       int32_t* topp_idx, float* importance, void* stream) {
   avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
   if (st != AVQ_OK) return st;
   if (P < 0 || P > M0) return fail(AVQ_ERR_INVALID_ARG, "P=%d outside [0, M0=%d]", P, M0);
@@ -183,24 +188,46 @@ avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t 
   if (block_q < 1) return fail(AVQ_ERR_INVALID_ARG, "block_q=%d must be positive", block_q);
   if (block_q > 256) return fail(AVQ_ERR_UNSUPPORTED, "block_q=%d: at most 256", block_q);
   if (!Q || !Cp || (!Cc && Ch > 0) || !packed || !Y)
-    return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: null pointer argument");
+    return fail(AVQ_ERR_INVALID_ARG, "%s: null pointer argument", name);
   if (!aligned16(Q) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(packed) ||
       !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance))
-    return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd: arrays must be 16-byte aligned");
+    return fail(AVQ_ERR_INVALID_ARG, "%s: arrays must be 16-byte aligned", name);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int BH = B * H;
   hipError_t e;
   if (dtype == AVQ_BF16)
-    e = d == 64 ? avq::launch_attention<avq::bf16, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
-                                                       Y, topp_idx, importance, s)
-                : avq::launch_attention<avq::bf16, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
-                                                        Y, topp_idx, importance, s);
+    e = d == 64 ? avq::launch_attention<avq::bf16, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
+                                                       packed, Y, topp_idx, importance, tiled, s)
+                : avq::launch_attention<avq::bf16, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
+                                                        packed, Y, topp_idx, importance, tiled, s);
   else
-    e = d == 64 ? avq::launch_attention<float, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
-                                                   Y, topp_idx, importance, s)
-                : avq::launch_attention<float, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc, packed,
-                                                    Y, topp_idx, importance, s);
-  return from_hip(e, "avq_attention_fwd launch");
+    e = d == 64 ? avq::launch_attention<float, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
+                                                   packed, Y, topp_idx, importance, tiled, s)
+                : avq::launch_attention<float, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
+                                                    packed, Y, topp_idx, importance, tiled, s);
+  return from_hip(e, "attention launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int32_t d,
+                               int32_t M0, int32_t Ch, int32_t P, int32_t block_q,
+                               const void* Q, const void* Cp, const void* Cc,
+                               const void* packed, void* Y,
+                               int32_t* topp_idx, float* importance, void* stream) {
+  return attention("avq_attention_fwd", false, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp, Cc,
+                   packed, Y, topp_idx, importance, stream);
+}
+
+avq_status_t avq_attention_fwd_tiled(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                                     int32_t d, int32_t M0, int32_t Ch, int32_t P,
+                                     int32_t block_q, const void* Q, const void* Cp,
+                                     const void* Cc, const void* packed, void* Y,
+                                     int32_t* topp_idx, float* importance, void* stream) {
+  return attention("avq_attention_fwd_tiled", true, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp,
+                   Cc, packed, Y, topp_idx, importance, stream);
 }
 
 }  // extern "C"

@@ -33,6 +33,7 @@
 // distance is strictly smaller.
 #include "avq_common.hpp"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace avq {
@@ -458,7 +459,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     const T* __restrict__ K, const T* __restrict__ Cp, const T* __restrict__ Cc,
     const int32_t* __restrict__ parent_idx, int32_t* __restrict__ code_idx, int H, int N, int M0,
-    int Ch, int F, int ranges) {
+    int Ch, int F, int ranges, int splits, int chunk) {
   using Frag = typename std::conditional<Elem<T>::kBf16, bf16x8, float>::type;
   constexpr bool kB = Elem<T>::kBf16;
   constexpr int KQ = kB ? D / 32 : D / 4;
@@ -467,10 +468,14 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int g = lane / 16, c = lane % 16;
+  // workgroup (bh, family range, key split), the split fastest: the splits
+  // of one family range share its candidate rows in one L2
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int bh = blk / ranges;
+  const int split = blk % splits;
+  const int bh = blk / splits / ranges;
   const int h = bh % H;
-  const int p0 = (blk % ranges) * F;
+  const int p0 = (blk / splits % ranges) * F;
+  const int kbegin = split * chunk, kend = min(N, kbegin + chunk);
   const int nfam = min(F, M0 - p0);
   const int32_t* pidx = parent_idx + (size_t)bh * N;
   const T* kh = K + (size_t)bh * N * D;
@@ -536,13 +541,13 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     }
   };
 
-  for (int base = 0; base < N; base += kChildRound) {
+  for (int base = kbegin; base < kend; base += kChildRound) {
     // 1. queue the keys of this range in scan order
     int cur[kScanPerThread];
 #pragma unroll
     for (int k = 0; k < kScanPerThread; ++k) {
       const int j = base + k * kChildThreads + tid;
-      const int p = j < N ? pidx[j] : -1;
+      const int p = j < kend ? pidx[j] : -1;
       cur[k] = (p >= p0 && p < p0 + nfam) ? p - p0 : -1;
     }
     unsigned long long mask[kScanPerThread];
@@ -599,12 +604,14 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     for (int e = tid; e < qlen; e += kChildThreads)
       L.skey[atomicAdd(&L.cursor[L.qfam[e]], 1)] = L.qkey[e];
     __syncthreads();
-    // 3. each wave takes groups w, w + 4, ... (a group is 16 keys of one
-    //    family); consecutive groups of a wave mostly share the family, whose
-    //    rows stay in registers
+    // 3. each wave takes a contiguous run of groups (a group is 16 keys of
+    //    one family), so that consecutive groups of a wave mostly share the
+    //    family, whose rows stay in registers
     const int n_items = L.item_start[nfam];
+    const int per_wave = (n_items + kChildWaves - 1) / kChildWaves;
+    const int it_end = min(n_items, (wave + 1) * per_wave);
     int f = 0;
-    for (int it = wave; it < n_items; it += kChildWaves) {
+    for (int it = wave * per_wave; it < it_end; ++it) {
       while (L.item_start[f + 1] <= it) ++f;  // wave-uniform
       const int p = p0 + f;
       Frag kf[KQ];
@@ -667,12 +674,11 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   using Cfg = AssignCfg<T, D>;
   using SCfg = StreamCfg<T, D>;
   long long grid;
-  hipError_t e;
+  DeviceInfo dev;
+  hipError_t e = device_info(&dev);
+  if (e != hipSuccess) return e;
   if (SCfg::fits(M0)) {
     // persistent: two workgroups per CU, each a run of whole steps
-    DeviceInfo dev;
-    e = device_info(&dev);
-    if (e != hipSuccess) return e;
     const int per_bh = (N + SCfg::kKeysPerStep - 1) / SCfg::kKeysPerStep;
     const long long n_steps = (long long)BH * per_bh;
     if (n_steps > 0x7fffffff) return hipErrorInvalidConfiguration;
@@ -702,10 +708,18 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   if (e != hipSuccess) return e;
   if (Ch == 0) return hipSuccess;  // flat codebook: the parent is the code
 
-  // child compare: F parents per workgroup
+  // child compare: F parents per workgroup, and the keys split into chunks
+  // of whole scan rounds until the grid fills the device twice over (the
+  // keys are independent: a split only shortens each workgroup's scan)
   const int F = kMaxFam;
   const int ranges = (M0 + F - 1) / F;
-  grid = (long long)BH * ranges;
+  const long long want = 2LL * (dev.cus > 0 ? dev.cus : 1);
+  const int max_splits = (N + kChildRound - 1) / kChildRound;
+  const long long base_grid = (long long)BH * ranges;
+  int splits = (int)std::min<long long>(max_splits, std::max<long long>(1, (want + base_grid - 1) / base_grid));
+  const int chunk = ((N + splits - 1) / splits + kChildRound - 1) / kChildRound * kChildRound;
+  splits = (N + chunk - 1) / chunk;
+  grid = base_grid * splits;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   constexpr int slot_b = 28 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
   e = ensure_dynamic_lds((const void*)child_assign_kernel<T, D>, (int)sizeof(ChildLds), slot_b);
@@ -713,7 +727,7 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   hipLaunchKernelGGL((child_assign_kernel<T, D>), dim3((unsigned)grid), dim3(kChildThreads),
                      sizeof(ChildLds), stream, static_cast<const T*>(K),
                      static_cast<const T*>(Cp), static_cast<const T*>(Cc), parent_idx, code_idx,
-                     H, N, M0, Ch, F, ranges);
+                     H, N, M0, Ch, F, ranges, splits, chunk);
   return hipGetLastError();
 }
 

@@ -121,7 +121,9 @@ __device__ __forceinline__ int row_swizzle(int r) {
 
 // Register budget: two or three waves per SIMD (at most 256 or 168 registers
 // each), so that other tiles' MFMA work runs while one workgroup waits.
-template <typename T, int D, int MAXW>
+// TILED: importance with the count-extrapolated denominator of App. B, one
+// codeword tile per chunk, computed in the parent sweep (no second sweep).
+template <typename T, int D, int MAXW, bool TILED>
 __global__ __launch_bounds__(MAXW * 64)
 __attribute__((amdgpu_waves_per_eu(AttnCfg<T, D, MAXW>::kWavesPerEu)))
 void attention_kernel(AttnArgs args) {
@@ -545,6 +547,34 @@ void attention_kernel(AttnArgs args) {
     }
   };
 
+  // App. B: keys seen so far (the counts of the parents of the chunks up to
+  // the current one), the same in every lane
+  const bool tiled_importance = TILED && need_importance && n_pchunks > 1;
+  float seen = 0.f;
+  auto tiled_partials = [&](const unsigned char* B, const f32x4 (&W0)[2][QS],
+                            const f32x4 (&W1)[2][QS], int k) {
+    // this lane group's 16 rows of the chunk, then the other three groups'
+    float cnt = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < TPC; ++tt) {
+      const f32x4 n4 = info4(B, tt, 0);
+      cnt += (n4[0] + n4[1]) + (n4[2] + n4[3]);
+    }
+    cnt += shfl_xor(cnt, 16);
+    cnt += shfl_xor(cnt, 32);
+    seen += cnt;  // integers below 2^24: exact
+    // weight / Ztilde = W * seen / (N * Z), W and Z relative to the same max
+    float mul[QS];
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      float z = zp[s];
+      z += shfl_xor(z, 16);
+      z += shfl_xor(z, 32);
+      mul[s] = (qvalid[s] && seen > 0.f) ? seen / ((float)N * z) : 0.f;
+    }
+    importance_partials(W0, W1, mul, k % 2);
+  };
+
   // ---- phase 1: parent sweep -------------------------------------------------
   // Per chunk: the logits of both tile pairs are issued first; the second
   // pair's MFMAs run while the first pair's weights are computed, and the
@@ -552,6 +582,7 @@ void attention_kernel(AttnArgs args) {
   issue_parent(0, buffer(0), true);
   for (int k = 0; k < n_pchunks; ++k) {
     wait_chunk();
+    if (tiled_importance && k > 0) importance_flush(k - 1);
     if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, buffer((k + 1) % 2), true);
     const unsigned char* B = buffer(k % Cfg::NBUF);
     if (has_rows) {
@@ -571,6 +602,7 @@ void attention_kernel(AttnArgs args) {
         for (int s = 0; s < QS; ++s) rz[s] = exp2_hw(m[s] - mz[s]);
         importance_partials(S0, S1, rz, 0);
       }
+      if (tiled_importance) tiled_partials(B, S0, S1, k);
     }
     if (Cfg::NBUF == 1 && k + 1 < n_pchunks) {
       __syncthreads();
@@ -580,9 +612,9 @@ void attention_kernel(AttnArgs args) {
 
   // ---- phase 2: importance with the final max and denominators ---------------
   if (need_importance) {
-    if (n_pchunks == 1) {
+    if (n_pchunks == 1 || TILED) {
       __syncthreads();
-      importance_flush(0);
+      importance_flush(n_pchunks - 1);
     } else {
       if (has_rows) set_mz();
       float one[QS];
@@ -728,24 +760,26 @@ void attention_kernel(AttnArgs args) {
   }
 }
 
-template <typename T, int D, int MAXW>
+template <typename T, int D, int MAXW, bool TILED>
 hipError_t launch_attention_cfg(const AttnArgs& a, int BH, hipStream_t stream) {
   const long long grid = (long long)BH * a.n_tiles;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   using Cfg = AttnCfg<T, D, MAXW>;
-  constexpr int slot = 8 + (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0) + (MAXW == 8 ? 1 : 0);
-  hipError_t e = ensure_dynamic_lds((const void*)attention_kernel<T, D, MAXW>,
+  constexpr int slot = (TILED ? 48 : 8) + (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0) +
+                       (MAXW == 8 ? 1 : 0);
+  hipError_t e = ensure_dynamic_lds((const void*)attention_kernel<T, D, MAXW, TILED>,
                                     (int)Cfg::LDS_BYTES, slot);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attention_kernel<T, D, MAXW>), dim3((unsigned)grid), dim3(MAXW * 64),
-                     Cfg::LDS_BYTES, stream, a);
+  hipLaunchKernelGGL((attention_kernel<T, D, MAXW, TILED>), dim3((unsigned)grid),
+                     dim3(MAXW * 64), Cfg::LDS_BYTES, stream, a);
   return hipGetLastError();
 }
 
 template <typename T, int D>
 hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
                             const void* Q, const void* Cp, const void* Cc, const void* packed,
-                            void* Y, int32_t* topp_idx, float* importance, hipStream_t stream) {
+                            void* Y, int32_t* topp_idx, float* importance, bool tiled,
+                            hipStream_t stream) {
   AttnArgs a;
   a.Q = Q;
   a.Cp = Cp;
@@ -761,14 +795,18 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
   a.P = P;
   a.block_q = block_q;
   a.n_tiles = (N + block_q - 1) / block_q;
-  if (block_q <= 128) return launch_attention_cfg<T, D, 4>(a, BH, stream);
-  return launch_attention_cfg<T, D, 8>(a, BH, stream);
+  if (tiled) {
+    if (block_q <= 128) return launch_attention_cfg<T, D, 4, true>(a, BH, stream);
+    return launch_attention_cfg<T, D, 8, true>(a, BH, stream);
+  }
+  if (block_q <= 128) return launch_attention_cfg<T, D, 4, false>(a, BH, stream);
+  return launch_attention_cfg<T, D, 8, false>(a, BH, stream);
 }
 
 #define AVQ_INSTANTIATE(T, D)                                                                \
   template hipError_t launch_attention<T, D>(int, int, int, int, int, int, int, const void*, \
                                              const void*, const void*, const void*, void*,   \
-                                             int32_t*, float*, hipStream_t);
+                                             int32_t*, float*, bool, hipStream_t);
 AVQ_INSTANTIATE(bf16, 64)
 AVQ_INSTANTIATE(bf16, 128)
 AVQ_INSTANTIATE(float, 64)

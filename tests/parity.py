@@ -45,12 +45,13 @@ def to_gpu(x: dict) -> dict:
     return {k: v.cuda() for k, v in x.items()}
 
 
-def gpu_forward(xd: dict, w) -> dict:
-    """Runs the three entry points and returns every output on the CPU."""
+def gpu_forward(xd: dict, w, tiled: bool = False) -> dict:
+    """Runs the three entry points and returns every output on the CPU
+    (tiled: the App. B importance entry point)."""
     par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
     packed, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
     Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q,
-                                     debug=True)
+                                     debug=True, tiled_importance=tiled)
     torch.cuda.synchronize()
     out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, packed=packed, counts=counts, Y=Y,
                topp=topp, importance=imp)
@@ -283,11 +284,12 @@ def check_output(x, w, g, o, sel_ok) -> Report:
                   median_rel=float(f"{np.median(rel_rows):.3g}"), frob_rel=float(f"{fro:.3g}"))
 
 
-def compare(x, w, tiles_per_head=None, seed=0, recovered=True) -> dict:
+def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False) -> dict:
     """Runs GPU and oracle on the same inputs and checks every output.
 
     tiles_per_head: number of query tiles per head evaluated by the oracle
-    (None: all). The first and last tile are always included."""
+    (None: all). The first and last tile are always included. tiled: the
+    App. B importance on both sides (tiles of avq.IMPORTANCE_TILE parents)."""
     T = w.n_tiles
     mask = np.ones((w.B, w.H, T), np.uint8)
     if tiles_per_head is not None and tiles_per_head < T:
@@ -298,9 +300,10 @@ def compare(x, w, tiles_per_head=None, seed=0, recovered=True) -> dict:
                 pick = rng.choice(T, tiles_per_head, replace=False)
                 mask[b, h, pick] = 1
                 mask[b, h, [0, T - 1]] = 1
-    g = gpu_forward(to_gpu(x), w)
+    g = gpu_forward(to_gpu(x), w, tiled)
     o = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], w.P, w.block_q,
-                       recovered=recovered, tile_mask=mask)
+                       recovered=recovered, tile_mask=mask,
+                       importance_tile=avq.IMPORTANCE_TILE if tiled else None)
     clean, ra = check_assign(x, w, g, o)
     rg = check_aggregate(x, w, g, o, clean)
     sel_ok, rt = check_topp(x, w, g, o, clean, mask.astype(bool))

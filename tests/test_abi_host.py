@@ -37,7 +37,7 @@ def test_header_declares_the_entry_points():
 def test_library_exports_every_declared_symbol(L):
     for name in declared_functions():
         assert hasattr(L, name), name
-    assert L.avq_version() == 201
+    assert L.avq_version() == 202
 
 
 NULL = None
@@ -56,6 +56,10 @@ def attn(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,
     return L.avq_attention_fwd(dtype, B, H, N, d, M0, Ch, P, bq, *ptrs, NULL, NULL, NULL)
 
 
+def attn_tiled(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,) * 5):
+    return L.avq_attention_fwd_tiled(dtype, B, H, N, d, M0, Ch, P, bq, *ptrs, NULL, NULL, NULL)
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(dtype=7), INVALID),
     (dict(B=0), INVALID), (dict(H=-1), INVALID), (dict(N=0), INVALID), (dict(M0=0), INVALID),
@@ -65,7 +69,7 @@ def attn(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64, ptrs=(FAKE,
     (dict(B=1 << 14, H=1 << 10, N=1 << 10, d=128), UNSUPPORTED),
 ])
 def test_shape_validation(L, kw, status):
-    for fn in (assign, aggregate, attn):
+    for fn in (assign, aggregate, attn, attn_tiled):
         assert fn(L, **kw) == status, (fn.__name__, kw)
         assert L.avq_last_error().decode() != ""
 
@@ -81,11 +85,12 @@ def test_null_pointers_are_rejected(L):
         ptrs[i] = NULL
         assert aggregate(L, ptrs=ptrs) == INVALID
     assert aggregate(L, ptrs=(FAKE, FAKE, NULL, FAKE, NULL)) == INVALID
-    for i in range(5):
-        ptrs = [FAKE] * 5
-        ptrs[i] = NULL
-        assert attn(L, ptrs=ptrs) == INVALID
-    assert "null" in L.avq_last_error().decode()
+    for fn in (attn, attn_tiled):
+        for i in range(5):
+            ptrs = [FAKE] * 5
+            ptrs[i] = NULL
+            assert fn(L, ptrs=ptrs) == INVALID
+        assert "null" in L.avq_last_error().decode()
 
 
 def test_packed_size(L):
@@ -118,12 +123,14 @@ def test_misaligned_pointers_are_rejected(L):
                                          (1, 257, UNSUPPORTED)])
 def test_attention_argument_validation(L, P, bq, status):
     assert attn(L, P=P, bq=bq) == status
+    assert attn_tiled(L, P=P, bq=bq) == status
 
 
 def test_flat_codebook_arguments(L):
     # Ch = 0: no children to select, so P must be 0
     assert attn(L, Ch=0, P=1) == INVALID
     assert "flat" in L.avq_last_error().decode()
+    assert attn_tiled(L, Ch=0, P=1) == INVALID
     # Cc may be NULL: validation goes on to the next problem (here a
     # misaligned output), which also proves nothing was launched
     odd = ctypes.c_void_p(24)

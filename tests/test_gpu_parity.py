@@ -139,6 +139,57 @@ def test_repeat_runs_identical_integers():
     torch.testing.assert_close(a["Y"], b["Y"], rtol=2e-3, atol=1e-5)
 
 
+# App. B importance (tiles of 64 parents) against the oracle's tiled importance
+TILED = {
+    "tiled_m0_256_d128": small(M0=256, Ch=8, P=32, d=128, N=2048, B=1, H=2),
+    "tiled_m0_300_ragged": small(M0=300, Ch=4, P=30, N=1024, B=1, H=2),
+    "tiled_fp32_d64": small(dtype="f32", M0=150, Ch=4, P=12, N=900),
+    "tiled_p0_importance": small(M0=200, P=0, N=700),
+    "tiled_bq200": small(M0=130, Ch=8, P=11, block_q=200, N=1300),
+    "tiled_m0_512_bq256": small(M0=512, Ch=8, P=64, block_q=256, N=1536, d=128, B=1, H=2),
+}
+
+
+@pytest.mark.parametrize("name", list(TILED))
+def test_tiled_importance(name):
+    w = TILED[name]
+    banner(name, w)
+    x = inputs.generate(w)
+    res = parity.compare(x, w, tiled=True)
+    report(res)
+
+
+def test_tiled_importance_empty_first_tile():
+    """No key reaches the first 64 parents: their tile has N_seen = 0 and adds
+    nothing; the later tiles extrapolate from the keys they have seen."""
+    w = small(M0=200, Ch=4, P=20, N=900, B=1, H=2)
+    banner("tiled_empty_first_tile", w)
+    x = inputs.generate(w)
+    Cp = x["Cp"].clone()
+    Cp[:, :64] += 40.0
+    x["Cp"] = Cp
+    res = parity.compare(x, w, tiled=True)
+    report(res)
+    assert (res["oracle"]["counts"][..., :64] == 0).all()
+    assert (res["gpu"]["importance"][..., :64] == 0).all()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_tiled_single_tile_equals_exact(dtype):
+    """M0 <= 64: one codeword tile, N_seen = N, and the two entry points give
+    identical results."""
+    from paper_2607_12789_amd import avq
+    w = small(M0=64, Ch=8, P=6, dtype=dtype)
+    xd = parity.to_gpu(inputs.generate(w))
+    _, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+    packed, _, _ = avq.aggregate(xd["V"], code, w.M0, w.Ch)
+    a = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q, debug=True)
+    b = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q, debug=True,
+                          tiled_importance=True)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+
+
 SAMPLE = {"c1": None, "c2": None, "c3": None, "c4": 12, "c5": 4}
 
 

@@ -44,6 +44,13 @@ MUTANTS = [
     ("child logits against the parent codeword",
      "double v = dot(q, Cc + (((long long)h * M0 + p) * Ch + c) * d, d);",
      "double v = dot(q, Cp + ((long long)h * M0 + p) * d, d);"),
+    ("tiled importance without the count extrapolation",
+     "double zt = (double)N / (double)seen * zsum;", "double zt = zsum;"),
+    ("tiled importance counts the keys of the current tile only",
+     "for (int a0 = 0; a0 < M0; a0 += tile_c) {\n", "for (int a0 = 0; a0 < M0; a0 += tile_c) {\n        seen = 0;\n"),
+    ("tiled importance scales by the partial denominator of the tile alone",
+     "if (n[a] > 0) zsum += (double)n[a] * exp(S[a] - mu);",
+     "if (n[a] > 0) zsum = (double)n[a] * exp(S[a] - mu);"),
 ]
 
 PIN_CALLS = [
@@ -59,6 +66,9 @@ PIN_CALLS = [
     pins.test_children_equal_parent_reduce_to_vq,
     pins.test_large_logits_stay_finite,
     pins.test_empty_far_children_do_not_poison,
+    lambda: pins.test_tiled_importance_last_tile_is_exact(3),
+    pins.test_tiled_importance_first_tile_closed_form,
+    lambda: pins.test_tiled_importance_zero_queries(3),
 ]
 
 

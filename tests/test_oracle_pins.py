@@ -130,6 +130,75 @@ def test_importance_zero_for_empty_parents():
         assert (wimp[:, :, t][empty] == 0).all()
 
 
+def _tiled_inputs(**kw):
+    w = small(M0=10, N=150, block_q=40, **kw)
+    x = inputs.generate(w)
+    o = run(x, w)
+    return w, x, o, o["counts"]
+
+
+@pytest.mark.parametrize("tile_c", [10, 16])
+def test_tiled_importance_single_tile_is_exact(tile_c):
+    """App. B: with every parent in one tile, N_seen = N after it and the
+    extrapolated denominator is the exact one: Eq. (importance)."""
+    w, x, o, n = _tiled_inputs()
+    wt = oracle.importance_tiled(x["Q"], x["Cp"], n, w.Ch, w.block_q, tile_c)
+    np.testing.assert_allclose(wt, o["importance"], rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("tile_c", [1, 3, 4])
+def test_tiled_importance_last_tile_is_exact(tile_c):
+    """The tile processed last has seen every key (N_seen = N): its parents
+    get their Eq. (importance) values; earlier tiles differ in general."""
+    w, x, o, n = _tiled_inputs()
+    wt = oracle.importance_tiled(x["Q"], x["Cp"], n, w.Ch, w.block_q, tile_c)
+    last = ((w.M0 - 1) // tile_c) * tile_c
+    np.testing.assert_allclose(wt[..., last:], o["importance"][..., last:], rtol=1e-12,
+                               atol=1e-15)
+    assert not np.allclose(wt[..., :last], o["importance"][..., :last], rtol=1e-6)
+
+
+def test_tiled_importance_first_tile_closed_form():
+    """tile_c = 1: after the first parent, Ztilde_i = N/n_0 * n_0 e^S_i0, so
+    w_0 = |I| n_0 / N whatever the logits; a tile of empty parents gets 0."""
+    w, x, o, n = _tiled_inputs(seed=4)
+    wt = oracle.importance_tiled(x["Q"], x["Cp"], n, w.Ch, w.block_q, 1)
+    sizes = np.array([min(w.block_q, w.N - t * w.block_q) for t in range(w.n_tiles)])
+    for b in range(w.B):
+        for h in range(w.H):
+            first = int(np.argmax(n[b, h, :w.M0] > 0))
+            expect = sizes * n[b, h, first] / w.N
+            np.testing.assert_allclose(wt[b, h, :, first], expect, rtol=1e-12)
+            assert (wt[b, h, :, :w.M0][:, n[b, h, :w.M0] == 0] == 0).all()
+
+
+@pytest.mark.parametrize("tile_c", [1, 3])
+def test_tiled_importance_zero_queries(tile_c):
+    """Q = 0: every logit is 0, each partial denominator is exactly N_seen,
+    Ztilde = N, and tiled importance equals exact importance = |I| n_a / N."""
+    w, x, o, n = _tiled_inputs()
+    Q0 = torch.zeros_like(x["Q"])
+    wt = oracle.importance_tiled(Q0, x["Cp"], n, w.Ch, w.block_q, tile_c)
+    we = oracle.importance(Q0, x["Cp"], n, w.Ch, w.block_q)
+    np.testing.assert_allclose(wt, we, rtol=1e-12, atol=1e-15)
+    sizes = np.array([min(w.block_q, w.N - t * w.block_q) for t in range(w.n_tiles)])
+    np.testing.assert_allclose(wt, sizes[None, None, :, None] * n[:, :, None, :w.M0] / w.N,
+                               rtol=1e-12)
+
+
+def test_capture_of_full_selection_is_one():
+    """Capture (App. B): selecting every parent captures all attention mass;
+    the best selection of P parents captures at least as much as any other."""
+    w, x, o, n = _tiled_inputs()
+    T = w.n_tiles
+    full = np.broadcast_to(np.arange(w.M0, dtype=np.int32), (w.B, w.H, T, w.M0))
+    cap = oracle.capture(x["Q"], x["K"], o["parent_idx"], full, w.block_q)
+    assert abs(cap["selected"] - 1.0) < 1e-12 and abs(cap["exact"] - 1.0) < 1e-12
+    sel = oracle.topp(o["importance"], 3)
+    cap3 = oracle.capture(x["Q"], x["K"], o["parent_idx"], sel, w.block_q)
+    assert 0 < cap3["selected"] <= cap3["exact"] + 1e-12 < 1
+
+
 # ---------------------------------------------------------------- top-P
 
 @pytest.mark.parametrize("P", [0, 1, 3, 6])
