@@ -2,6 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
     python bench.py --sweep [--steps K] [--warmup W]
+    python bench.py --codebook-update [--steps K] [--warmup W]
 
 One step is the whole forward pass over one batch of synthetic inputs
 already resident in HBM: avq_assign -> avq_aggregate -> avq_attention_fwd.
@@ -196,6 +197,66 @@ def sweep(args):
     print(json.dumps(summary), flush=True)
 
 
+def codebook_bench(args):
+    """The codebook step of App. A on the same workload: avq_assign, then
+    avq_aggregate on the keys, then avq_codebook_update. One JSON line with
+    the per-kernel averages and the update kernel against the HBM peak."""
+    import torch
+    from paper_2607_12789_amd import avq, inputs
+    w = inputs.WORKLOADS[args.workload]
+    x = inputs.generate(w)
+    dev = torch.device("cuda:0")
+    xd = {k: v.to(dev) for k, v in x.items()}
+    B, H, N, d, M0, Ch = w.B, w.H, w.N, w.d, w.M0, w.Ch
+    Mtot = w.Mtot
+    par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
+    code = torch.empty_like(par)
+    sums = torch.empty((B, H, Mtot, d), dtype=torch.float32, device=dev)
+    counts = torch.empty((B, H, Mtot), dtype=torch.int32, device=dev)
+    packed = torch.empty((B, H, avq.packed_bytes(w.torch_dtype, M0, Ch, d)), dtype=torch.uint8,
+                         device=dev)
+    S = torch.zeros((H, Mtot, d), dtype=torch.float32, device=dev)
+    Nm = torch.ones((H, Mtot), dtype=torch.float32, device=dev)
+    Cp = torch.empty((H, M0, d), dtype=w.torch_dtype, device=dev)
+    Cc = torch.empty((H, M0, Ch, d), dtype=w.torch_dtype, device=dev)
+
+    def step(ev=None):
+        if ev: ev[0].record()
+        avq.assign(xd["K"], xd["Cp"], xd["Cc"], par, code)
+        if ev: ev[1].record()
+        avq.aggregate(xd["K"], code, M0, Ch, packed, counts, sums)
+        if ev: ev[2].record()
+        avq.codebook_update(sums, counts, S, Nm, M0, Ch, 0.99, Cp, Cc)
+        if ev: ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for ev in evs:
+        step(ev)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    t = [sum(ev[k].elapsed_time(ev[k + 1]) for ev in evs) / len(evs) for k in range(3)]
+    esz = 2 if w.dtype == "bf16" else 4
+    # sums and counts read once, S and N read and written, codewords written
+    bytes_update = (B * H * Mtot * (d + 1) * 4 + 2 * H * Mtot * (d + 1) * 4
+                    + H * Mtot * d * esz)
+    achieved = bytes_update / (t[2] * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "codebook EMA update step (App. A): assign + key aggregates + update",
+        "value": B * H * N / (ms * 1e-3), "unit": "keys*heads/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.describe()}", "lambda": 0.99},
+        "kernels_ms": {"assign": t[0], "aggregate_keys": t[1], "codebook_update": t[2]},
+        "roofline": {"kernel": "avq_codebook_update", "bound": "hbm", "achieved": achieved,
+                     "peak": 8000.0, "unit": "GB/s", "frac": achieved / 8000.0, "traffic": None,
+                     "bytes_per_launch": bytes_update},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -210,6 +271,8 @@ def main():
                     help="also launch one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--tiled-importance", action="store_true",
                     help="use the App. B importance (one parent sweep) instead of the exact one")
+    ap.add_argument("--codebook-update", action="store_true",
+                    help="time the codebook EMA step (App. A) instead")
     ap.add_argument("--sweep", action="store_true",
                     help="run the sequence-length scaling sweep instead")
     ap.add_argument("--sweep-only", default="",
@@ -231,6 +294,9 @@ def main():
         sys.exit(1)
     if args.sweep:
         sweep(args)
+        return
+    if args.codebook_update:
+        codebook_bench(args)
         return
     w = inputs.WORKLOADS[args.workload]
     x = inputs.generate(w)

@@ -17,6 +17,8 @@
  *                      (parent_recovery), (correcting_attention), Alg. 2)
  *   avq_attention_fwd_tiled  the same with the tiled-codeword importance of
  *                      App. B (Eq. (aproxdenom), (codewordimportance))
+ *   avq_codebook_update  EMA codebook statistics and the constrained child
+ *                      projection (App. A, Eq. (child_constraint_solve))
  *
  * Conventions shared by every call:
  *   - Every array argument is a DEVICE pointer owned by the caller, contiguous,
@@ -208,6 +210,44 @@ avq_status_t avq_attention_fwd_tiled(avq_dtype_t dtype, int32_t B, int32_t H, in
                                      int32_t block_q, const void* Q, const void* Cp,
                                      const void* Cc, const void* packed, void* Y,
                                      int32_t* topp_idx, float* importance, void* stream);
+
+/*
+ * avq_codebook_update - one step of the codebook's exponential moving
+ * averages under the parent-child constraint (App. A).
+ *
+ * The batch statistics are the aggregates of the KEYS (avq_aggregate called
+ * with K in place of V, after avq_assign): sums[b][h][x] is the sum of the
+ * keys with code x in batch entry b (a parent row covers its whole cell) and
+ * counts[b][h][x] their number. For every head h (one codebook per head,
+ * shared by the batch) and code x, summing over b in order:
+ *   S_x <- lambda S_x + (1 - lambda) sum_b sums[b][h][x]
+ *   N_x <- lambda N_x + (1 - lambda) sum_b counts[b][h][x]
+ * Parents take the unconstrained mean C_p = S_p / N_p. The Ch children of p,
+ * with means M_c = S_c / N_c, are projected onto the constraint that their
+ * mean is C_p by the mass-weighted least-squares solution
+ * (Eq. (child_constraint_solve)):
+ *   delta = sum_c M_c - Ch C_p,  sigma = sum_c 1 / N_c,
+ *   C_pc  = M_c - delta / (N_c sigma).
+ *
+ *   lambda   EMA decay, 0 < lambda <= 1 (else AVQ_ERR_INVALID_ARG)
+ *   sums     [B][H][Mtot][d]  fp32 (the Vbar output of avq_aggregate on K)
+ *   counts   [B][H][Mtot]     int32 (its counts)
+ *   S        [H][Mtot][d]     fp32, in/out: the EMA key sums
+ *   Nema     [H][Mtot]        fp32, in/out: the EMA counts; must be positive
+ *                             on entry (then they stay positive); a
+ *                             non-positive mass gives non-finite codewords
+ *   Cp_out   [H][M0][d]       dtype, out: the new parents
+ *   Cc_out   [H][M0][Ch][d]   dtype, out: the new children (NULL allowed
+ *                             when Ch = 0)
+ * Sizes as for the other calls (N does not apply). Arithmetic is fp32, one
+ * thread per (family, dimension), batch entries summed in order; counts are
+ * exact while the total count of a code stays below 2^24. The codewords are
+ * rounded once to dtype.
+ */
+avq_status_t avq_codebook_update(avq_dtype_t dtype, int32_t B, int32_t H, int32_t d,
+                                 int32_t M0, int32_t Ch, float lambda, const float* sums,
+                                 const int32_t* counts, float* S, float* Nema, void* Cp_out,
+                                 void* Cc_out, void* stream);
 
 #ifdef __cplusplus
 }

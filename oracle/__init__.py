@@ -58,6 +58,8 @@ def open_library(path):
     lib.avqo_importance.argtypes = [i, i, i, i, i, i, i, _f64p, _f64p, _i64p, _u8p, _f64p]
     lib.avqo_importance_tiled.argtypes = [i, i, i, i, i, i, i, i, _f64p, _f64p, _i64p, _u8p,
                                           _f64p]
+    lib.avqo_codebook_update.argtypes = [i, i, i, i, i, ctypes.c_double, _f64p, _i64p, _f64p,
+                                         _f64p, _f64p, _f64p]
     lib.avqo_topp.argtypes = [ctypes.c_longlong, i, i, _f64p, _u8p, _i32p]
     lib.avqo_output.argtypes = [i, i, i, i, i, i, i, i, _f64p, _f64p, _f64p, _f64p,
                                 _i64p, _i32p, i, _u8p, _f64p, _f64p]
@@ -194,6 +196,27 @@ def capture(Q, K, parent_idx, sel, block_q: int, tile_mask=None) -> dict:
                 best += mass[:, top].sum()
                 count += i1 - i0
     return {"selected": got / count, "exact": best / count}
+
+
+def codebook_update(sums, counts, S, Nema, M0: int, Ch: int, lam: float):
+    """App. A codebook update (EMA statistics, constrained child projection).
+
+    sums [B, H, Mtot, d] key sums and counts [B, H, Mtot] of one batch (the
+    aggregates of the keys); S [H, Mtot, d] and Nema [H, Mtot] the EMA state.
+    Returns (S', Nema', Cp [H, M0, d], Cc [H, M0, Ch, d]) as fp64 arrays; the
+    inputs are not modified."""
+    sums = f64(sums)
+    B, H, Mtot, d = sums.shape
+    if Mtot != M0 * (1 + Ch):
+        raise ValueError("sums do not hold M0 * (1 + Ch) codes")
+    n = np.ascontiguousarray(counts, dtype=np.int64)
+    S2 = np.array(f64(S), dtype=np.float64, copy=True)
+    N2 = np.array(f64(Nema), dtype=np.float64, copy=True)
+    Cp = np.zeros((H, M0, d))
+    Cc = np.zeros((H, M0, Ch, d))
+    _load().avqo_codebook_update(B, H, d, M0, Ch, float(lam), _p(sums, _f64p), _p(n, _i64p),
+                                 _p(S2, _f64p), _p(N2, _f64p), _p(Cp, _f64p), _p(Cc, _f64p))
+    return S2, N2, Cp, Cc
 
 
 def topp(w, P: int, row_mask=None) -> np.ndarray:

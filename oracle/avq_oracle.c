@@ -364,3 +364,60 @@ void avqo_output(int BH, int H, int N, int d, int M0, int Ch, int P, int block_q
     free(X);
   }
 }
+
+/*
+ * Codebook update by exponential moving averages with the parent-child
+ * constraint (App. A). For every head h and code x (parents and children),
+ * the batch statistics are the key sums and counts of that code over all
+ * batch entries b (parent rows cover the whole parent cell, as the
+ * aggregates of Eq. (aggregates) do):
+ *   S_x <- lambda S_x + (1 - lambda) sum_b sums[b][h][x],
+ *   N_x <- lambda N_x + (1 - lambda) sum_b counts[b][h][x].
+ * Parents take the unconstrained mean, C_p = S_p / N_p. The children of p,
+ * with unconstrained means M_c = S_c / N_c, are projected onto the constraint
+ * (mean of the children = C_p) by the mass-weighted least-squares solution
+ * Eq. (child_constraint_solve):
+ *   delta = sum_c M_c - Ch C_p,  sigma = sum_c 1 / N_c,
+ *   C_pc = M_c - delta / (N_c sigma).
+ * S [H][Mtot][d] and Nema [H][Mtot] are updated in place; Cp_out [H][M0][d]
+ * and Cc_out [H][M0][Ch][d] receive the new codewords.
+ */
+void avqo_codebook_update(int B, int H, int d, int M0, int Ch, double lambda,
+                          const double* sums, const int64_t* counts, double* S, double* Nema,
+                          double* Cp_out, double* Cc_out) {
+  int Mtot = M0 * (1 + Ch);
+#pragma omp parallel for schedule(static)
+  for (int h = 0; h < H; ++h) {
+    for (int x = 0; x < Mtot; ++x) {
+      double n = 0.0;
+      for (int b = 0; b < B; ++b) n += (double)counts[((long long)b * H + h) * Mtot + x];
+      long long r = (long long)h * Mtot + x;
+      Nema[r] = lambda * Nema[r] + (1.0 - lambda) * n;
+      for (int e = 0; e < d; ++e) {
+        double sx = 0.0;
+        for (int b = 0; b < B; ++b) sx += sums[(((long long)b * H + h) * Mtot + x) * d + e];
+        S[r * d + e] = lambda * S[r * d + e] + (1.0 - lambda) * sx;
+      }
+    }
+    for (int p = 0; p < M0; ++p) {
+      long long rp = (long long)h * Mtot + p;
+      double* cp = Cp_out + ((long long)h * M0 + p) * d;
+      for (int e = 0; e < d; ++e) cp[e] = S[rp * d + e] / Nema[rp];
+      if (Ch == 0) continue;
+      double sigma = 0.0;
+      for (int c = 0; c < Ch; ++c) sigma += 1.0 / Nema[(long long)h * Mtot + M0 + p * Ch + c];
+      for (int e = 0; e < d; ++e) {
+        double delta = -(double)Ch * cp[e];
+        for (int c = 0; c < Ch; ++c) {
+          long long rc = (long long)h * Mtot + M0 + p * Ch + c;
+          delta += S[rc * d + e] / Nema[rc];
+        }
+        for (int c = 0; c < Ch; ++c) {
+          long long rc = (long long)h * Mtot + M0 + p * Ch + c;
+          Cc_out[(((long long)h * M0 + p) * Ch + c) * d + e] =
+              S[rc * d + e] / Nema[rc] - delta / (Nema[rc] * sigma);
+        }
+      }
+    }
+  }
+}

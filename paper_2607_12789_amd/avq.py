@@ -21,7 +21,8 @@ AVQ_OK, AVQ_ERR_INVALID_ARG, AVQ_ERR_UNSUPPORTED, AVQ_ERR_DEVICE = 0, 1, 2, 3
 AVQ_F32, AVQ_BF16 = 0, 1
 _DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
 SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_bytes", "avq_assign",
-           "avq_aggregate", "avq_attention_fwd", "avq_attention_fwd_tiled")
+           "avq_aggregate", "avq_attention_fwd", "avq_attention_fwd_tiled",
+           "avq_codebook_update")
 IMPORTANCE_TILE = 64  # parents per codeword tile of attention_fwd(tiled_importance=True)
 
 
@@ -54,8 +55,10 @@ def lib():
         for name in ("avq_attention_fwd", "avq_attention_fwd_tiled"):
             getattr(L, name).argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32, i32,
                                          vp, vp, vp, vp, vp, vp, vp, vp]
+        L.avq_codebook_update.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, ctypes.c_float,
+                                          vp, vp, vp, vp, vp, vp, vp]
         for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd",
-                     "avq_attention_fwd_tiled"):
+                     "avq_attention_fwd_tiled", "avq_codebook_update"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -192,3 +195,31 @@ def forward(Q, K, V, Cp, Cc, P: int, block_q: int, stream=None):
     _, code_idx = assign(K, Cp, Cc, stream=stream)
     packed, _, _ = aggregate(V, code_idx, M0, Ch, stream=stream)
     return attention_fwd(Q, Cp, Cc, packed, P, block_q, stream=stream)
+
+
+def codebook_update(sums, counts, S, Nema, M0: int, Ch: int, lam: float, Cp_out=None,
+                    Cc_out=None, dtype=None, stream=None):
+    """EMA codebook step with the constrained child projection
+    (``avq_codebook_update``). sums [B, H, Mtot, d] fp32 and counts
+    [B, H, Mtot] int32 are the aggregates of the keys; S [H, Mtot, d] and
+    Nema [H, Mtot] (fp32) are updated in place. Returns (Cp, Cc) in ``dtype``
+    (default bfloat16 unless Cp_out is given)."""
+    B, H, Mtot, d = sums.shape
+    if Mtot != M0 * (1 + Ch):
+        raise ValueError(f"sums hold {Mtot} codes, expected M0 * (1 + Ch) = {M0 * (1 + Ch)}")
+    _dev(sums, "sums", torch.float32)
+    _dev(counts, "counts", torch.int32, (B, H, Mtot))
+    _dev(S, "S", torch.float32, (H, Mtot, d))
+    _dev(Nema, "Nema", torch.float32, (H, Mtot))
+    if dtype is None:
+        dtype = Cp_out.dtype if Cp_out is not None else torch.bfloat16
+    if Cp_out is None:
+        Cp_out = torch.empty((H, M0, d), dtype=dtype, device=sums.device)
+    if Cc_out is None:
+        Cc_out = torch.empty((H, M0, Ch, d), dtype=dtype, device=sums.device)
+    _dev(Cp_out, "Cp_out", dtype, (H, M0, d))
+    _dev(Cc_out, "Cc_out", dtype, (H, M0, Ch, d))
+    _check(lib().avq_codebook_update(_dtype_code(Cp_out), B, H, d, M0, Ch, float(lam), _ptr(sums),
+                                     _ptr(counts), _ptr(S), _ptr(Nema), _ptr(Cp_out),
+                                     _ptr(Cc_out), _stream(stream)))
+    return Cp_out, Cc_out

@@ -16,7 +16,8 @@ PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
 CSRC = PKG / "csrc"
 LIB = PKG / "libavq.so"
-SOURCES = ["avq_api.hip", "avq_assign.hip", "avq_aggregate.hip", "avq_attention.hip"]
+SOURCES = ["avq_api.hip", "avq_assign.hip", "avq_aggregate.hip", "avq_attention.hip",
+           "avq_codebook.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 COMPILE_FLAGS = [

@@ -24,6 +24,10 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
                             const void* Q, const void* Cp, const void* Cc, const void* packed,
                             void* Y, int32_t* topp_idx,
                             float* importance, bool tiled, hipStream_t stream);
+template <typename T>
+hipError_t launch_codebook_update(int B, int H, int d, int M0, int Ch, float lam,
+                                  const float* sums, const int32_t* counts, float* S,
+                                  float* Nema, void* Cp_out, void* Cc_out, hipStream_t stream);
 }  // namespace avq
 
 namespace avq {
@@ -228,6 +232,29 @@ avq_status_t avq_attention_fwd_tiled(avq_dtype_t dtype, int32_t B, int32_t H, in
                                      int32_t* topp_idx, float* importance, void* stream) {
   return attention("avq_attention_fwd_tiled", true, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp,
                    Cc, packed, Y, topp_idx, importance, stream);
+}
+
+avq_status_t avq_codebook_update(avq_dtype_t dtype, int32_t B, int32_t H, int32_t d,
+                                 int32_t M0, int32_t Ch, float lambda, const float* sums,
+                                 const int32_t* counts, float* S, float* Nema, void* Cp_out,
+                                 void* Cc_out, void* stream) {
+  avq_status_t st = check_common(dtype, B, H, 1, d, M0, Ch);
+  if (st != AVQ_OK) return st;
+  if (!(lambda > 0.f && lambda <= 1.f))
+    return fail(AVQ_ERR_INVALID_ARG, "lambda=%g outside (0, 1]", (double)lambda);
+  if (!sums || !counts || !S || !Nema || !Cp_out || (!Cc_out && Ch > 0))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_codebook_update: null pointer argument");
+  if (!aligned16(sums) || !aligned16(counts) || !aligned16(S) || !aligned16(Nema) ||
+      !aligned16(Cp_out) || !aligned16(Cc_out))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_codebook_update: arrays must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e =
+      dtype == AVQ_BF16
+          ? avq::launch_codebook_update<avq::bf16>(B, H, d, M0, Ch, lambda, sums, counts, S, Nema,
+                                                   Cp_out, Cc_out, s)
+          : avq::launch_codebook_update<float>(B, H, d, M0, Ch, lambda, sums, counts, S, Nema,
+                                               Cp_out, Cc_out, s);
+  return from_hip(e, "avq_codebook_update launch");
 }
 
 }  // extern "C"

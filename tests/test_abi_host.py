@@ -150,3 +150,27 @@ def test_binding_refuses_cpu_tensors():
     Cc = torch.zeros(1, 4, 2, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         avq.assign(K, Cp, Cc)
+
+
+def update(L, dtype=BF16, B=1, H=1, d=64, M0=4, Ch=2, lam=0.9, ptrs=(FAKE,) * 6):
+    return L.avq_codebook_update(dtype, B, H, d, M0, Ch, lam, *ptrs, NULL)
+
+
+def test_codebook_update_validation(L):
+    for lam in (0.0, -0.5, 1.5, float("nan")):
+        assert update(L, lam=lam) == INVALID
+        assert "lambda" in L.avq_last_error().decode()
+    assert update(L, lam=1.0, ptrs=(FAKE,) * 5 + (ctypes.c_void_p(24),)) == INVALID  # lambda 1 ok
+    assert "aligned" in L.avq_last_error().decode()
+    for i in range(6):
+        ptrs = [FAKE] * 6
+        ptrs[i] = NULL
+        assert update(L, ptrs=ptrs) == INVALID
+        assert "null" in L.avq_last_error().decode()
+    # Ch = 0: no children to write
+    assert update(L, Ch=0, ptrs=(FAKE,) * 4 + (ctypes.c_void_p(24), NULL)) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
+    assert update(L, d=96) == UNSUPPORTED
+    assert update(L, Ch=3) == UNSUPPORTED
+    assert update(L, M0=0) == INVALID
+

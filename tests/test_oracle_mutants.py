@@ -51,6 +51,15 @@ MUTANTS = [
     ("tiled importance scales by the partial denominator of the tile alone",
      "if (n[a] > 0) zsum += (double)n[a] * exp(S[a] - mu);",
      "if (n[a] > 0) zsum = (double)n[a] * exp(S[a] - mu);"),
+    ("projection ignores the child masses",
+     "- delta / (Nema[rc] * sigma);", "- delta / (double)Ch;"),
+    ("EMA adds the batch statistics at full weight",
+     "Nema[r] = lambda * Nema[r] + (1.0 - lambda) * n;", "Nema[r] = lambda * Nema[r] + n;"),
+    ("harmonic weight without the reciprocal",
+     "sigma += 1.0 / Nema[(long long)h * Mtot + M0 + p * Ch + c];",
+     "sigma += Nema[(long long)h * Mtot + M0 + p * Ch + c];"),
+    ("constraint residual with the wrong sign",
+     "double delta = -(double)Ch * cp[e];", "double delta = (double)Ch * cp[e];"),
 ]
 
 PIN_CALLS = [
@@ -69,6 +78,9 @@ PIN_CALLS = [
     lambda: pins.test_tiled_importance_last_tile_is_exact(3),
     pins.test_tiled_importance_first_tile_closed_form,
     lambda: pins.test_tiled_importance_zero_queries(3),
+    pins.test_codebook_update_keeps_the_constraint,
+    lambda: pins.test_codebook_update_solves_the_weighted_least_squares(4),
+    pins.test_codebook_update_ema_closed_form,
 ]
 
 

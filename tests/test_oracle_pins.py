@@ -434,3 +434,113 @@ def test_empty_far_children_do_not_poison():
         khat = ref.quantised_keys(Cp[0], Cc[0], o["parent_idx"][0, 0], o["code_idx"][0, 0])
         np.testing.assert_allclose(o["Y"][0, 0, rows], ref.sdpa(Q[0, 0, rows], khat, V[0, 0]),
                                    rtol=1e-9, atol=1e-11)
+
+
+# ---------------------------------------------------------------- codebook update
+
+def _ema_state(H=2, M0=5, Ch=4, d=6, B=3, seed=0):
+    """A random EMA state and batch statistics (positive masses)."""
+    rng = np.random.default_rng(seed)
+    Mtot = M0 * (1 + Ch)
+    S = rng.standard_normal((H, Mtot, d)) * 3
+    Nema = rng.uniform(0.5, 20.0, (H, Mtot))
+    sums = rng.standard_normal((B, H, Mtot, d)) * 5
+    counts = rng.integers(0, 30, (B, H, Mtot))
+    return S, Nema, sums, counts
+
+
+def test_codebook_update_keeps_the_constraint():
+    """App. A: after the update every parent is the mean of its children."""
+    S, Nema, sums, counts = _ema_state()
+    _, _, Cp, Cc = oracle.codebook_update(sums, counts, S, Nema, 5, 4, 0.9)
+    np.testing.assert_allclose(Cc.mean(axis=2), Cp, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("Ch", [1, 2, 4, 8])
+def test_codebook_update_solves_the_weighted_least_squares(Ch):
+    """Eq. (child_constraint_solve) is the minimiser of sum_c N_c ||M_c - C_c||^2
+    under mean(C_c) = C_p: checked against the KKT system solved by
+    numpy.linalg.solve, per parent and dimension."""
+    M0, d = 3, 5
+    S, Nema, sums, counts = _ema_state(M0=M0, Ch=Ch, d=d, seed=Ch)
+    S2, N2, Cp, Cc = oracle.codebook_update(sums, counts, S, Nema, M0, Ch, 0.7)
+    for h in range(S.shape[0]):
+        for p in range(M0):
+            rows = M0 + p * Ch + np.arange(Ch)
+            Nc = N2[h, rows]
+            M = S2[h, rows] / Nc[:, None]
+            # unknowns C_1..C_Ch and the multiplier mu:
+            # 2 N_c (C_c - M_c) + mu = 0;  sum_c C_c = Ch C_p
+            A = np.zeros((Ch + 1, Ch + 1))
+            A[:Ch, :Ch] = np.diag(2 * Nc)
+            A[:Ch, Ch] = 1.0
+            A[Ch, :Ch] = 1.0
+            for e in range(d):
+                rhs = np.concatenate([2 * Nc * M[:, e], [Ch * Cp[h, p, e]]])
+                sol = np.linalg.solve(A, rhs)
+                np.testing.assert_allclose(Cc[h, p, :, e], sol[:Ch], rtol=1e-10, atol=1e-10)
+
+
+def test_codebook_update_ema_closed_form():
+    """Constant inputs: S' = lambda S + (1 - lambda) B s and
+    N' = lambda N + (1 - lambda) B n, worked by hand for lambda = 0.75,
+    S = 4, N = 2, B = 3 batches of sums 8 and counts 5: S' = 9, N' = 5.25."""
+    B, H, M0, Ch, d = 3, 1, 2, 2, 3
+    Mtot = M0 * (1 + Ch)
+    S = np.full((H, Mtot, d), 4.0)
+    Nema = np.full((H, Mtot), 2.0)
+    sums = np.full((B, H, Mtot, d), 8.0)
+    counts = np.full((B, H, Mtot), 5)
+    S2, N2, Cp, Cc = oracle.codebook_update(sums, counts, S, Nema, M0, Ch, 0.75)
+    np.testing.assert_array_equal(S2, 9.0)
+    np.testing.assert_array_equal(N2, 5.25)
+    np.testing.assert_allclose(Cp, 9.0 / 5.25, rtol=1e-15)
+    np.testing.assert_allclose(Cc, 9.0 / 5.25, rtol=1e-15)  # already constrained
+
+
+def test_codebook_update_lambda_zero_gives_batch_means():
+    """lambda = 0: the parents move to the mean of the keys of their cell and
+    the children, whose cells hold keys, to a projection of their own means;
+    compared with means computed from the keys by numpy grouping."""
+    w = small(B=2, N=300, sigma_k=0.2)
+    x = inputs.generate(w)
+    a = oracle.assign(x["K"], x["Cp"], x["Cc"])
+    sums, counts = oracle.aggregate(x["K"], a["parent_idx"], a["code_idx"], w.M0, w.Ch)
+    Mtot = w.Mtot
+    S0 = np.zeros((w.H, Mtot, w.d))
+    N0 = np.ones((w.H, Mtot))
+    _, N2, Cp, _ = oracle.codebook_update(sums, counts, S0, N0, w.M0, w.Ch, 0.0)
+    K = np64(x["K"])
+    for h in range(w.H):
+        keys = K[:, h].reshape(-1, w.d)
+        par = a["parent_idx"][:, h].reshape(-1)
+        for p in range(w.M0):
+            sel = par == p
+            assert N2[h, p] == sel.sum()
+            if sel.any():
+                np.testing.assert_allclose(Cp[h, p], keys[sel].mean(axis=0), rtol=1e-12,
+                                           atol=1e-12)
+
+
+def test_codebook_update_equal_masses_shift_uniformly():
+    """Equal child masses: the projection moves every child by the same
+    amount, -delta / Ch (the plain Euclidean projection)."""
+    S, Nema, sums, counts = _ema_state(M0=2, Ch=4)
+    Nema[:] = 3.0
+    counts[:] = 2
+    S2, N2, Cp, Cc = oracle.codebook_update(sums, counts, S, Nema, 2, 4, 0.5)
+    M = (S2[:, 2:] / N2[:, 2:, None]).reshape(2, 2, 4, -1)
+    shift = Cc - M
+    np.testing.assert_allclose(shift, np.broadcast_to(shift[:, :, :1], shift.shape), atol=1e-12)
+    delta = M.sum(axis=2) - 4 * Cp
+    np.testing.assert_allclose(shift[:, :, 0], -delta / 4, atol=1e-12)
+
+
+def test_codebook_update_heavier_children_move_less():
+    """Two children: each is displaced in inverse proportion to its mass."""
+    S, Nema, sums, counts = _ema_state(M0=1, Ch=2, seed=3)
+    S2, N2, Cp, Cc = oracle.codebook_update(sums, counts, S, Nema, 1, 2, 0.8)
+    M = S2[:, 1:] / N2[:, 1:, None]
+    d1 = np.linalg.norm(Cc[:, 0, 0] - M[:, 0], axis=-1)
+    d2 = np.linalg.norm(Cc[:, 0, 1] - M[:, 1], axis=-1)
+    np.testing.assert_allclose(d1 * N2[:, 1], d2 * N2[:, 2], rtol=1e-10)
