@@ -90,10 +90,11 @@ class Runner:
     """Device buffers of one workload and its timed step (the three entry
     points on torch's current stream)."""
 
-    def __init__(self, w, x, dev, tiled=False):
+    def __init__(self, w, x, dev, tiled=False, order=None):
         import torch
         from paper_2607_12789_amd import avq
         self.avq, self.w, self.tiled = avq, w, tiled
+        self.order = None if order is None else order.to(dev)
         self.xd = {k: v.to(dev) for k, v in x.items()}
         B, H, N, d = w.B, w.H, w.N, w.d
         self.par = torch.empty((B, H, N), dtype=torch.int32, device=dev)
@@ -113,7 +114,7 @@ class Runner:
         avq.aggregate(xd["V"], self.code, w.M0, w.Ch, self.packed, self.counts)
         if ev: ev[2].record()
         avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], self.packed, w.P, w.block_q, Y=self.Y,
-                          tiled_importance=self.tiled)
+                          tiled_importance=self.tiled, query_order=self.order)
         if ev: ev[3].record()
 
     def timed(self, steps: int, warmup: int):
@@ -271,6 +272,9 @@ def main():
                     help="also launch one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--tiled-importance", action="store_true",
                     help="use the App. B importance (one parent sweep) instead of the exact one")
+    ap.add_argument("--query-order", choices=["token", "gilbert", "random"], default="token",
+                    help="order of the queries: token order, or the tokens as a square grid "
+                         "along a Gilbert curve, or a random permutation")
     ap.add_argument("--codebook-update", action="store_true",
                     help="time the codebook EMA step (App. A) instead")
     ap.add_argument("--sweep", action="store_true",
@@ -302,7 +306,18 @@ def main():
     x = inputs.generate(w)
     dev = torch.device("cuda:0")
     B, H, N, d, M0, Ch, P = w.B, w.H, w.N, w.d, w.M0, w.Ch, w.P
-    ms_per_step, per = Runner(w, x, dev, args.tiled_importance).timed(args.steps, args.warmup)
+    order = None
+    if args.query_order == "gilbert":
+        side = int(round(math.sqrt(w.N)))
+        if side * side != w.N:
+            print(f"--query-order gilbert needs a square number of tokens (N={w.N})",
+                  file=sys.stderr)
+            sys.exit(2)
+        order = avq.gilbert_order(side, side)[0]
+    elif args.query_order == "random":
+        order = torch.randperm(w.N, generator=torch.Generator().manual_seed(0)).to(torch.int32)
+    ms_per_step, per = Runner(w, x, dev, args.tiled_importance, order).timed(args.steps,
+                                                                            args.warmup)
     # per-kernel average launch duration over the timed steps
     t_assign, t_agg, t_attn = (sum(p[i] for p in per) / max(len(per), 1) for i in range(3))
     if args.calib_copy_mib > 0:
@@ -315,7 +330,7 @@ def main():
     qh = B * H * N
     flops_attn = 4.0 * d * (M0 + P * Ch) * qh
     achieved = flops_attn / (t_attn * 1e-3) / 1e12
-    traffic = None if args.tiled_importance else read_traffic()
+    traffic = None if (args.tiled_importance or order is not None) else read_traffic()
     line = {
         "metric": METRIC,
         "value": qh / (ms_per_step * 1e-3),
@@ -332,10 +347,11 @@ def main():
         "config": {"workload": f"{w.name}: {w.describe()}", "B": B, "H": H, "N": N, "d": d,
                    "M0": M0, "Ch": Ch, "P": P, "block_q": w.block_q,
                    "importance": "tiled (App. B, 64-parent tiles)" if args.tiled_importance
-                   else "exact"},
+                   else "exact", "query_order": args.query_order},
         "kernels_ms": {"assign": t_assign, "aggregate": t_agg, "attention_fwd": t_attn},
-        "roofline": {"kernel": "avq_attention_fwd_tiled" if args.tiled_importance
-                     else "avq_attention_fwd", "bound": "mfma", "achieved": achieved,
+        "roofline": {"kernel": ("avq_attention_fwd_ordered" if order is not None else
+                                "avq_attention_fwd_tiled" if args.tiled_importance
+                                else "avq_attention_fwd"), "bound": "mfma", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                      "flops_per_launch": flops_attn},

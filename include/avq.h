@@ -19,6 +19,9 @@
  *                      App. B (Eq. (aproxdenom), (codewordimportance))
  *   avq_codebook_update  EMA codebook statistics and the constrained child
  *                      projection (App. A, Eq. (child_constraint_solve))
+ *   avq_attention_fwd_ordered  attention with the queries in a given order
+ *                      (the space-filling-curve reordering of Sec. 4)
+ *   avq_gilbert_order  host helper: that order for a 2-D grid of tokens
  *
  * Conventions shared by every call:
  *   - Every array argument is a DEVICE pointer owned by the caller, contiguous,
@@ -210,6 +213,54 @@ avq_status_t avq_attention_fwd_tiled(avq_dtype_t dtype, int32_t B, int32_t H, in
                                      int32_t block_q, const void* Q, const void* Cp,
                                      const void* Cc, const void* packed, void* Y,
                                      int32_t* topp_idx, float* importance, void* stream);
+
+/*
+ * avq_attention_fwd_ordered - avq_attention_fwd (tiled_importance = 0) or
+ * avq_attention_fwd_tiled (tiled_importance = 1) with the queries taken in
+ * the order query_order instead of token order: query tile t is the tokens
+ * query_order[t*block_q .. t*block_q + block_q - 1]. The result equals
+ * permuting the rows of Q by query_order, calling the unordered entry point
+ * and writing each output row back to its token: Y[b][h][query_order[k]] is
+ * the output of query position k. The reordering is the one the paper
+ * applies before tiling (Sec. 4, along a space-filling curve; see
+ * avq_gilbert_order), so that the tokens of a tile, which share one top-P
+ * selection, are spatial neighbours. Keys, values and the aggregates are
+ * order-free (Sec. 3.2) and are not reordered.
+ *
+ *   query_order  [N] int32, device, a permutation of 0 .. N-1 shared by every
+ *                batch entry and head. An entry outside [0, N) makes that
+ *                query position take no part (no output row is written for
+ *                it); a repeated entry writes that token's row more than once,
+ *                in an unspecified order, and leaves some token unwritten.
+ *   topp_idx, importance  per tile of the ORDERED queries.
+ * Other arguments, layouts, ownership and errors as avq_attention_fwd.
+ */
+avq_status_t avq_attention_fwd_ordered(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                                       int32_t d, int32_t M0, int32_t Ch, int32_t P,
+                                       int32_t block_q, const int32_t* query_order,
+                                       int32_t tiled_importance, const void* Q, const void* Cp,
+                                       const void* Cc, const void* packed, void* Y,
+                                       int32_t* topp_idx, float* importance, void* stream);
+
+/*
+ * avq_gilbert_order - host helper: the cells of a width x height grid of
+ * tokens (token y*width + x) in the order of a generalized Hilbert curve
+ * (the Gilbert curve the paper reorders tokens along, Sec. 4,
+ * Fig. per-tile adaptivity, App. spatial reordering ablation).
+ *
+ * The curve starts at cell (0, 0), visits every cell once, and each step
+ * moves to a 4-neighbour, except for at most one diagonal step on some grids
+ * with odd sides; on a 2^k x 2^k grid it is a Hilbert curve. Any run of
+ * consecutive cells therefore covers a compact region, whatever the tile size.
+ *
+ *   width, height  grid sizes, >= 1, width*height <= 2^24
+ *   order          [width*height] int32, HOST, out: order[k] = token of the
+ *                  k-th cell (the query_order of avq_attention_fwd_ordered)
+ *   rank           [width*height] int32, HOST, out, nullable: the inverse,
+ *                  rank[order[k]] = k
+ * Runs on the host only (no device call); copy order to the device once.
+ */
+avq_status_t avq_gilbert_order(int32_t width, int32_t height, int32_t* order, int32_t* rank);
 
 /*
  * avq_codebook_update - one step of the codebook's exponential moving

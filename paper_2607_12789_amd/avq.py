@@ -22,7 +22,7 @@ AVQ_F32, AVQ_BF16 = 0, 1
 _DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
 SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_bytes", "avq_assign",
            "avq_aggregate", "avq_attention_fwd", "avq_attention_fwd_tiled",
-           "avq_codebook_update")
+           "avq_codebook_update", "avq_attention_fwd_ordered", "avq_gilbert_order")
 IMPORTANCE_TILE = 64  # parents per codeword tile of attention_fwd(tiled_importance=True)
 
 
@@ -55,10 +55,14 @@ def lib():
         for name in ("avq_attention_fwd", "avq_attention_fwd_tiled"):
             getattr(L, name).argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32, i32,
                                          vp, vp, vp, vp, vp, vp, vp, vp]
+        L.avq_attention_fwd_ordered.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32, i32,
+                                                i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.avq_gilbert_order.argtypes = [i32, i32, vp, vp]
         L.avq_codebook_update.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, ctypes.c_float,
                                           vp, vp, vp, vp, vp, vp, vp]
         for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd",
-                     "avq_attention_fwd_tiled", "avq_codebook_update"):
+                     "avq_attention_fwd_tiled", "avq_codebook_update",
+                     "avq_attention_fwd_ordered", "avq_gilbert_order"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -154,10 +158,13 @@ def aggregate(V, code_idx, M0: int, Ch: int, packed=None, counts=None, Vbar=None
 
 def attention_fwd(Q, Cp, Cc, packed, P: int, block_q: int, Y=None, topp_idx=None,
                   importance=None, debug: bool = False, tiled_importance: bool = False,
-                  stream=None):
+                  query_order=None, stream=None):
     """Refined-codebook attention (``avq_attention_fwd``, or
     ``avq_attention_fwd_tiled`` with ``tiled_importance``: the importance of
     App. B over tiles of IMPORTANCE_TILE parents).
+
+    query_order (int32 [N] on the GPU): take the queries in this order
+    (``avq_attention_fwd_ordered``); Y rows still land on their tokens.
 
     Returns Y, or (Y, topp_idx, importance) when ``debug`` is set (the two
     debug outputs are then allocated if not given).
@@ -181,9 +188,16 @@ def attention_fwd(Q, Cp, Cc, packed, P: int, block_q: int, Y=None, topp_idx=None
         _dev(topp_idx, "topp_idx", torch.int32, (B, H, T, P))
     if importance is not None:
         _dev(importance, "importance", torch.float32, (B, H, T, M0))
-    fn = lib().avq_attention_fwd_tiled if tiled_importance else lib().avq_attention_fwd
-    _check(fn(_dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(Q), _ptr(Cp), _ptr(Cc),
-              _ptr(packed), _ptr(Y), _ptr(topp_idx), _ptr(importance), _stream(stream)))
+    if query_order is not None:
+        _dev(query_order, "query_order", torch.int32, (N,))
+        _check(lib().avq_attention_fwd_ordered(
+            _dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(query_order),
+            int(bool(tiled_importance)), _ptr(Q), _ptr(Cp), _ptr(Cc), _ptr(packed), _ptr(Y),
+            _ptr(topp_idx), _ptr(importance), _stream(stream)))
+    else:
+        fn = lib().avq_attention_fwd_tiled if tiled_importance else lib().avq_attention_fwd
+        _check(fn(_dtype_code(Q), B, H, N, d, M0, Ch, P, block_q, _ptr(Q), _ptr(Cp), _ptr(Cc),
+                  _ptr(packed), _ptr(Y), _ptr(topp_idx), _ptr(importance), _stream(stream)))
     if debug:
         return Y, topp_idx, importance
     return Y
@@ -223,3 +237,15 @@ def codebook_update(sums, counts, S, Nema, M0: int, Ch: int, lam: float, Cp_out=
                                      _ptr(counts), _ptr(S), _ptr(Nema), _ptr(Cp_out),
                                      _ptr(Cc_out), _stream(stream)))
     return Cp_out, Cc_out
+
+
+def gilbert_order(width: int, height: int):
+    """Tokens of a width x height grid (token y*width + x) in the order of a
+    generalized Hilbert curve (``avq_gilbert_order``, host only). Returns
+    (order, rank) as int32 CPU tensors, rank[order[k]] = k."""
+    n = int(width) * int(height)
+    order = torch.empty(max(n, 0), dtype=torch.int32)
+    rank = torch.empty(max(n, 0), dtype=torch.int32)
+    _check(lib().avq_gilbert_order(int(width), int(height), _ptr(order), _ptr(rank)))
+    return order, rank
+

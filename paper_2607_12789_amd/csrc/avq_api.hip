@@ -23,7 +23,9 @@ template <typename T, int D>
 hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
                             const void* Q, const void* Cp, const void* Cc, const void* packed,
                             void* Y, int32_t* topp_idx,
-                            float* importance, bool tiled, hipStream_t stream);
+                            float* importance, bool tiled, const int32_t* order,
+                            hipStream_t stream);
+long long gilbert_order(int width, int height, int32_t* order);
 template <typename T>
 hipError_t launch_codebook_update(int B, int H, int d, int M0, int Ch, float lam,
                                   const float* sums, const int32_t* counts, float* S,
@@ -180,10 +182,11 @@ namespace {
 
 // avq_attention_fwd and avq_attention_fwd_tiled: the same checks and launch;
 // tiled selects the App. B importance.
-avq_status_t attention(const char* name, bool tiled, avq_dtype_t dtype, int32_t B, int32_t H,
-                       int32_t N, int32_t d, int32_t M0, int32_t Ch, int32_t P, int32_t block_q,
-                       const void* Q, const void* Cp, const void* Cc, const void* packed, void* Y,
-                       int32_t* topp_idx, float* importance, void* stream) {
+avq_status_t attention(const char* name, bool tiled, const int32_t* order, avq_dtype_t dtype,
+                       int32_t B, int32_t H, int32_t N, int32_t d, int32_t M0, int32_t Ch,
+                       int32_t P, int32_t block_q, const void* Q, const void* Cp, const void* Cc,
+                       const void* packed, void* Y, int32_t* topp_idx, float* importance,
+                       void* stream) {
   avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
   if (st != AVQ_OK) return st;
   if (P < 0 || P > M0) return fail(AVQ_ERR_INVALID_ARG, "P=%d outside [0, M0=%d]", P, M0);
@@ -194,21 +197,21 @@ avq_status_t attention(const char* name, bool tiled, avq_dtype_t dtype, int32_t 
   if (!Q || !Cp || (!Cc && Ch > 0) || !packed || !Y)
     return fail(AVQ_ERR_INVALID_ARG, "%s: null pointer argument", name);
   if (!aligned16(Q) || !aligned16(Cp) || !aligned16(Cc) || !aligned16(packed) ||
-      !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance))
+      !aligned16(Y) || !aligned16(topp_idx) || !aligned16(importance) || !aligned16(order))
     return fail(AVQ_ERR_INVALID_ARG, "%s: arrays must be 16-byte aligned", name);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int BH = B * H;
   hipError_t e;
   if (dtype == AVQ_BF16)
     e = d == 64 ? avq::launch_attention<avq::bf16, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
-                                                       packed, Y, topp_idx, importance, tiled, s)
+                                                       packed, Y, topp_idx, importance, tiled, order, s)
                 : avq::launch_attention<avq::bf16, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
-                                                        packed, Y, topp_idx, importance, tiled, s);
+                                                        packed, Y, topp_idx, importance, tiled, order, s);
   else
     e = d == 64 ? avq::launch_attention<float, 64>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
-                                                   packed, Y, topp_idx, importance, tiled, s)
+                                                   packed, Y, topp_idx, importance, tiled, order, s)
                 : avq::launch_attention<float, 128>(BH, H, N, M0, Ch, P, block_q, Q, Cp, Cc,
-                                                    packed, Y, topp_idx, importance, tiled, s);
+                                                    packed, Y, topp_idx, importance, tiled, order, s);
   return from_hip(e, "attention launch");
 }
 
@@ -221,7 +224,7 @@ avq_status_t avq_attention_fwd(avq_dtype_t dtype, int32_t B, int32_t H, int32_t 
                                const void* Q, const void* Cp, const void* Cc,
                                const void* packed, void* Y,
                                int32_t* topp_idx, float* importance, void* stream) {
-  return attention("avq_attention_fwd", false, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp, Cc,
+  return attention("avq_attention_fwd", false, nullptr, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp, Cc,
                    packed, Y, topp_idx, importance, stream);
 }
 
@@ -230,7 +233,7 @@ avq_status_t avq_attention_fwd_tiled(avq_dtype_t dtype, int32_t B, int32_t H, in
                                      int32_t block_q, const void* Q, const void* Cp,
                                      const void* Cc, const void* packed, void* Y,
                                      int32_t* topp_idx, float* importance, void* stream) {
-  return attention("avq_attention_fwd_tiled", true, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp,
+  return attention("avq_attention_fwd_tiled", true, nullptr, dtype, B, H, N, d, M0, Ch, P, block_q, Q, Cp,
                    Cc, packed, Y, topp_idx, importance, stream);
 }
 
@@ -255,6 +258,34 @@ avq_status_t avq_codebook_update(avq_dtype_t dtype, int32_t B, int32_t H, int32_
           : avq::launch_codebook_update<float>(B, H, d, M0, Ch, lambda, sums, counts, S, Nema,
                                                Cp_out, Cc_out, s);
   return from_hip(e, "avq_codebook_update launch");
+}
+
+avq_status_t avq_attention_fwd_ordered(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                                       int32_t d, int32_t M0, int32_t Ch, int32_t P,
+                                       int32_t block_q, const int32_t* query_order,
+                                       int32_t tiled_importance, const void* Q, const void* Cp,
+                                       const void* Cc, const void* packed, void* Y,
+                                       int32_t* topp_idx, float* importance, void* stream) {
+  if (!query_order)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_attention_fwd_ordered: null query_order");
+  if (tiled_importance != 0 && tiled_importance != 1)
+    return fail(AVQ_ERR_INVALID_ARG, "tiled_importance=%d: must be 0 or 1", tiled_importance);
+  return attention("avq_attention_fwd_ordered", tiled_importance == 1, query_order, dtype, B, H,
+                   N, d, M0, Ch, P, block_q, Q, Cp, Cc, packed, Y, topp_idx, importance, stream);
+}
+
+avq_status_t avq_gilbert_order(int32_t width, int32_t height, int32_t* order, int32_t* rank) {
+  if (width < 1 || height < 1)
+    return fail(AVQ_ERR_INVALID_ARG, "grid %d x %d: sizes must be positive", width, height);
+  if ((long long)width * height > (1LL << 24))
+    return fail(AVQ_ERR_UNSUPPORTED, "grid %d x %d: at most 2^24 cells", width, height);
+  if (!order) return fail(AVQ_ERR_INVALID_ARG, "avq_gilbert_order: null order");
+  const long long n = avq::gilbert_order(width, height, order);
+  if (n != (long long)width * height)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_gilbert_order: internal count mismatch");
+  if (rank)
+    for (long long k = 0; k < n; ++k) rank[order[k]] = (int32_t)k;
+  return ok();
 }
 
 }  // extern "C"

@@ -100,6 +100,7 @@ struct AttnArgs {
   void* Y;
   int32_t* topp_idx;
   float* importance;
+  const int32_t* order;  // nullable: token row of each query position
   int H, N, M0, Ch, P, block_q, n_tiles;
 };
 
@@ -166,14 +167,23 @@ void attention_kernel(AttnArgs args) {
   const T* cp_head = Cp + (size_t)h * M0 * D;
   const T* cc_head = Cc + (size_t)h * M0 * Ch * D;
 
+  // token row of query position i (the query order, if any; -1 for an entry
+  // outside [0, N), which then takes no part)
+  auto token_row = [&](int i) -> int {
+    if (args.order == nullptr) return i;
+    const int r = args.order[i];
+    return (unsigned)r < (unsigned)N ? r : -1;
+  };
+
   // ---- query fragments (B operand of S^T = C . Q^T) -------------------------
   QFrag qf[QS][KQ];
   bool qvalid[QS];
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
     const int i = row0 + 16 * s + c;
-    qvalid[s] = i < q_end;
-    const T* qrow = Q + ((size_t)bh * N + (qvalid[s] ? i : q_begin)) * D;
+    const int src = i < q_end ? token_row(i) : -1;
+    qvalid[s] = src >= 0;
+    const T* qrow = Q + ((size_t)bh * N + (qvalid[s] ? src : 0)) * D;
 #pragma unroll
     for (int kq = 0; kq < KQ; ++kq) {
       if constexpr (kB) {
@@ -745,7 +755,7 @@ void attention_kernel(AttnArgs args) {
     const float z = __shfl(X[DT][s][0], c, kWave);
     if (!qvalid[s]) continue;
     const float rinv = 1.f / z;
-    const int i = row0 + 16 * s + c;
+    const int i = token_row(row0 + 16 * s + c);
     T* yrow = static_cast<T*>(args.Y) + ((size_t)bh * N + i) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -779,7 +789,7 @@ template <typename T, int D>
 hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
                             const void* Q, const void* Cp, const void* Cc, const void* packed,
                             void* Y, int32_t* topp_idx, float* importance, bool tiled,
-                            hipStream_t stream) {
+                            const int32_t* order, hipStream_t stream) {
   AttnArgs a;
   a.Q = Q;
   a.Cp = Cp;
@@ -788,6 +798,7 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
   a.Y = Y;
   a.topp_idx = topp_idx;
   a.importance = importance;
+  a.order = order;
   a.H = H;
   a.N = N;
   a.M0 = M0;
@@ -806,7 +817,8 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
 #define AVQ_INSTANTIATE(T, D)                                                                \
   template hipError_t launch_attention<T, D>(int, int, int, int, int, int, int, const void*, \
                                              const void*, const void*, const void*, void*,   \
-                                             int32_t*, float*, bool, hipStream_t);
+                                             int32_t*, float*, bool, const int32_t*,     \
+                                             hipStream_t);
 AVQ_INSTANTIATE(bf16, 64)
 AVQ_INSTANTIATE(bf16, 128)
 AVQ_INSTANTIATE(float, 64)

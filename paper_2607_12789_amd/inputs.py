@@ -186,3 +186,63 @@ def dyadic_exact(B: int, H: int, N: int, d: int, M0: int, Ch: int, seed: int = 0
     v = rng.integers(-16, 17, size=(B, H, N, d)) / 8.0
     return {"Q": _round(q, dtype), "K": _round(k, dtype), "V": _round(v, dtype),
             "Cp": _round(cp, dtype), "Cc": _round(cc, dtype)}
+
+
+def spatial(w: Workload, width: int, height: int, regions: int = 48,
+            comps_per_region: int = 4) -> dict:
+    """Tokens on a width x height grid (token y*width + x, N = width*height)
+    whose keys and queries depend on where they lie, the 2-D structure of
+    image tokens that makes per-tile refinement adaptive (Sec. 4,
+    Fig. per-tile adaptivity).
+
+    Draw order (one PCG64 generator, fp64): the codebook as in ``generate``;
+    then per head: ``regions`` seed cells uniform on the grid (each token
+    belongs to the region of its nearest seed, lowest seed on ties) and, per
+    region, ``comps_per_region`` mixture components (children, or parents for a
+    flat codebook) uniform without replacement; then per (batch, head): each
+    token's component uniform over its region's, key = component +
+    sigma_k N(0, I); query = (q_scale / d) * component + (1 / sqrt(d)) N(0, I),
+    so that a query attends mostly to keys of its own component; values
+    N(0, 1). Rounding as in ``generate``.
+    """
+    N = width * height
+    if w.N != N:
+        raise ValueError(f"workload N={w.N} but the grid has {N} tokens")
+    rng = np.random.default_rng(w.seed)
+    B, H, d, M0, Ch = w.B, w.H, w.d, w.M0, w.Ch
+    cp = rng.standard_normal((H, M0, d))
+    if Ch > 0:
+        eps = w.sigma_c * rng.standard_normal((H, M0, Ch, d))
+        eps -= eps.mean(axis=2, keepdims=True)
+        cc = cp[:, :, None, :] + eps
+        comps = cc.reshape(H, M0 * Ch, d)
+    else:
+        cc = np.zeros((H, M0, 0, d))
+        comps = cp
+    n_comp = comps.shape[1]
+    ys, xs = np.divmod(np.arange(N), width)
+    region = np.empty((H, N), np.int64)
+    members = np.empty((H, regions, comps_per_region), np.int64)
+    for h in range(H):
+        seeds = rng.integers(0, N, size=regions)
+        sy, sx = np.divmod(seeds, width)
+        d2 = (ys[:, None] - sy[None, :]) ** 2 + (xs[:, None] - sx[None, :]) ** 2
+        region[h] = np.argmin(d2, axis=1)
+        for r in range(regions):
+            members[h, r] = rng.choice(n_comp, size=comps_per_region, replace=False)
+    k = np.empty((B, H, N, d))
+    q = np.empty((B, H, N, d))
+    for b in range(B):
+        for h in range(H):
+            pick = rng.integers(0, comps_per_region, size=N)
+            comp = members[h, region[h], pick]
+            k[b, h] = comps[h, comp] + w.sigma_k * rng.standard_normal((N, d))
+            q[b, h] = (w.q_scale / d) * comps[h, comp] + rng.standard_normal((N, d)) / math.sqrt(d)
+    v = rng.standard_normal((B, H, N, d))
+    return {
+        "Q": _round(q, w.dtype),
+        "K": _round(k, w.dtype),
+        "V": _round(v, w.dtype),
+        "Cp": _round(cp, w.dtype),
+        "Cc": _round(cc, w.dtype),
+    }

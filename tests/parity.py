@@ -45,13 +45,17 @@ def to_gpu(x: dict) -> dict:
     return {k: v.cuda() for k, v in x.items()}
 
 
-def gpu_forward(xd: dict, w, tiled: bool = False) -> dict:
+def gpu_forward(xd: dict, w, tiled: bool = False, query_order=None) -> dict:
     """Runs the three entry points and returns every output on the CPU
-    (tiled: the App. B importance entry point)."""
+    (tiled: the App. B importance entry point; query_order: the ordered entry
+    point, with Y returned in query order)."""
     par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
     packed, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
+    order = None if query_order is None else torch.as_tensor(query_order, dtype=torch.int32).cuda()
     Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q,
-                                     debug=True, tiled_importance=tiled)
+                                     debug=True, tiled_importance=tiled, query_order=order)
+    if order is not None:
+        Y = Y[:, :, order.long()]
     torch.cuda.synchronize()
     out = dict(parent_idx=par, code_idx=code, Vbar=Vbar, packed=packed, counts=counts, Y=Y,
                topp=topp, importance=imp)
@@ -284,12 +288,16 @@ def check_output(x, w, g, o, sel_ok) -> Report:
                   median_rel=float(f"{np.median(rel_rows):.3g}"), frob_rel=float(f"{fro:.3g}"))
 
 
-def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False) -> dict:
+def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False,
+            query_order=None) -> dict:
     """Runs GPU and oracle on the same inputs and checks every output.
 
     tiles_per_head: number of query tiles per head evaluated by the oracle
     (None: all). The first and last tile are always included. tiled: the
-    App. B importance on both sides (tiles of avq.IMPORTANCE_TILE parents)."""
+    App. B importance on both sides (tiles of avq.IMPORTANCE_TILE parents).
+    query_order: the GPU takes the queries in this order; the oracle gets Q
+    with its rows permuted the same way, and the GPU's Y is compared in that
+    order."""
     T = w.n_tiles
     mask = np.ones((w.B, w.H, T), np.uint8)
     if tiles_per_head is not None and tiles_per_head < T:
@@ -300,7 +308,9 @@ def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False) -> d
                 pick = rng.choice(T, tiles_per_head, replace=False)
                 mask[b, h, pick] = 1
                 mask[b, h, [0, T - 1]] = 1
-    g = gpu_forward(to_gpu(x), w, tiled)
+    g = gpu_forward(to_gpu(x), w, tiled, query_order)
+    if query_order is not None:
+        x = dict(x, Q=x["Q"][:, :, torch.as_tensor(query_order, dtype=torch.long)].contiguous())
     o = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], w.P, w.block_q,
                        recovered=recovered, tile_mask=mask,
                        importance_tile=avq.IMPORTANCE_TILE if tiled else None)

@@ -115,3 +115,28 @@ def topp_by_enumeration(w: np.ndarray, P: int):
         if best_key is None or key < best_key:
             best_key, best = key, [a for _, a in vals]
     return np.array(best, np.int64)
+
+
+def hilbert_cells(n: int):
+    """Cells (x, y) of the Hilbert curve of an n x n grid (n a power of two),
+    in curve order: the textbook conversion of a curve index to a cell, which
+    reads the index two bits at a time from the lowest, rotating or reflecting
+    the partial cell in each quadrant."""
+    xs = np.empty(n * n, np.int64)
+    ys = np.empty(n * n, np.int64)
+    for t0 in range(n * n):
+        t, x, y, s = t0, 0, 0, 1
+        while s < n:
+            rx = 1 & (t // 2)
+            ry = 1 & (t ^ rx)
+            if ry == 0:
+                if rx == 1:
+                    x, y = s - 1 - x, s - 1 - y
+                x, y = y, x
+            x += s * rx
+            y += s * ry
+            t //= 4
+            s *= 2
+        xs[t0], ys[t0] = x, y
+    return xs, ys
+

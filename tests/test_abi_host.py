@@ -174,3 +174,20 @@ def test_codebook_update_validation(L):
     assert update(L, Ch=3) == UNSUPPORTED
     assert update(L, M0=0) == INVALID
 
+
+def test_ordered_attention_validation(L):
+    def ordered(order=FAKE, tiled=0, **kw):
+        args = dict(dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, P=1, bq=64)
+        args.update(kw)
+        return L.avq_attention_fwd_ordered(args["dtype"], args["B"], args["H"], args["N"],
+                                           args["d"], args["M0"], args["Ch"], args["P"],
+                                           args["bq"], order, tiled, *(FAKE,) * 5, NULL, NULL,
+                                           NULL)
+    assert ordered(order=NULL) == INVALID
+    assert "query_order" in L.avq_last_error().decode()
+    assert ordered(tiled=2) == INVALID
+    assert ordered(order=ctypes.c_void_p(24)) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
+    assert ordered(d=96) == UNSUPPORTED
+    assert ordered(P=9) == INVALID
+

@@ -190,6 +190,70 @@ def test_tiled_single_tile_equals_exact(dtype):
         assert torch.equal(u, v)
 
 
+# Queries in a given order (Gilbert curve, or a random permutation) on
+# spatially structured tokens: against the oracle run on the permuted queries
+ORDERED = {
+    "gilbert_64x64": (small(M0=64, Ch=8, P=16, N=4096, B=1, H=2, block_q=64, q_scale=8.0), 64, 64,
+                      "gilbert", False),
+    "gilbert_28x28_tiled": (small(M0=128, Ch=8, P=16, N=784, B=2, H=2, block_q=128,
+                                  q_scale=8.0), 28, 28, "gilbert", True),
+    "random_40x25_fp32": (small(dtype="f32", M0=96, Ch=4, P=12, N=1000, B=1, H=3, block_q=100,
+                                q_scale=8.0), 40, 25, "random", False),
+}
+
+
+@pytest.mark.parametrize("name", list(ORDERED))
+def test_ordered_queries(name):
+    from paper_2607_12789_amd import avq
+    w, width, height, kind, tiled = ORDERED[name]
+    banner(name, w)
+    x = inputs.spatial(w, width, height)
+    if kind == "gilbert":
+        order = avq.gilbert_order(width, height)[0].numpy()
+    else:
+        order = np.random.default_rng(7).permutation(w.N).astype(np.int32)
+    res = parity.compare(x, w, tiled=tiled, query_order=order)
+    report(res)
+
+
+def test_identity_order_equals_unordered():
+    """query_order = 0 .. N-1 gives the unordered result bit for bit."""
+    from paper_2607_12789_amd import avq
+    w = small(Ch=8, P=6, N=700)
+    xd = parity.to_gpu(inputs.generate(w))
+    _, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+    packed, _, _ = avq.aggregate(xd["V"], code, w.M0, w.Ch)
+    ident = torch.arange(w.N, dtype=torch.int32, device="cuda")
+    for tiled in (False, True):
+        a = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q, debug=True,
+                              tiled_importance=tiled)
+        b = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q, debug=True,
+                              tiled_importance=tiled, query_order=ident)
+        for u, v in zip(a, b):
+            assert torch.equal(u, v)
+
+
+def test_order_entries_out_of_range_are_skipped():
+    """An entry outside [0, N) takes no part: its query position writes no
+    row; every other token's row equals the one of the valid permutation."""
+    from paper_2607_12789_amd import avq
+    w = small(Ch=4, P=0, N=500, B=1, H=1)
+    xd = parity.to_gpu(inputs.generate(w))
+    _, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+    packed, _, _ = avq.aggregate(xd["V"], code, w.M0, w.Ch)
+    ident = torch.arange(w.N, dtype=torch.int32, device="cuda")
+    bad = ident.clone()
+    bad[17] = w.N + 5
+    bad[300] = -3
+    y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, 0, w.block_q, query_order=ident)
+    y1 = torch.full_like(y0, 7.0)
+    avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, 0, w.block_q, Y=y1, query_order=bad)
+    keep = torch.ones(w.N, dtype=torch.bool)
+    keep[[17, 300]] = False
+    assert torch.equal(y1[:, :, keep.cuda()], y0[:, :, keep.cuda()])
+    assert (y1[:, :, 17] == 7.0).all() and (y1[:, :, 300] == 7.0).all()
+
+
 SAMPLE = {"c1": None, "c2": None, "c3": None, "c4": 12, "c5": 4}
 
 
