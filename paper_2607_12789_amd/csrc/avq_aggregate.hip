@@ -32,7 +32,7 @@ namespace avq {
 constexpr int kAggThreads = 1024;
 constexpr int kAggWaves = kAggThreads / kWave;
 constexpr int kFamLanes = 32;                          // lanes per family
-constexpr int kFamilies = kAggThreads / kFamLanes;     // families per workgroup
+constexpr int kFamilies = kAggThreads / kFamLanes;     // half waves = most families per workgroup
 constexpr int kCodesPerThread = 8;                     // codes scanned per thread per round
 constexpr int kRound = kAggThreads * kCodesPerThread;
 constexpr int kQueueCap = 8192;                        // queued keys per flush
@@ -72,7 +72,12 @@ struct Chunk<16> {
   typedef uint4 type;
 };
 
-template <typename T, int D, int CHM>
+// SPLIT half waves share one family (families per workgroup: kFamilies /
+// SPLIT): each sums a contiguous share of the family's keys in every flush,
+// and the shares are added in a fixed order at the end. More than one for
+// heads with many keys per parent, where one half wave's chain of loads
+// would set the time.
+template <typename T, int D, int CHM, int SPLIT>
 __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restrict__ V,
                                                                 const int32_t* __restrict__ code_idx,
                                                                 float* __restrict__ Vbar,
@@ -88,11 +93,12 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   const int Mtot = M0 * (1 + Ch);
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = blk / ranges;
-  const int p0 = (blk % ranges) * kFamilies;
-  const int nfam = min(kFamilies, M0 - p0);
+  constexpr int FAM = kFamilies / SPLIT;  // families of this workgroup
+  const int p0 = (blk % ranges) * FAM;
+  const int nfam = min(FAM, M0 - p0);
   const int rows = nfam * (1 + Ch);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const int sub = lane % kFamLanes, fam = tid / kFamLanes;
+  const int sub = lane % kFamLanes, fam = tid / kFamLanes / SPLIT, part = tid / kFamLanes % SPLIT;
   const int ch_shift = Ch > 0 ? 31 - __builtin_clz(Ch) : 0;  // Ch = 0: a flat codebook
 
   for (int r = tid; r < kMaxRows; r += kAggThreads) L.total[r] = 0;
@@ -187,7 +193,9 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         // the family's keys, bucketed by row, in kInFlight<CHM, T> batches; the
         // running row sum goes into the table when its row ends
         const int r_begin = fam * (1 + Ch);
-        const int kb = L.start[r_begin], ke = L.start[r_begin + 1 + Ch];
+        const int fb = L.start[r_begin], fe = L.start[r_begin + 1 + Ch];
+        // this half wave's share of the family's keys
+        const int kb = fb + (fe - fb) * part / SPLIT, ke = fb + (fe - fb) * (part + 1) / SPLIT;
         int rr = 0;                          // current row of the family
         int row_end = L.start[r_begin + 1];  // end of its bucket
         float cur[CPL];
@@ -249,8 +257,31 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   //    directly; the parents' octets (8 parents from 8 owners each) are put
   //    together through LDS (the queue area is free now).
   const PackedLayout PL = packed_layout(M0, Ch, D, (int)sizeof(T));
-  float* pmean = reinterpret_cast<float*>(L.qkey);  // [kFamilies][D]
-  int* pcell = reinterpret_cast<int*>(pmean + kFamilies * D);  // [kFamilies] cell sizes
+  if constexpr (SPLIT > 1) {
+    // add the shares of parts 1 .. SPLIT-1 into part 0's table, row by row,
+    // in part order, through the free key queue
+    float* share = reinterpret_cast<float*>(L.qkey);  // [SPLIT - 1][FAM][D]
+    static_assert((SPLIT - 1) * FAM * D * 4 <= sizeof(L.qkey), "shares fit the key queue");
+#pragma unroll
+    for (int r = 0; r <= CHM; ++r) {
+      if (r <= Ch) {  // uniform
+        if (fam < nfam && part > 0) {
+#pragma unroll
+          for (int i = 0; i < CPL; ++i) share[((part - 1) * FAM + fam) * D + sub * CPL + i] = acc[r][i];
+        }
+        __syncthreads();
+        if (fam < nfam && part == 0) {
+#pragma unroll
+          for (int q = 1; q < SPLIT; ++q)
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) acc[r][i] += share[((q - 1) * FAM + fam) * D + sub * CPL + i];
+        }
+        __syncthreads();
+      }
+    }
+  }
+  float* pmean = reinterpret_cast<float*>(L.qkey);  // [FAM][D]
+  int* pcell = reinterpret_cast<int*>(pmean + FAM * D);  // [FAM] cell sizes
   static_assert((kFamilies * D + kFamilies) * 4 <= sizeof(L.qkey), "parent means fit the key queue");
   // child octets leave through a 1 KB staging area per family (in the free
   // row and bucket queues), so that each store writes 16 consecutive bytes
@@ -265,7 +296,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   float* info = reinterpret_cast<float*>(pk + PL.info_off);
   constexpr float kNegInf = -__builtin_inff();
   constexpr float kLn2 = 0.6931471805599453f;
-  if (fam < nfam) {
+  if (fam < nfam && part == 0) {
     const int p = p0 + fam;
     const int* tot = &L.total[fam * (1 + Ch)];
     float par[CPL];
@@ -411,26 +442,59 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   }
 }
 
+template <typename T, int D, int CHM, int SPLIT>
+hipError_t launch_aggregate_dcs(int BH, int N, int M0, int Ch, const void* V,
+                                const int32_t* code_idx, float* Vbar, int32_t* counts,
+                                void* packed, hipStream_t stream) {
+  // one range of kFamilies / SPLIT parents per workgroup: ranges start at
+  // multiples of 8 parents, so each packed octet of parent means is written
+  // by one workgroup
+  constexpr int FAM = kFamilies / SPLIT;
+  static_assert(FAM % 8 == 0, "parent octets are assembled by one workgroup");
+  static_assert(kRound <= kQueueCap, "one round of codes fits the queue");
+  const int ranges = (M0 + FAM - 1) / FAM;
+  const int lds = (int)sizeof(AggLds);
+  constexpr int chm_i = CHM == 0 ? 0 : CHM == 8 ? 1 : 2;
+  constexpr int split_i = SPLIT == 1 ? 0 : SPLIT == 2 ? 1 : 2;
+  constexpr int slot =
+      64 + (((Elem<T>::kBf16 ? 0 : 1) * 2 + (D == 128 ? 1 : 0)) * 3 + chm_i) * 3 + split_i;
+  hipError_t e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM, SPLIT>, lds, slot);
+  if (e != hipSuccess) return e;
+  const long long grid = (long long)BH * ranges;
+  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((aggregate_kernel<T, D, CHM, SPLIT>), dim3((unsigned)grid), dim3(kAggThreads),
+                     lds, stream, static_cast<const T*>(V), code_idx, Vbar, counts,
+                     static_cast<unsigned char*>(packed), N, M0, Ch, ranges);
+  return hipGetLastError();
+}
+
+// Half waves per family. Each workgroup scans all codes of its head, so
+// splitting a family over more half waves (more, smaller workgroups) costs
+// scanning; it pays only when one half wave per family would walk a long
+// chain of value loads (at least 256 keys per parent) while fewer than half
+// the CUs have a workgroup (few heads, few parents). Then the fewest half
+// waves (2 or 4) that give half the CUs a workgroup.
 template <typename T, int D, int CHM>
 hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
                                const int32_t* code_idx, float* Vbar, int32_t* counts,
                                void* packed, hipStream_t stream) {
-  // one range of kFamilies parents per workgroup: ranges start at multiples
-  // of 8 parents, so each packed octet of parent means is written by one
-  // workgroup
-  static_assert(kFamilies % 8 == 0, "parent octets are assembled by one workgroup");
-  static_assert(kRound <= kQueueCap, "one round of codes fits the queue");
-  const int ranges = (M0 + kFamilies - 1) / kFamilies;
-  const int lds = (int)sizeof(AggLds);
-  constexpr int slot = (CHM == 0 ? 40 : CHM == 16 ? 1 : 0) + (Elem<T>::kBf16 ? 0 : 4) + (D == 128 ? 2 : 0);
-  hipError_t e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM>, lds, slot);
+  DeviceInfo dev;
+  hipError_t e = device_info(&dev);
   if (e != hipSuccess) return e;
-  const long long grid = (long long)BH * ranges;
-  if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((aggregate_kernel<T, D, CHM>), dim3((unsigned)grid), dim3(kAggThreads), lds,
-                     stream, static_cast<const T*>(V), code_idx, Vbar, counts,
-                     static_cast<unsigned char*>(packed), N, M0, Ch, ranges);
-  return hipGetLastError();
+  const long long half_cus = dev.cus > 1 ? dev.cus / 2 : 1;
+  auto grid = [&](int split) {
+    const int fam = kFamilies / split;
+    return (long long)BH * ((M0 + fam - 1) / fam);
+  };
+  const bool long_chains = (long long)N >= 256LL * M0;
+  if (!long_chains || grid(1) >= half_cus)
+    return launch_aggregate_dcs<T, D, CHM, 1>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
+                                              stream);
+  if (grid(2) >= half_cus)
+    return launch_aggregate_dcs<T, D, CHM, 2>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
+                                              stream);
+  return launch_aggregate_dcs<T, D, CHM, 4>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
+                                            stream);
 }
 
 template <typename T, int D>

@@ -35,7 +35,7 @@ hipError_t launch_codebook_update(int B, int H, int d, int M0, int Ch, float lam
 namespace avq {
 
 constexpr int kMaxDevices = 64;
-constexpr int kMaxSlots = 64;
+constexpr int kMaxSlots = 128;
 
 hipError_t device_info(DeviceInfo* out) {
   static DeviceInfo cache[kMaxDevices];

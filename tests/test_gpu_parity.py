@@ -77,6 +77,15 @@ EDGE = {
     "flat_fp32_d128": small(Ch=0, P=0, dtype="f32", d=128, block_q=64),
     "flat_m0_300_split": small(Ch=0, P=0, M0=300, B=1, H=1, N=2000),
     "flat_m0_512_d128": small(Ch=0, P=0, M0=512, d=128, N=1536, B=1, H=2, block_q=256),
+    # few workgroups and at least 256 keys per parent: two or four half waves
+    # share a family in the aggregation (on a 256-CU device: two for 64 heads
+    # of 32 parents, four for fewer)
+    "agg_split2": small(M0=32, Ch=4, P=4, N=8192, B=8, H=8, block_q=256),
+    "agg_split4": small(M0=8, Ch=8, P=3, N=4200, B=1, H=2, block_q=256),
+    "agg_split4_ragged_fp32_d128": small(dtype="f32", M0=20, Ch=2, P=4, N=11000, d=128, B=1,
+                                         H=1, block_q=256),
+    "agg_split4_flat": small(Ch=0, P=0, M0=16, N=9000, B=1, H=2, block_q=256),
+    "agg_split4_ch16": small(M0=10, Ch=16, P=3, N=2600, B=1, H=2),
 }
 
 
