@@ -455,7 +455,9 @@ struct ChildLds {
 };
 static_assert(kScanPerThread * kChildWaves <= 128, "one wave scans the slot offsets");
 
-template <typename T, int D>
+// NT: 16-row candidate tiles (the parent and its Ch children): 1 for Ch < 16,
+// 2 for Ch = 16.
+template <typename T, int D, int NT>
 __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     const T* __restrict__ K, const T* __restrict__ Cp, const T* __restrict__ Cc,
     const int32_t* __restrict__ parent_idx, int32_t* __restrict__ code_idx, int H, int N, int M0,
@@ -479,18 +481,18 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
   const int nfam = min(F, M0 - p0);
   const int32_t* pidx = parent_idx + (size_t)bh * N;
   const T* kh = K + (size_t)bh * N * D;
-  const int n_tiles = (Ch + 1 + 15) / 16;  // candidate tiles: parent + children
+  constexpr bool kPrefetch = kB && D == 64;
   int cur_fam = -1;  // the family whose rows the wave holds
-  Frag cf[2][KQ];
-  f32x4 cn[2];
+  Frag cf[NT][KQ];
+  f32x4 cn[NT];
 
   // candidate rows of a family (A operand): lane (g, c) holds row c of each
   // tile; row 0 = the parent, row 1 + j = child j (rows past Ch repeat the
   // last child and are ignored)
-  auto load_rows = [&](int p, Frag (&cf)[2][KQ]) {
+  auto load_rows = [&](int p, Frag (&cf)[NT][KQ]) {
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
-      if (t2 < n_tiles) {
+    for (int t2 = 0; t2 < NT; ++t2) {
+      {
         const int cand = 16 * t2 + c;
         const T* row = cand == 0 ? Cp + ((size_t)h * M0 + p) * D
                                  : Cc + (((size_t)h * M0 + p) * Ch + min(cand - 1, Ch - 1)) * D;
@@ -509,10 +511,10 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
   // then the rows are moved to the lanes that hold their products. The rows
   // are then scaled by -2 (exact), so that the product accumulated onto
   // ||c||^2 is the distance.
-  auto row_norms = [&](Frag (&cf)[2][KQ], f32x4 (&cn)[2]) {
+  auto row_norms = [&](Frag (&cf)[NT][KQ], f32x4 (&cn)[NT]) {
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
-      if (t2 < n_tiles) {
+    for (int t2 = 0; t2 < NT; ++t2) {
+      {
         float part = 0.f;
 #pragma unroll
         for (int kq = 0; kq < KQ; ++kq) part = frag_sq<T>(cf[t2][kq], part);
@@ -607,17 +609,33 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     // 3. each wave takes a contiguous run of groups (a group is 16 keys of
     //    one family), so that consecutive groups of a wave mostly share the
     //    family, whose rows stay in registers
+    //    The next group's keys load while the current group is compared.
     const int n_items = L.item_start[nfam];
     const int per_wave = (n_items + kChildWaves - 1) / kChildWaves;
-    const int it_end = min(n_items, (wave + 1) * per_wave);
+    const int it_begin = wave * per_wave, it_end = min(n_items, it_begin + per_wave);
     int f = 0;
-    for (int it = wave * per_wave; it < it_end; ++it) {
-      while (L.item_start[f + 1] <= it) ++f;  // wave-uniform
+    Frag kf[KQ];
+    int key = 0;
+    bool valid = false;
+    if (it_begin < it_end) {
+      while (L.item_start[f + 1] <= it_begin) ++f;  // wave-uniform
+      load_keys(f, it_begin, kf, key, valid);
+    }
+    for (int it = it_begin; it < it_end; ++it) {
       const int p = p0 + f;
-      Frag kf[KQ];
-      int key;
-      bool valid;
-      load_keys(f, it, kf, key, valid);
+      Frag kn[KQ];
+      int key_n = 0, fn = f;
+      bool valid_n = false;
+      if (it + 1 < it_end) {
+        while (L.item_start[fn + 1] <= it + 1) ++fn;  // wave-uniform
+        // a second set of key registers fits the 128 of a 1024-thread
+        // workgroup for bf16 at d = 64 only; otherwise the keys load just in
+        // time
+        if constexpr (kPrefetch) load_keys(fn, it + 1, kn, key_n, valid_n);
+      }
+      if constexpr (!kPrefetch) {
+        if (it > it_begin) load_keys(f, it, kf, key, valid);
+      }
       if (p != cur_fam) {
         load_rows(p, cf);
         row_norms(cf, cn);
@@ -627,8 +645,8 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
       float dpar = 0.f, dch = __builtin_inff();
       int cbest = 0;
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        if (t2 < n_tiles) {
+      for (int t2 = 0; t2 < NT; ++t2) {
+        {
           f32x4 acc = cn[t2];
 #pragma unroll
           for (int kq = 0; kq < KQ; ++kq) {
@@ -662,6 +680,11 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
       }
       if (g == 0 && valid)
         code_idx[(size_t)bh * N + key] = (dch < dpar) ? (M0 + p * Ch + cbest) : p;
+#pragma unroll
+      for (int kq = 0; kq < KQ; ++kq) kf[kq] = kn[kq];
+      key = key_n;
+      valid = valid_n;
+      f = fn;
     }
     __syncthreads();  // the queue is reused by the next round
   }
@@ -721,14 +744,18 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   splits = (N + chunk - 1) / chunk;
   grid = base_grid * splits;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  constexpr int slot_b = 28 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
-  e = ensure_dynamic_lds((const void*)child_assign_kernel<T, D>, (int)sizeof(ChildLds), slot_b);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((child_assign_kernel<T, D>), dim3((unsigned)grid), dim3(kChildThreads),
-                     sizeof(ChildLds), stream, static_cast<const T*>(K),
-                     static_cast<const T*>(Cp), static_cast<const T*>(Cc), parent_idx, code_idx,
-                     H, N, M0, Ch, F, ranges, splits, chunk);
-  return hipGetLastError();
+  auto launch_child = [&](auto kernel, int slot) {
+    hipError_t err = ensure_dynamic_lds((const void*)kernel, (int)sizeof(ChildLds), slot);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kChildThreads), sizeof(ChildLds),
+                       stream, static_cast<const T*>(K), static_cast<const T*>(Cp),
+                       static_cast<const T*>(Cc), parent_idx, code_idx, H, N, M0, Ch, F, ranges,
+                       splits, chunk);
+    return hipGetLastError();
+  };
+  constexpr int slot_b = 100 + ((Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0)) * 2;
+  if (Ch + 1 > 16) return launch_child(child_assign_kernel<T, D, 2>, slot_b + 1);
+  return launch_child(child_assign_kernel<T, D, 1>, slot_b);
 }
 
 template hipError_t launch_assign<bf16, 64>(int, int, int, int, int, const void*, const void*,
