@@ -746,6 +746,10 @@ void attention_kernel(AttnArgs args) {
         child_weights(B, 1, S1);
         accumulate_pair(B, 1, S1);
       }
+      if (Cfg::NBUF == 1 && k + 1 < n_cchunks) {  // one buffer: refill it when all are done
+        __syncthreads();
+        issue_child(k + 1, buffer(0));
+      }
     }
   }
 

@@ -112,6 +112,7 @@ CASES = {
     "bf16_ch1_b1": (small(Ch=1, B=1, M0=70), 0.3),
     "f32_lambda_one": (small(dtype="f32", Ch=2, M0=50), 1.0),
     "bf16_m0_512_d128": (small(M0=512, Ch=8, d=128, N=4096, B=1, H=2), 0.95),
+    "f32_ch16_d64": (small(dtype="f32", Ch=16, M0=20, N=1500), 0.75),
 }
 
 

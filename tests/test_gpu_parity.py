@@ -70,6 +70,10 @@ EDGE = {
     "m0_24_split": small(M0=24, Ch=2, P=5, B=1, H=1, N=700),
     "m0_44_split": small(M0=44, Ch=4, P=5, B=1, H=1, N=700),
     "fp32_ch16_d64": small(dtype="f32", M0=70, Ch=16, P=9, N=600),
+    # fp32 at d = 128 stages one chunk at a time: several parent, importance
+    # and child chunks
+    "fp32_d128_multichunk": small(dtype="f32", d=128, M0=130, Ch=8, P=10, N=700, block_q=64),
+    "fp32_d128_ch16_multichunk": small(dtype="f32", d=128, M0=70, Ch=16, P=9, N=500),
     # flat codebook (Ch = 0): VQ attention over the parents alone
     "flat": small(Ch=0, P=0),
     "flat_n_one": small(Ch=0, P=0, N=1, B=1, H=1),
@@ -156,6 +160,8 @@ TILED = {
     "tiled_p0_importance": small(M0=200, P=0, N=700),
     "tiled_bq200": small(M0=130, Ch=8, P=11, block_q=200, N=1300),
     "tiled_m0_512_bq256": small(M0=512, Ch=8, P=64, block_q=256, N=1536, d=128, B=1, H=2),
+    "tiled_fp32_d128_ragged": small(dtype="f32", d=128, M0=130, Ch=8, P=10, N=700,
+                                    block_q=64),
 }
 
 
@@ -208,6 +214,8 @@ ORDERED = {
                                   q_scale=8.0), 28, 28, "gilbert", True),
     "random_40x25_fp32": (small(dtype="f32", M0=96, Ch=4, P=12, N=1000, B=1, H=3, block_q=100,
                                 q_scale=8.0), 40, 25, "random", False),
+    "gilbert_32x32_flat": (small(Ch=0, P=0, M0=64, N=1024, B=1, H=2, block_q=64, q_scale=8.0),
+                           32, 32, "gilbert", False),
 }
 
 
