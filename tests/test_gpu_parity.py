@@ -74,6 +74,8 @@ EDGE = {
     # and child chunks
     "fp32_d128_multichunk": small(dtype="f32", d=128, M0=130, Ch=8, P=10, N=700, block_q=64),
     "fp32_d128_ch16_multichunk": small(dtype="f32", d=128, M0=70, Ch=16, P=9, N=500),
+    "fp32_d128_bq256_multichunk": small(dtype="f32", d=128, M0=200, Ch=4, P=20, N=600,
+                                        block_q=256),
     # flat codebook (Ch = 0): VQ attention over the parents alone
     "flat": small(Ch=0, P=0),
     "flat_n_one": small(Ch=0, P=0, N=1, B=1, H=1),
@@ -162,6 +164,7 @@ TILED = {
     "tiled_m0_512_bq256": small(M0=512, Ch=8, P=64, block_q=256, N=1536, d=128, B=1, H=2),
     "tiled_fp32_d128_ragged": small(dtype="f32", d=128, M0=130, Ch=8, P=10, N=700,
                                     block_q=64),
+    "tiled_fp32_d128_bq256": small(dtype="f32", d=128, M0=200, Ch=4, P=20, N=600, block_q=256),
 }
 
 
@@ -282,3 +285,32 @@ def test_workload(name):
     x = inputs.generate(w)
     res = parity.compare(x, w, tiles_per_head=SAMPLE[name])
     report(res)
+
+
+@pytest.mark.parametrize("Ch", [0, 4])
+def test_aggregate_ignores_out_of_range_codes(Ch):
+    """Codes outside [0, Mtot) (here -1, -7, Mtot, 2^30) take no part: counts
+    and sums equal those of the valid codes alone (numpy add.at reference)."""
+    from paper_2607_12789_amd import avq
+    from tests import references as ref
+    w = small(Ch=Ch, P=0, M0=24, N=900, B=1, H=2, dtype="f32")
+    x = inputs.generate(w)
+    rng = np.random.default_rng(3)
+    code = rng.integers(0, w.Mtot, size=(w.B, w.H, w.N)).astype(np.int32)
+    bad = rng.random((w.B, w.H, w.N)) < 0.1
+    code[bad] = rng.choice(np.array([-1, -7, w.Mtot, 1 << 30], np.int32), size=int(bad.sum()))
+    V = x["V"].cuda()
+    _, counts, Vbar = avq.aggregate(V, torch.from_numpy(code).cuda(), w.M0, w.Ch, sums=True)
+    torch.cuda.synchronize()
+    good = ~bad
+    par = np.where(code < w.M0, code, (code - w.M0) // max(w.Ch, 1)).astype(np.int64)
+    Vn = x["V"].double().numpy()
+    exp_V, exp_n = np.zeros((w.B, w.H, w.Mtot, w.d)), np.zeros((w.B, w.H, w.Mtot), np.int64)
+    for b in range(w.B):
+        for h in range(w.H):
+            g = good[b, h]
+            rv, rn = ref.aggregates(Vn[b:b + 1, h:h + 1][:, :, g], par[b:b + 1, h:h + 1][:, :, g],
+                                    code[b:b + 1, h:h + 1][:, :, g].astype(np.int64), w.M0, w.Ch)
+            exp_V[b, h], exp_n[b, h] = rv[0, 0], rn[0, 0]
+    np.testing.assert_array_equal(counts.cpu().numpy(), exp_n)
+    np.testing.assert_allclose(Vbar.cpu().numpy(), exp_V, rtol=1e-5, atol=1e-4)
