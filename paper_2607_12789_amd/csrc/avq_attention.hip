@@ -371,41 +371,36 @@ void attention_kernel(AttnArgs args) {
     thr[s] = (kMaxFloor + kLazy) * kLn2;
     zp[s] = 0.f;
   }
-  // Raises the running max if some lane's logit in the tile pair S passed the
-  // threshold, rescaling the accumulators; returns whether it moved (the same
-  // for the whole wave) and the factors applied, sc.
-  auto check_pair = [&](const f32x4 (&S)[2][QS], float (&sc)[QS]) -> bool {
+  // Raises the running max if some lane's logit in the chunk (both tile pairs)
+  // passed the threshold, rescaling the accumulators (rare: the max lags by
+  // up to kLazy). One check per chunk keeps the weights and value products of
+  // the chunk in one basic block, where the compiler interleaves the second
+  // pair's exponentials with the first pair's MFMAs.
+  auto check_chunk = [&](const f32x4 (&S0)[2][QS], const f32x4 (&S1)[2][QS]) {
     float mx[QS];
     bool over = false;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
-      mx[s] = S[0][s][0];
+      mx[s] = S0[0][s][0];
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mx[s] = fmaxf(mx[s], S[h2][s][r]);
+        for (int r = 0; r < 4; ++r) mx[s] = fmaxf(mx[s], fmaxf(S0[h2][s][r], S1[h2][s][r]));
       over |= mx[s] > thr[s];
     }
-    if (__ballot(over) == 0) return false;
+    if (__ballot(over) == 0) return;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
       mx[s] = fmaxf(mx[s], shfl_xor(mx[s], 16));
       mx[s] = fmaxf(mx[s], shfl_xor(mx[s], 32));
       const float mnew = mx[s] > thr[s] ? mx[s] * kLog2e : m[s];
-      sc[s] = exp2_hw(m[s] - mnew);
-      zp[s] *= sc[s];
+      const float scs = exp2_hw(m[s] - mnew);
+      zp[s] *= scs;
 #pragma unroll
-      for (int dt = 0; dt < XT; ++dt) X[dt][s] *= sc[s];
+      for (int dt = 0; dt < XT; ++dt) X[dt][s] *= scs;
       m[s] = mnew;
       thr[s] = (mnew + kLazy) * kLn2;
     }
-    return true;
-  };
-  auto rescale_pair = [&](f32x4 (&W)[2][QS], const float (&sc)[QS]) {
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-      for (int s = 0; s < QS; ++s) W[h2][s] *= sc[s];
   };
   // parent weights n exp(S - m) = exp2((S + ln n) log2 e - m), in place
   auto parent_weights = [&](f32x4 (&S)[2][QS]) {
@@ -458,8 +453,8 @@ void attention_kernel(AttnArgs args) {
     }
   };
   // logits of the chunk's two tile pairs; parents start from ln n
-  // (bf16: all 16 A fragments of the chunk are read before the first product,
-  // so the LDS latency is paid once per chunk, not once per k-step)
+  // (bf16: the A fragments of tile tt + 1 are read from LDS while the
+  // products of tile tt run; scheduling barriers keep that order)
   auto chunk_logits = [&](const unsigned char* B, bool with_ln, f32x4 (&S0)[2][QS],
                           f32x4 (&S1)[2][QS]) {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
@@ -468,24 +463,28 @@ void attention_kernel(AttnArgs args) {
     for (int tt = 0; tt < TPC; ++tt) init[tt] = with_ln ? info4(B, tt, 1) : zero;
     if constexpr (kB) {
       const T* lc = reinterpret_cast<const T*>(B + Cfg::OFF_C);
-      bf16x8 a[TPC][KQ];
-#pragma unroll
-      for (int tt = 0; tt < TPC; ++tt) {
+      bf16x8 a[2][KQ];
+      auto load_tile = [&](int tt, bf16x8 (&dst)[KQ]) {
         const int r = 32 * (tt / 2) + 8 * (c / 4) + 4 * (tt % 2) + (c % 4);
         const int sw = row_swizzle<U>(r);
 #pragma unroll
         for (int kq = 0; kq < KQ; ++kq)
-          a[tt][kq] = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
-      }
+          dst[kq] = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
+      };
+      load_tile(0, a[0]);
 #pragma unroll
-      for (int tt = 0; tt < TPC; ++tt)
+      for (int tt = 0; tt < TPC; ++tt) {
+        if (tt + 1 < TPC) load_tile(tt + 1, a[(tt + 1) % 2]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kq = 0; kq < KQ; ++kq)
 #pragma unroll
           for (int s = 0; s < QS; ++s) {
             f32x4& o = tt < 2 ? S0[tt][s] : S1[tt - 2][s];
-            o = mfma_bf16(a[tt][kq], qf[s][kq], kq == 0 ? init[tt] : o);
+            o = mfma_bf16(a[tt % 2][kq], qf[s][kq], kq == 0 ? init[tt] : o);
           }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     } else {
       logits(B, 0, S0[0], init[0]);
       logits(B, 1, S0[1], init[1]);
@@ -586,9 +585,9 @@ void attention_kernel(AttnArgs args) {
   };
 
   // ---- phase 1: parent sweep -------------------------------------------------
-  // Per chunk: the logits of both tile pairs are issued first; the second
-  // pair's MFMAs run while the first pair's weights are computed, and the
-  // first pair's value MFMAs while the second pair's weights are computed.
+  // Per chunk: the logits of both tile pairs are issued first, then one max
+  // check; the first pair's value MFMAs run while the second pair's weights
+  // are computed.
   issue_parent(0, buffer(0), true);
   for (int k = 0; k < n_pchunks; ++k) {
     wait_chunk();
@@ -598,10 +597,8 @@ void attention_kernel(AttnArgs args) {
     if (has_rows) {
       f32x4 S0[2][QS], S1[2][QS];
       chunk_logits(B, true, S0, S1);
-      float sc[QS];
-      check_pair(S0, sc);
+      check_chunk(S0, S1);
       parent_weights(S0);
-      if (check_pair(S1, sc)) rescale_pair(S0, sc);
       accumulate_pair(B, 0, S0);
       parent_weights(S1);
       accumulate_pair(B, 1, S1);
@@ -738,10 +735,8 @@ void attention_kernel(AttnArgs args) {
       if (has_rows) {
         f32x4 S0[2][QS], S1[2][QS];
         chunk_logits(B, false, S0, S1);
-        float sc[QS];
-        check_pair(S0, sc);
+        check_chunk(S0, S1);
         child_weights(B, 0, S0);
-        if (check_pair(S1, sc)) rescale_pair(S0, sc);
         accumulate_pair(B, 0, S0);
         child_weights(B, 1, S1);
         accumulate_pair(B, 1, S1);
