@@ -420,24 +420,23 @@ void attention_kernel(AttnArgs args) {
   // even tile (the rest is padding); Ch = 4: the 4 rows of each tile (one
   // parent per tile); Ch = 8: the whole octet; Ch = 16: and the partner lane
   // group's octet.
+  // 0/1 weights of the recovered-logit cases (exact products and sums)
+  const float w2 = Ch == 2 ? 1.f : 0.f, w4 = Ch == 4 ? 1.f : 0.f, w8 = Ch == 8 ? 1.f : 0.f,
+              w16 = Ch == 16 ? 1.f : 0.f;
   auto child_weights = [&](const unsigned char* B, int b, f32x4 (&S)[2][QS]) {
     float er[2][QS];
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
+      // every case computed and one kept by 0/1 weights: no branch splits
+      // the chunk's weights from its value products
       const f32x4 v0 = S[0][s], v1 = S[1][s];
-      float s0, s1;
-      if (Ch == 2) {
-        s0 = v0[0] + v0[1];
-        s1 = s0;
-      } else {
-        s0 = (v0[0] + v0[1]) + (v0[2] + v0[3]);
-        s1 = (v1[0] + v1[1]) + (v1[2] + v1[3]);
-        if (Ch >= 8) {
-          s0 += s1;
-          if (Ch == 16) s0 += shfl_xor(s0, 16);
-          s1 = s0;
-        }
-      }
+      const float a01 = v0[0] + v0[1];
+      const float a = a01 + (v0[2] + v0[3]);
+      const float bs = (v1[0] + v1[1]) + (v1[2] + v1[3]);
+      const float ab = a + bs;
+      const float ab16 = ab + shfl_xor(ab, 16);
+      const float s0 = fmaf(w2, a01, fmaf(w4, a, fmaf(w8, ab, w16 * ab16)));
+      const float s1 = fmaf(w2, a01, fmaf(w4, bs, fmaf(w8, ab, w16 * ab16)));
       const float scale = kLog2e / (float)Ch;
       er[0][s] = exp2_hw(fminf(fmaf(s0, scale, -m[s]), 64.f));
       er[1][s] = exp2_hw(fminf(fmaf(s1, scale, -m[s]), 64.f));
