@@ -36,20 +36,24 @@
 // XOR-swizzled by 16-byte unit (the 16 rows of a logit tile hit different
 // banks), packed mean octets and their count info as they lie in HBM, all by
 // direct global->LDS loads (no registers, no VALU), double buffered: the next
-// chunk is in flight while the current one is computed. Phases per tile:
+// chunk is in flight while the current one is computed (fp32 at d = 128: one
+// buffer, refilled after each chunk). Phases per tile:
 //   1. parent sweep: logits, running max, weights, fp32 parent denominator,
 //      Xbar += Vmean^T W;
 //   2. importance (Eq. (importance)) with the final max and denominator: a
 //      second sweep recomputes the parent logits (or reuses them when all
 //      parents fit one chunk) and takes exp(t - m - ln Z) directly; sums over
 //      the tile's queries by a reduce-scatter butterfly over lanes, then a
-//      fixed order over waves;
+//      fixed order over waves. TILED instead takes the importance of App. B
+//      inside phase 1, chunk by chunk, and skips the second sweep;
 //   3. top-P in one wave: a threshold on the importance bits, built bit by
 //      bit from the top, finds the P-th largest value; ties at it go to the
 //      lowest indices; the selected parents are listed in index order;
 //   4. child sweep over the child octets of the selected parents: logits,
 //      recovered parent logit, correcting weights, Xbar += Vmean^T dW;
 //   5. Y = Xbar / Z.
+// With a query order, tile position i takes token order[i]: Q rows are read
+// from, and Y rows written to, those tokens.
 #include "avq_common.hpp"
 #include "avq_packed.hpp"
 
