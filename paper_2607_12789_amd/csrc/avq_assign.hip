@@ -358,12 +358,18 @@ __global__ __launch_bounds__(256) void parent_stream_kernel(const T* __restrict_
       for (int kq = 0; kq < KQ; ++kq) kf[s][kq] = kn[s][kq];
     if (st + 1 < s_end) load_keys(st + 1, kn);
 
+    // per key subtile: the largest value so far, its 16-row tile, and that
+    // tile's 4 values of the lane (the row within the tile is found once at
+    // the end): 9 VALU per tile and subtile instead of 12 for a running
+    // (value, row) pair
     float best[KS];
-    int bidx[KS];
+    int btile[KS];
+    f32x4 bv[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       best[s] = -__builtin_inff();
-      bidx[s] = 0;
+      btile[s] = 0;
+      if constexpr (kB) bv[s] = f32x4{best[s], best[s], best[s], best[s]};
     }
     // two 16-row tiles per step: all their row fragments are read before
     // the products, and the second tile's products overlap the first
@@ -400,17 +406,38 @@ __global__ __launch_bounds__(256) void parent_stream_kernel(const T* __restrict_
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = 16 * (tt + h2) + 4 * g + q;
+        for (int s = 0; s < KS; ++s) {
+          const f32x4 v = acc[h2][s];
+          if constexpr (kB) {
+            const float tmax = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+            const bool gt = tmax > best[s];  // strict: the earlier tile keeps a tie
+            best[s] = gt ? tmax : best[s];
+            btile[s] = gt ? tt + h2 : btile[s];
 #pragma unroll
-          for (int s = 0; s < KS; ++s) {
-            const float v = acc[h2][s][q];
-            if (v > best[s]) {  // strict: the first (lowest) row keeps a tie
-              best[s] = v;
-              bidx[s] = row;
+            for (int q = 0; q < 4; ++q) bv[s][q] = gt ? v[q] : bv[s][q];
+          } else {
+            // fp32: no registers to spare for the tile's values; a running
+            // (value, row) pair, the first (lowest) row keeping a tie
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const bool gt = v[q] > best[s];
+              best[s] = gt ? v[q] : best[s];
+              btile[s] = gt ? 4 * (tt + h2) + q : btile[s];
             }
           }
         }
+    }
+    // the row: bf16, the first of the best tile's 4 rows that holds the best
+    // value; fp32, recorded as 4 tile + q
+    int bidx[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if constexpr (kB) {
+        const int q = bv[s][0] == best[s] ? 0 : bv[s][1] == best[s] ? 1 : bv[s][2] == best[s] ? 2 : 3;
+        bidx[s] = 16 * btile[s] + 4 * g + q;
+      } else {
+        bidx[s] = 16 * (btile[s] / 4) + 4 * g + btile[s] % 4;
+      }
     }
     // merge the four lane groups: largest value, lowest index on ties
     const int key0 = (st % steps_per_bh) * Cfg::kKeysPerStep + wave * KS * 16;
