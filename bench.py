@@ -48,9 +48,12 @@ TRAFFIC_SUMMARY = ROOT / "profiles" / "attention_fwd_c4_traffic.md"
 
 
 def kernel_hash() -> str:
+    """The attention kernel's sources and the compiler flags they are built with."""
+    from paper_2607_12789_amd.build import COMPILE_FLAGS
     h = hashlib.sha256()
     for name in ("avq_attention.hip", "avq_common.hpp", "avq_packed.hpp"):
         h.update((KERNEL_SRC.parent / name).read_bytes())
+    h.update(" ".join(COMPILE_FLAGS).encode())
     return h.hexdigest()[:16]
 
 

@@ -42,7 +42,9 @@
  *   - Arguments are validated on the host before anything is launched; a
  *     non-OK status means nothing was enqueued (AVQ_ERR_DEVICE: a launch was
  *     rejected). avq_last_error() then returns a message for the calling
- *     thread. Non-finite inputs are not checked; they propagate.
+ *     thread. Inputs are not checked for NaN or infinity; the kernels are
+ *     compiled without NaN semantics, so outputs for such inputs are
+ *     unspecified (they need not be NaN).
  *   - Supported: d in {64, 128}; Ch in {0, 1, 2, 4, 8, 16}; 1 <= M0 <= 512;
  *     1 <= N <= 2^24, B >= 1, H >= 1 and B*H*N*d < 2^31. Other shapes return
  *     AVQ_ERR_UNSUPPORTED.

@@ -3,7 +3,10 @@
     python -m paper_2607_12789_amd.build
 
 Every HIP source is compiled with hipcc for gfx950 only, with the packed-fp32
-instructions disabled.
+instructions disabled. Device code is compiled without NaN semantics
+(``-fno-honor-nans``): the maxima and minima over MFMA results then need no
+sNaN-quieting canonicalisation of each operand (one extra VALU instruction per
+value in the softmax max and the argmin); host code keeps IEEE semantics.
 """
 from __future__ import annotations
 
@@ -26,6 +29,7 @@ COMPILE_FLAGS = [
     "-std=c++17",
     "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Xarch_device", "-fno-honor-nans",
     "-Wall",
 ]
 
