@@ -7,6 +7,10 @@ instructions disabled. Device code is compiled without NaN semantics
 (``-fno-honor-nans``): the maxima and minima over MFMA results then need no
 sNaN-quieting canonicalisation of each operand (one extra VALU instruction per
 value in the softmax max and the argmin); host code keeps IEEE semantics.
+MFMA results are kept in architectural VGPRs (``-amdgpu-mfma-vgpr-form``): the
+assignment kernels compare every product with VALU instructions, which cannot
+read accumulation registers, so products left there cost one extra move per
+value.
 """
 from __future__ import annotations
 
@@ -30,6 +34,7 @@ COMPILE_FLAGS = [
     "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Xarch_device", "-fno-honor-nans",
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wall",
 ]
 
