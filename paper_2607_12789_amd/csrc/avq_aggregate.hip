@@ -72,6 +72,19 @@ struct Chunk<16> {
   typedef uint4 type;
 };
 
+// An empty asm statement on each 32-bit word of a loaded value: the value is
+// first used here, as it was loaded, so the compiler can neither move work on
+// it closer to the load nor wait for the load any earlier.
+template <typename R>
+__device__ __forceinline__ void pin_words(R& r) {
+  constexpr int W = sizeof(R) / 4;
+  uint32_t w[W];
+  __builtin_memcpy(w, &r, sizeof(R));
+#pragma unroll
+  for (int j = 0; j < W; ++j) asm volatile("" : "+v"(w[j]));
+  __builtin_memcpy(&r, w, sizeof(R));
+}
+
 // SPLIT half waves share one family (families per workgroup: kFamilies /
 // SPLIT): each sums a contiguous share of the family's keys in every flush,
 // and the shares are added in a fixed order at the end. More than one for
@@ -212,14 +225,22 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
 #pragma unroll
           for (int i = 0; i < CPL; ++i) cur[i] = 0.f;
         };
+        // a ring of kIF rows in flight: slot u holds key k0 + u; once it is
+        // summed it is refilled with key k0 + kIF + u, so kIF - 1 loads stay
+        // in flight while the rows are added. Keys past the share repeat its
+        // last key: the refills are unconditional, so the compiler's count
+        // of outstanding loads is exact and every wait leaves kIF - 1 of them
+        // in flight (a conditional refill makes it wait for more).
         constexpr int kIF = kInFlight<CHM, T>;
-        for (int k0 = kb; k0 < ke; k0 += kIF) {
-          Raw raw[kIF];
+        auto row_of = [&](int k) {
+          return *reinterpret_cast<const Raw*>(vhead + (size_t)L.skey[min(k, ke - 1)] * D + sub * CPL);
+        };
+        Raw raw[kIF];
+        if (kb < ke) {
 #pragma unroll
-          for (int u = 0; u < kIF; ++u) {
-            const int k = min(k0 + u, ke - 1);
-            raw[u] = *reinterpret_cast<const Raw*>(vhead + (size_t)L.skey[k] * D + sub * CPL);
-          }
+          for (int u = 0; u < kIF; ++u) raw[u] = row_of(kb + u);
+        }
+        for (int k0 = kb; k0 < ke; k0 += kIF) {
 #pragma unroll
           for (int u = 0; u < kIF; ++u) {
             if (k0 + u < ke) {
@@ -228,10 +249,15 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
                 ++rr;
                 row_end = L.start[r_begin + rr + 1];
               }
+              // the row is unpacked here, not where it was loaded: otherwise
+              // the compiler moves the unpacking next to the loads and waits
+              // for all of them there
+              pin_words(raw[u]);
               const T* x = reinterpret_cast<const T*>(&raw[u]);
 #pragma unroll
               for (int i = 0; i < CPL; ++i) cur[i] += to_f32(x[i]);
             }
+            raw[u] = row_of(k0 + kIF + u);
           }
         }
         if (kb < ke) close_row();
