@@ -248,8 +248,11 @@ __global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict_
 template <typename T, int D>
 struct StreamCfg {
   static constexpr bool kB = Elem<T>::kBf16;
-  static constexpr int kWaves = 4;
-  static constexpr int KS = 4;                    // key subtiles (of 16) per wave
+  // bf16: 8 waves of 32 keys (under 128 VGPRs, four waves per SIMD with two
+  // workgroups per CU); fp32: 4 waves of 64 keys (its fragments need the
+  // registers of two waves per SIMD)
+  static constexpr int kWaves = kB ? 8 : 4;
+  static constexpr int KS = kB ? 2 : 4;           // key subtiles (of 16) per wave
   static constexpr int kKeysPerStep = kWaves * KS * 16;
   static constexpr int KQ = kB ? D / 32 : D / 4;
   static constexpr int ESZ = sizeof(T);
@@ -263,7 +266,7 @@ struct StreamCfg {
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__(256) void parent_stream_kernel(const T* __restrict__ K,
+__global__ __launch_bounds__((StreamCfg<T, D>::kWaves * 64)) void parent_stream_kernel(const T* __restrict__ K,
                                                             const T* __restrict__ Cp,
                                                             int32_t* __restrict__ parent_idx,
                                                             int32_t* __restrict__ code_idx, int H,
@@ -739,7 +742,8 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
     constexpr int slot_s = 32 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
     e = ensure_dynamic_lds((const void*)parent_stream_kernel<T, D>, SCfg::LDS_HALF, slot_s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid), dim3(256), lds, stream,
+    hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid), dim3(SCfg::kWaves * kWave),
+                       lds, stream,
                        static_cast<const T*>(K), static_cast<const T*>(Cp), parent_idx,
                        Ch == 0 ? code_idx : nullptr, H, N, M0, per_bh, (int)n_steps);
   } else {
