@@ -511,9 +511,11 @@ void attention_kernel(AttnArgs args) {
     for (int tt = 0; tt < TPC; ++tt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float acc = 0.f;
+        // the first product starts the sum (a sum from 0.0 keeps an add of
+        // zero per value: x + 0 is not x for x = -0)
+        float acc = (tt < 2 ? W0[tt][0][r] : W1[tt - 2][0][r]) * mul[0];
 #pragma unroll
-        for (int s = 0; s < QS; ++s)
+        for (int s = 1; s < QS; ++s)
           acc = fmaf(tt < 2 ? W0[tt][s][r] : W1[tt - 2][s][r], mul[s], acc);
         u[4 * tt + r] = acc;
       }
