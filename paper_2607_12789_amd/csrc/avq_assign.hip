@@ -763,16 +763,14 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   if (Ch == 0) return hipSuccess;  // flat codebook: the parent is the code
 
   // child compare: F parents per workgroup, and the keys split into chunks
-  // of whole scan rounds until the grid fills the device twice over (the
-  // keys are independent: a split only shortens each workgroup's scan)
+  // of one scan round each (the keys are independent: a workgroup scans only
+  // its chunk, so the splits add no scan work; they shorten each wave's
+  // chain of groups and let the grid fill the device in whole rounds)
   const int F = kMaxFam;
   const int ranges = (M0 + F - 1) / F;
-  const long long want = 2LL * (dev.cus > 0 ? dev.cus : 1);
-  const int max_splits = (N + kChildRound - 1) / kChildRound;
   const long long base_grid = (long long)BH * ranges;
-  int splits = (int)std::min<long long>(max_splits, std::max<long long>(1, (want + base_grid - 1) / base_grid));
-  const int chunk = ((N + splits - 1) / splits + kChildRound - 1) / kChildRound * kChildRound;
-  splits = (N + chunk - 1) / chunk;
+  const int chunk = kChildRound;
+  const int splits = (N + chunk - 1) / chunk;
   grid = base_grid * splits;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
   auto launch_child = [&](auto kernel, int slot) {
