@@ -92,6 +92,10 @@ EDGE = {
                                          H=1, block_q=256),
     "agg_split4_flat": small(Ch=0, P=0, M0=16, N=9000, B=1, H=2, block_q=256),
     "agg_split4_ch16": small(M0=10, Ch=16, P=3, N=2600, B=1, H=2),
+    # every key of a head in one workgroup's range, more than its key queue
+    # holds: the queue is bucketed and summed in the middle of the scan
+    "agg_queue_overflow": small(M0=8, Ch=8, P=3, N=20000, B=1, H=2, block_q=256),
+    "agg_queue_overflow_flat": small(Ch=0, P=0, M0=4, N=30000, B=1, H=1, block_q=256),
 }
 
 
