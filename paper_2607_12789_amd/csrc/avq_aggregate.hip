@@ -14,10 +14,12 @@
 //   2. when the queue is full or the codes are exhausted, buckets the queued
 //      keys by their row (stay row of the parent, or one of its children) with
 //      integer LDS atomics: histogram, prefix sum, scatter;
-//   3. lets each half wave walk its family's keys in bucket order, 8 value
-//      rows (4 for Ch = 16) in flight at a time whatever rows they belong to (lane l holds
-//      columns l*CPL .. l*CPL+CPL-1), summing in fp32 into a running row sum
-//      that is added to the family's register table when the row ends.
+//   3. lets each half wave walk its family's keys in bucket order through a
+//      ring of 8 value rows (4 for Ch = 16) in flight, whatever rows they
+//      belong to, each slot refilled as soon as its row is added (lane l
+//      holds columns l*CPL .. l*CPL+CPL-1), summing in fp32 into a running
+//      row sum that is added to the family's register table when the row
+//      ends.
 // At the end the parent row is the stay row plus the children (the whole
 // cell), every row is written once, and counts come from the histograms.
 // Optionally the packed aggregates are also written (avq_packed.hpp): the

@@ -266,12 +266,9 @@ struct StreamCfg {
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__((StreamCfg<T, D>::kWaves * 64)) void parent_stream_kernel(const T* __restrict__ K,
-                                                            const T* __restrict__ Cp,
-                                                            int32_t* __restrict__ parent_idx,
-                                                            int32_t* __restrict__ code_idx, int H,
-                                                            int N, int M0, int steps_per_bh,
-                                                            int n_steps) {
+__global__ __launch_bounds__((StreamCfg<T, D>::kWaves * 64)) void parent_stream_kernel(
+    const T* __restrict__ K, const T* __restrict__ Cp, int32_t* __restrict__ parent_idx,
+    int32_t* __restrict__ code_idx, int H, int N, int M0, int steps_per_bh, int n_steps) {
   using Cfg = StreamCfg<T, D>;
   constexpr bool kB = Cfg::kB;
   constexpr int KS = Cfg::KS, KQ = Cfg::KQ, U = Cfg::U, EPU = Cfg::EPU;
@@ -742,8 +739,8 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
     constexpr int slot_s = 32 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
     e = ensure_dynamic_lds((const void*)parent_stream_kernel<T, D>, SCfg::LDS_HALF, slot_s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid), dim3(SCfg::kWaves * kWave),
-                       lds, stream,
+    hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid),
+                       dim3(SCfg::kWaves * kWave), lds, stream,
                        static_cast<const T*>(K), static_cast<const T*>(Cp), parent_idx,
                        Ch == 0 ? code_idx : nullptr, H, N, M0, per_bh, (int)n_steps);
   } else {
