@@ -12,9 +12,10 @@
 // kernel) and the MFMA accumulator starts at ||c||^2, so the accumulator holds
 // the distance itself.
 //
-// parent_assign_kernel: one workgroup = 4 waves = 256 keys of one
-// (batch, head), 64 keys per wave (4 subtiles of 16). The norms of the head's
-// parents are summed once per workgroup (one row per thread, in order); the
+// parent_assign_kernel: one workgroup = 256 keys of one (batch, head): bf16
+// 8 waves of 32 keys (2 subtiles of 16), fp32 4 waves of 64 keys. The norms
+// of the head's parents are summed once per workgroup (one row per thread, in
+// order); the
 // parent codebook streams through LDS in chunks of 64 rows by direct
 // global->LDS copies, double buffered. Every lane keeps a running
 // (distance, index) minimum over its rows in ascending codeword order with a
@@ -54,8 +55,9 @@ __device__ __forceinline__ void copy16_lds(const void* src, void* lds) {
 template <typename T, int D>
 struct AssignCfg {
   static constexpr bool kB = Elem<T>::kBf16;
-  static constexpr int kWaves = 4;
-  static constexpr int KS = 4;                    // key subtiles (of 16) per wave
+  // bf16: 8 waves of 32 keys (80 VGPRs at d = 128); fp32: 4 waves of 64 keys
+  static constexpr int kWaves = kB ? 8 : 4;
+  static constexpr int KS = kB ? 2 : 4;           // key subtiles (of 16) per wave
   static constexpr int kKeysPerBlock = kWaves * KS * 16;
   static constexpr int CW = 64;                   // codebook rows per chunk
   static constexpr int KQ = kB ? D / 32 : D / 4;  // MFMA k-steps over d
@@ -111,11 +113,9 @@ __device__ __forceinline__ float row_norm(const T* row) {
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(256) void parent_assign_kernel(const T* __restrict__ K,
-                                                            const T* __restrict__ Cp,
-                                                            int32_t* __restrict__ parent_idx,
-                                                            int32_t* __restrict__ code_idx, int H,
-                                                            int N, int M0, int blocks_per_bh) {
+__global__ __launch_bounds__((AssignCfg<T, D>::kWaves * 64)) void parent_assign_kernel(
+    const T* __restrict__ K, const T* __restrict__ Cp, int32_t* __restrict__ parent_idx,
+    int32_t* __restrict__ code_idx, int H, int N, int M0, int blocks_per_bh) {
   using Cfg = AssignCfg<T, D>;
   constexpr bool kB = Cfg::kB;
   constexpr int KS = Cfg::KS, CW = Cfg::CW, KQ = Cfg::KQ, U = Cfg::U, EPU = Cfg::EPU,
@@ -750,7 +750,8 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
     constexpr int slot_a = 24 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
     e = ensure_dynamic_lds((const void*)parent_assign_kernel<T, D>, Cfg::LDS_BYTES, slot_a);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid), dim3(256),
+    hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid),
+                       dim3(Cfg::kWaves * kWave),
                        Cfg::LDS_BYTES, stream, static_cast<const T*>(K),
                        static_cast<const T*>(Cp), parent_idx, Ch == 0 ? code_idx : nullptr, H, N,
                        M0, per_bh);
