@@ -15,9 +15,8 @@
 // parent_assign_kernel: one workgroup = 256 keys of one (batch, head): bf16
 // 8 waves of 32 keys (2 subtiles of 16), fp32 4 waves of 64 keys. The norms
 // of the head's parents are summed once per workgroup (one row per thread, in
-// order); the
-// parent codebook streams through LDS in chunks of 64 rows by direct
-// global->LDS copies, double buffered. Every lane keeps a running
+// order); the parent codebook streams through LDS in chunks of 64 rows by
+// direct global->LDS copies, double buffered. Every lane keeps a running
 // (distance, index) minimum over its rows in ascending codeword order with a
 // strict <, and the four lane groups merge lexicographically, so exact ties
 // go to the lowest index.
