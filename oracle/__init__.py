@@ -181,8 +181,9 @@ def capture(Q, K, parent_idx, sel, block_q: int, tile_mask=None) -> dict:
     got, best, count = 0.0, 0.0, 0
     for b in range(B):
         for h in range(H):
-            onehot = np.zeros((N, M0))
-            onehot[np.arange(N), par[b, h]] = 1.0
+            nk = K.shape[2]  # one row per key (the keys need not number N)
+            onehot = np.zeros((nk, M0))
+            onehot[np.arange(nk), par[b, h]] = 1.0
             for t in range(T):
                 if tile_mask is not None and not tile_mask[b, h, t]:
                     continue

@@ -112,3 +112,52 @@ def test_pins_catch_mutant(tmp_path, name, old, new):
                 caught.append(call)
                 break
     assert caught, f"no pin fails for the mutant '{name}'"
+
+
+# Mistakes planted in the oracle's capture (App. B, tab. tiled_capture), a
+# Python function: each is a textual edit of its source, compiled in the
+# oracle module's namespace and swapped in for the duration of the pins.
+CAPTURE_MUTANTS = [
+    ("best selection is the given selection",
+     "best += mass[:, top].sum()", "best += mass[:, sel[b, h, t]].sum()"),
+    ("best selection ranked per query instead of per tile",
+     "best += mass[:, top].sum()", "best += np.sort(mass, axis=1)[:, mass.shape[1] - P:].sum()"),
+    ("best selection ranked by key count",
+     "top = np.argsort(-mass.sum(axis=0), kind=\"stable\")[:P]",
+     "top = np.argsort(-onehot.sum(axis=0), kind=\"stable\")[:P]"),
+    ("best selection takes the smallest masses",
+     "top = np.argsort(-mass.sum(axis=0), kind=\"stable\")[:P]",
+     "top = np.argsort(mass.sum(axis=0), kind=\"stable\")[:P]"),
+    ("attention weights not normalised",
+     "A /= A.sum(axis=1, keepdims=True)", "A = A"),
+]
+
+CAPTURE_PINS = [
+    lambda: pins.test_capture_best_selection_by_enumeration(2),
+    pins.test_capture_hand_worked,
+    pins.test_capture_of_full_selection_is_one,
+]
+
+
+@pytest.mark.parametrize("name,old,new", CAPTURE_MUTANTS, ids=[m[0] for m in CAPTURE_MUTANTS])
+def test_capture_pins_catch_mutant(monkeypatch, name, old, new):
+    import inspect
+    import textwrap
+    src = textwrap.dedent(inspect.getsource(oracle.capture))
+    assert src.count(old) == 1, f"mutation anchor not unique: {old!r}"
+    ns = dict(vars(oracle))
+    exec(compile(src.replace(old, new), "<capture mutant>", "exec"), ns)
+    monkeypatch.setattr(oracle, "capture", ns["capture"])
+    caught = []
+    for call in CAPTURE_PINS:
+        try:
+            call()
+        except (AssertionError, ValueError, IndexError):
+            caught.append(call)
+            break
+    assert caught, f"no pin fails for the capture mutant '{name}'"
+
+
+def test_capture_pins_pass_on_the_oracle():
+    for call in CAPTURE_PINS:
+        call()

@@ -6,6 +6,8 @@ term, a wrong sign or index, or a transposed operand in the oracle fails at
 least one of them. ``test_oracle_mutants.py`` plants such mistakes in copies
 of the oracle and checks that these pins catch them.
 """
+import itertools
+
 import numpy as np
 import pytest
 import torch
@@ -200,6 +202,66 @@ def test_capture_of_full_selection_is_one():
 
 
 # ---------------------------------------------------------------- top-P
+
+def _capture_by_subsets(Q, K, par, M0, P, block_q):
+    """Best capture by exhaustive search: per tile, the attention mass each
+    query puts on each parent cell comes from SDPA with one-hot parent values
+    (softmax over the original keys, Eq. (standardattention)); every P-subset
+    of parents is tried and the largest total mass over the tile kept."""
+    N = Q.shape[0]
+    onehot = np.eye(M0)[par]
+    total, count = 0.0, 0
+    for t0 in range(0, N, block_q):
+        mass = ref.sdpa(Q[t0:t0 + block_q], K, onehot)  # [queries, M0]
+        best = max(mass[:, list(sub)].sum() for sub in itertools.combinations(range(M0), P))
+        total += best
+        count += mass.shape[0]
+    return total / count
+
+
+@pytest.mark.parametrize("P", [1, 2, 4])
+def test_capture_best_selection_by_enumeration(P):
+    """Capture (App. B, tab. tiled_capture): the "exact" figure is the best
+    P-subset of parents per tile, found by trying every subset; a selection
+    given to it is scored by the same SDPA masses."""
+    w = small(N=70, M0=7, Ch=2, P=P, block_q=16, d=6, q_scale=4.0)
+    x = inputs.generate(w)
+    o = run(x, w)
+    sel = np.broadcast_to(np.arange(P, dtype=np.int32)[::-1], (w.B, w.H, w.n_tiles, P))
+    cap = oracle.capture(x["Q"], x["K"], o["parent_idx"], sel, w.block_q)
+    Q, K = np64(x["Q"]), np64(x["K"])
+    exact, got, count = 0.0, 0.0, 0
+    for h in range(w.H):
+        exact += _capture_by_subsets(Q[0, h], K[0, h], o["parent_idx"][0, h], w.M0, P,
+                                     w.block_q) * w.N
+        onehot = np.eye(w.M0)[o["parent_idx"][0, h]]
+        got += ref.sdpa(Q[0, h], K[0, h], onehot)[:, :P].sum()
+        count += w.N
+    np.testing.assert_allclose(cap["exact"], exact / count, rtol=1e-12)
+    np.testing.assert_allclose(cap["selected"], got / count, rtol=1e-12)
+    assert cap["selected"] < cap["exact"]  # the fixed selection is not the best here
+
+
+def test_capture_hand_worked():
+    """Two queries, three keys in two parent cells, logits chosen so that the
+    masses are simple fractions:
+      query 0: logits (ln 1, ln 1, ln 8) on keys (cell 0, cell 0, cell 1)
+               -> masses cell 0: 2/10, cell 1: 8/10;
+      query 1: logits (ln 3, ln 3, ln 4) -> cell 0: 6/10, cell 1: 4/10.
+    Tile sums: cell 0: 0.8, cell 1: 1.2, so with P = 1 the best selection of
+    the tile is cell 1 (capture (0.8 + 0.4) / 2 = 0.6), although it holds fewer
+    keys and query 1 alone prefers cell 0 (each query's own best would give
+    0.7). Selecting cell 0 captures (0.2 + 0.6) / 2 = 0.4."""
+    K = np.array([[1.0, 0.0], [1.0, 0.0], [0.0, 1.0]])
+    Q = np.array([[0.0, np.log(8.0)], [np.log(3.0), np.log(4.0)]])
+    par = np.array([0, 0, 1], np.int32)[None, None]
+    Qb, Kb = Q[None, None], K[None, None]
+    c1 = oracle.capture(Qb, Kb, par, np.array([[[[1]]]], np.int32), block_q=2)
+    c0 = oracle.capture(Qb, Kb, par, np.array([[[[0]]]], np.int32), block_q=2)
+    assert abs(c1["exact"] - 0.6) < 1e-12 and abs(c0["exact"] - 0.6) < 1e-12
+    assert abs(c1["selected"] - 0.6) < 1e-12
+    assert abs(c0["selected"] - 0.4) < 1e-12
+
 
 @pytest.mark.parametrize("P", [0, 1, 3, 6])
 def test_topp_matches_enumeration(P):
