@@ -5,10 +5,13 @@ compared under a certification rule: a decision is *certified* when the
 oracle's fp64 margin exceeds a bound on the kernel's fp32 rounding error, and
 certified decisions must match bit for bit. An uncertified decision may go
 either way; if the kernel's choice differs from the oracle's it must be a
-valid choice within that bound, and values downstream of it (the aggregates
-of that head, the output rows of that tile) are then left out of the
-element-wise comparison and counted. Everything else is compared element by
-element: integers exactly, floats within the stated tolerance.
+valid choice within that bound, and everything downstream of it is then
+compared with the oracle re-run on the kernel's choice: where codes differ,
+the oracle's aggregates, importance, top-P and output are recomputed from the
+GPU's codes (every head is compared); where a tile's top-P set differs, its
+output rows are compared with the oracle's output for the GPU's selection
+(every tile is compared). Nothing is left out. Integers are compared exactly,
+floats within the stated tolerance.
 
 Error bounds (u = 2^-24, gamma_n = n u / (1 - n u)):
 * parent distances ||c||^2 - 2 k.c: products of bf16 inputs are exact in
@@ -109,8 +112,8 @@ class Report(dict):
 
 
 def check_assign(x, w, g, o) -> tuple:
-    """Certified-exact comparison of parent_idx / code_idx. Returns the mask of
-    (b, h) heads whose codes equal the oracle's everywhere, and a report."""
+    """Certified-exact comparison of parent_idx / code_idx; every differing
+    (uncertified) decision must be a valid choice within the bound."""
     K, Cp, Cc = oracle.f64(x["K"]), oracle.f64(x["Cp"]), oracle.f64(x["Cc"])
     d = w.d
     knorm = np.linalg.norm(K, axis=-1)
@@ -155,11 +158,10 @@ def check_assign(x, w, g, o) -> tuple:
         else:
             assert gc[b, h, j] == p
             assert dpar <= dc.min() + tol
-    clean = ~diff.any(axis=-1)
     rep = Report(keys=int(diff.size), uncertified=int((~code_cert).sum()),
-                 differing=int(diff.sum()), heads_excluded=int((~clean).sum()),
+                 differing=int(diff.sum()), heads_on_gpu_codes=int(diff.any(axis=-1).sum()),
                  moved_frac=round(float((oc >= w.M0).mean()), 4))
-    return clean, rep
+    return rep
 
 
 def _check_flat_assign(K, Cp, w, gp, gc, op, err_p, par_cert) -> tuple:
@@ -170,23 +172,24 @@ def _check_flat_assign(K, Cp, w, gp, gc, op, err_p, par_cert) -> tuple:
     for b, h, j in np.argwhere(diff):
         dp = ((Cp[h] - K[b, h, j]) ** 2).sum(-1)
         assert dp[gp[b, h, j]] <= dp.min() + 4 * err_p[b, h, j], "invalid parent choice"
-    clean = ~diff.any(axis=-1)
     rep = Report(keys=int(diff.size), uncertified=int((~par_cert).sum()),
-                 differing=int(diff.sum()), heads_excluded=int((~clean).sum()), moved_frac=0.0)
-    return clean, rep
+                 differing=int(diff.sum()), heads_on_gpu_codes=int(diff.any(axis=-1).sum()),
+                 moved_frac=0.0)
+    return rep
 
 
-def check_aggregate(x, w, g, o, clean) -> Report:
-    """Counts exact; Vbar within the fp32 summation bound, on clean heads."""
+def check_aggregate(x, w, g, o) -> Report:
+    """Counts exact; Vbar within the fp32 summation bound (o: the oracle on the
+    codes the GPU compared against, see oracle_on_gpu_codes)."""
     gn, gV = g["counts"].numpy(), g["Vbar"].numpy()
     on, oV = o["counts"], o["Vbar"]
-    np.testing.assert_array_equal(gn[clean], on[clean])
+    np.testing.assert_array_equal(gn, on)
     # |fl(sum) - sum| <= gamma_(n-1) sum |v| for each element; |V| aggregated by the oracle
     absV, _ = oracle.aggregate(np.abs(oracle.f64(x["V"])), o["parent_idx"], o["code_idx"], w.M0,
                                w.Ch)
     tol = gamma(np.maximum(on, 1))[..., None] * absV + 1e-30
     err = np.abs(gV.astype(np.float64) - oV)
-    assert (err[clean] <= tol[clean]).all(), f"Vbar error {err[clean].max()} above bound"
+    assert (err <= tol).all(), f"Vbar error {err.max()} above bound"
     assert (gn[..., :w.M0].sum(-1) == w.N).all()
     # Packed aggregates: means fl(fl(sum) * fl(1/n)) rounded to the storage
     # dtype; n exact; ln n within a few ulp; empty codes and padding slots
@@ -194,21 +197,20 @@ def check_aggregate(x, w, g, o, clean) -> Report:
     means, n_pk, ln_pk, pad = unpack_packed(g["packed"].numpy(), w.M0, w.Ch, w.d, w.dtype)
     assert (pad["means"] == 0).all(), "padding means of the packed aggregates are not zero"
     assert (pad["n"] == 0).all() and np.isneginf(pad["ln"]).all(), "padding info is not empty"
-    np.testing.assert_array_equal(n_pk[clean], on[clean].astype(np.float32))
+    np.testing.assert_array_equal(n_pk, on.astype(np.float32))
     nz = on > 0
     ln_err = np.abs(ln_pk.astype(np.float64) - np.log(np.maximum(on, 1)))
-    assert (ln_err[nz & clean[..., None]] <= 8 * U * np.log(np.maximum(on, 2))[nz & clean[..., None]]
-            + 1e-7).all(), "ln n of the packed aggregates is off"
-    assert np.isneginf(ln_pk[~nz & clean[..., None]]).all()
+    assert (ln_err[nz] <= 8 * U * np.log(np.maximum(on, 2))[nz] + 1e-7).all(), \
+        "ln n of the packed aggregates is off"
+    assert np.isneginf(ln_pk[~nz]).all()
     n = np.maximum(on, 1)[..., None]
     omean = oV / n
     r_store = 2.0 ** -8 if w.dtype == "bf16" else U
     tol_m = tol / n + (3 * U + r_store) * np.abs(omean) + 1e-30
     err_m = np.abs(means - omean)
-    assert (err_m[clean] <= tol_m[clean]).all(), f"mean error {err_m[clean].max()} above bound"
-    assert (means[clean][on[clean] == 0] == 0).all(), "mean of an empty code is not zero"
-    return Report(max_vbar_err=float(err[clean].max()) if clean.any() else 0.0,
-                  max_mean_err=float(err_m[clean].max()) if clean.any() else 0.0)
+    assert (err_m <= tol_m).all(), f"mean error {err_m.max()} above bound"
+    assert (means[on == 0] == 0).all(), "mean of an empty code is not zero"
+    return Report(max_vbar_err=float(err.max()), max_mean_err=float(err_m.max()))
 
 
 def importance_eps(x, w, o) -> float:
@@ -226,57 +228,78 @@ def importance_eps(x, w, o) -> float:
             + 2 * U * shift + 2 * gamma(w.M0 + w.block_q))
 
 
-def check_topp(x, w, g, o, clean, tile_mask) -> tuple:
-    """Importance within eps_w; top-P sets certified-exact. Returns the mask of
-    tiles whose selection equals the oracle's (and whose head is clean)."""
+def check_topp(x, w, g, o, tile_mask) -> tuple:
+    """Importance within eps_w; top-P sets certified-exact; the order of
+    topp_idx canonical. Returns the mask of tiles whose selection differs from
+    the oracle's (uncertified, valid alternatives) and a report.
+
+    Order: the kernel lists its selection by its own importance, descending,
+    lowest index first among equal values; that is checked exactly against
+    the importance it returns. Against the oracle, every certified cut point
+    of the oracle's order (a gap between ranks k and k+1 above the bound) must
+    split the kernel's list into the same two sets."""
     eps = importance_eps(x, w, o)
     T = w.n_tiles
-    sel_ok = np.zeros((w.B, w.H, T), bool)
+    differ = np.zeros((w.B, w.H, T), bool)
     gw, ow = g["importance"].numpy().astype(np.float64), o["importance"]
     gt, ot = g["topp"].numpy(), o["selection"]
-    rep = Report(tiles=0, uncertified=0, differing=0, eps_w=float(f"{eps:.3g}"))
-    for b, h, t in np.argwhere(tile_mask & clean[..., None]):
-        rep["tiles"] += 1
-        wt, gwt = ow[b, h, t], gw[b, h, t]
-        scale = wt.sum()  # = tile size
-        assert np.all(np.abs(gwt - wt) <= eps * wt + 1e-6 * eps * scale), (
-            f"importance off at tile {(b, h, t)}: max rel {np.max(np.abs(gwt - wt) / np.maximum(wt, 1e-30))}")
-        empty = o["counts"][b, h, :w.M0] == 0
-        assert (gwt[empty] == 0).all(), "empty parents must have exactly zero importance"
-        if w.P == 0:
-            sel_ok[b, h, t] = True
-            continue
+    rep = Report(tiles=int(tile_mask.sum()), uncertified=0, differing=0, cut_points=0,
+                 eps_w=float(f"{eps:.3g}"))
+    scale = ow.sum(-1, keepdims=True)  # = tile size
+    bad = tile_mask[..., None] & ~(np.abs(gw - ow) <= eps * ow + 1e-6 * eps * scale)
+    assert not bad.any(), (f"importance off at {np.argwhere(bad)[:3]}: max rel "
+                           f"{np.max(np.abs(gw - ow)[bad] / np.maximum(ow[bad], 1e-30))}")
+    empty = (o["counts"][..., :w.M0] == 0)[:, :, None, :]
+    assert (gw[np.broadcast_to(empty, gw.shape) & tile_mask[..., None]] == 0).all(), \
+        "empty parents must have exactly zero importance"
+    if w.P == 0:
+        return differ, rep
+    # the kernel's own canonical order, exactly
+    gsel = np.take_along_axis(g["importance"].numpy(), gt.astype(np.int64), -1)
+    desc = gsel[..., :-1] > gsel[..., 1:]
+    tie = (gsel[..., :-1] == gsel[..., 1:]) & (gt[..., :-1] < gt[..., 1:])
+    wrong = tile_mask[..., None] & ~(desc | tie)
+    assert not wrong.any(), f"topp_idx not in canonical order at {np.argwhere(wrong)[:3]}"
+    for b, h, t in np.argwhere(tile_mask):
+        wt = ow[b, h, t]
+        sc = scale[b, h, t, 0]
         order = np.lexsort((np.arange(w.M0), -wt))
         srt = wt[order]
         gs, os_ = set(gt[b, h, t].tolist()), set(ot[b, h, t].tolist())
         assert len(gs) == w.P, "selection has repeated parents"
         wP = srt[w.P - 1]
         wnext = srt[w.P] if w.P < w.M0 else -np.inf
-        certified = (wP - wnext) > 2 * eps * wP + 2e-6 * eps * scale or w.P == w.M0
+        certified = (wP - wnext) > 2 * eps * wP + 2e-6 * eps * sc or w.P == w.M0
         if not certified:
             rep["uncertified"] += 1
         if gs == os_:
-            sel_ok[b, h, t] = True
-            # order within the set: (w desc, index asc) where the gaps are certified
+            cut = (srt[:w.P - 1] - srt[1:w.P]) > 2 * eps * srt[:w.P - 1] + 2e-6 * eps * sc
+            for k in np.flatnonzero(cut):
+                assert set(gt[b, h, t, :k + 1].tolist()) == set(order[:k + 1].tolist()), (
+                    f"topp_idx order differs from the oracle's at a certified rank {k}, "
+                    f"tile {(b, h, t)}")
+            rep["cut_points"] += int(cut.sum())
             continue
         assert not certified, f"certified top-P set differs at tile {(b, h, t)}"
         rep["differing"] += 1
+        differ[b, h, t] = True
         # a valid alternative: nothing left out beats anything taken by more than the bound
         taken = np.array(sorted(gs))
         left = np.setdiff1d(np.arange(w.M0), taken)
-        assert wt[taken].min() >= wt[left].max() * (1 - 2 * eps) - 2e-6 * eps * scale, (
+        assert wt[taken].min() >= wt[left].max() * (1 - 2 * eps) - 2e-6 * eps * sc, (
             f"invalid top-P choice at tile {(b, h, t)}")
-    return sel_ok, rep
+    return differ, rep
 
 
-def check_output(x, w, g, o, sel_ok) -> Report:
+def check_output(x, w, g, o, tile_mask) -> Report:
     """Per row ||Y - Y*||_inf / ||Y*||_inf within the dtype's tolerance on every
     row of every compared tile."""
     tol = TOL_Y[w.dtype]
     gY = g["Y"].float().numpy().astype(np.float64)
     oY = o["Y"]
-    rows = np.repeat(sel_ok, w.block_q, axis=-1)[..., :w.N]
+    rows = np.repeat(tile_mask, w.block_q, axis=-1)[..., :w.N]
     assert np.isfinite(gY).all(), "non-finite output"
+    assert np.isfinite(oY[rows]).all()
     num = np.abs(gY - oY).max(-1)
     den = np.abs(oY).max(-1)
     rel = np.where(rows, num / np.maximum(den, 1e-30), 0.0)
@@ -286,6 +309,24 @@ def check_output(x, w, g, o, sel_ok) -> Report:
     fro = np.linalg.norm((gY - oY)[rows]) / np.linalg.norm(oY[rows])
     return Report(rows=int(rows.sum()), max_rel=float(f"{rel.max():.3g}"),
                   median_rel=float(f"{np.median(rel_rows):.3g}"), frob_rel=float(f"{fro:.3g}"))
+
+
+def oracle_on_gpu_codes(x, w, g, mask, recovered, importance_tile) -> dict:
+    """The oracle's aggregates, importance, top-P and output computed from the
+    GPU's codes (its certification distances are not needed downstream)."""
+    gp = g["parent_idx"].numpy().astype(np.int32)
+    gc = g["code_idx"].numpy().astype(np.int32)
+    Vbar, counts = oracle.aggregate(x["V"], gp, gc, w.M0, w.Ch)
+    if importance_tile is None:
+        imp = oracle.importance(x["Q"], x["Cp"], counts, w.Ch, w.block_q, mask)
+    else:
+        imp = oracle.importance_tiled(x["Q"], x["Cp"], counts, w.Ch, w.block_q, importance_tile,
+                                      mask)
+    sel = oracle.topp(imp, w.P, mask)
+    Y, zr = oracle.output(x["Q"], x["Cp"], x["Cc"], Vbar, counts, sel, w.block_q, recovered,
+                          mask)
+    return dict(parent_idx=gp, code_idx=gc, Vbar=Vbar, counts=counts, importance=imp,
+                selection=sel, Y=Y, zratio=zr)
 
 
 def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False,
@@ -311,12 +352,26 @@ def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False,
     g = gpu_forward(to_gpu(x), w, tiled, query_order)
     if query_order is not None:
         x = dict(x, Q=x["Q"][:, :, torch.as_tensor(query_order, dtype=torch.long)].contiguous())
+    itile = avq.IMPORTANCE_TILE if tiled else None
     o = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], w.P, w.block_q,
-                       recovered=recovered, tile_mask=mask,
-                       importance_tile=avq.IMPORTANCE_TILE if tiled else None)
-    clean, ra = check_assign(x, w, g, o)
-    rg = check_aggregate(x, w, g, o, clean)
-    sel_ok, rt = check_topp(x, w, g, o, clean, mask.astype(bool))
-    ry = check_output(x, w, g, o, sel_ok & mask.astype(bool) & clean[..., None])
+                       recovered=recovered, tile_mask=mask, importance_tile=itile)
+    ra = check_assign(x, w, g, o)
+    if ra["differing"]:
+        # uncertified codes went the other way: follow the GPU's codes downstream
+        o = oracle_on_gpu_codes(x, w, g, mask, recovered, itile)
+    rg = check_aggregate(x, w, g, o)
+    tmask = mask.astype(bool)
+    differ, rt = check_topp(x, w, g, o, tmask)
     assert rt["differing"] <= max(1, 0.01 * rt["tiles"]), "too many differing top-P sets"
+    if differ.any():
+        # tiles whose (uncertified) selection differs: the oracle's output on
+        # the GPU's selection
+        sel = np.array(o["selection"], copy=True)
+        sel[differ] = g["topp"].numpy()[differ]
+        Yf, _ = oracle.output(x["Q"], x["Cp"], x["Cc"], o["Vbar"], o["counts"], sel, w.block_q,
+                              recovered, differ.astype(np.uint8))
+        rows = np.repeat(differ, w.block_q, axis=-1)[..., :w.N]
+        o = dict(o, Y=np.where(rows[..., None], Yf, o["Y"]))
+    ry = check_output(x, w, g, o, tmask)
+    ry["rows_on_gpu_selection"] = int(np.repeat(differ, w.block_q, axis=-1)[..., :w.N].sum())
     return dict(assign=ra, aggregate=rg, topp=rt, output=ry, gpu=g, oracle=o)
