@@ -20,10 +20,12 @@
 // empty parent (ln n = -inf) drops out of the max and of every sum without
 // masks. It is applied to the parent's mean value Vbar/n, so
 // sum_p n_p exp(S_p - m) Vbar_p / n_p is the numerator of
-// Eq. (vqflashattention). The children keep their raw logits (the recovered
-// parent logit needs them) and their correcting weight is
-// n_c (exp(T_c - m) - exp(Srec - m)), Eq. (correcting_attention) times n_c,
-// which is zero for empty children and padding rows (n = 0). The denominator
+// Eq. (vqflashattention). The recovered parent logit is taken from the raw
+// child logits T_c (all Ch children, empty ones included); then the children
+// take the same bias, T_c + ln n_c, so that empty children and padding rows
+// (-inf) take no part in the running max (App. D), and their correcting weight
+// exp(T_c + ln n_c - m) - n_c exp(Srec - m), Eq. (correcting_attention) times
+// n_c, is exactly zero for them however far their logits lie. The denominator
 // comes out of the value MFMA through one extra d-tile whose first row is all
 // ones, so numerator and denominator use the same rounded weights.
 //
@@ -50,7 +52,8 @@
 //      bit from the top, finds the P-th largest value; ties at it go to the
 //      lowest indices; the selected parents are listed in index order;
 //   4. child sweep over the child octets of the selected parents: logits,
-//      recovered parent logit, correcting weights, Xbar += Vmean^T dW;
+//      recovered parent logit, log-count bias (running max over non-empty
+//      children), correcting weights, Xbar += Vmean^T dW;
 //   5. Y = Xbar / Z.
 // With a query order, tile position i takes token order[i]: Q rows are read
 // from, and Y rows written to, those tokens.
@@ -419,16 +422,16 @@ void attention_kernel(AttnArgs args) {
           zp[s] += w;
         }
   };
-  // correcting weights n (exp(T - m) - exp(Srec - m)) of tile pair b, in
-  // place. Recovered parent logit over the octet rows: Ch = 2: rows 0-1 of the
-  // even tile (the rest is padding); Ch = 4: the 4 rows of each tile (one
-  // parent per tile); Ch = 8: the whole octet; Ch = 16: and the partner lane
-  // group's octet.
+  // Recovered parent logit (Eq. (parent_recovery)) from the raw child logits
+  // of tile pair b: the sum over all Ch children of the parent, empty ones
+  // included (divided by Ch where it is used). Over the octet rows: Ch = 2:
+  // rows 0-1 of the even tile (the rest is padding); Ch = 4: the 4 rows of
+  // each tile (one parent per tile); Ch = 8: the whole octet; Ch = 16: and the
+  // partner lane group's octet.
   // 0/1 weights of the recovered-logit cases (exact products and sums)
   const float w2 = Ch == 2 ? 1.f : 0.f, w4 = Ch == 4 ? 1.f : 0.f, w8 = Ch == 8 ? 1.f : 0.f,
               w16 = Ch == 16 ? 1.f : 0.f;
-  auto child_weights = [&](const unsigned char* B, int b, f32x4 (&S)[2][QS]) {
-    float er[2][QS];
+  auto child_recover = [&](const f32x4 (&S)[2][QS], float (&rs)[2][QS]) {
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
       // every case computed and one kept by 0/1 weights: no branch splits
@@ -439,20 +442,40 @@ void attention_kernel(AttnArgs args) {
       const float bs = (v1[0] + v1[1]) + (v1[2] + v1[3]);
       const float ab = a + bs;
       const float ab16 = ab + shfl_xor(ab, 16);
-      const float s0 = fmaf(w2, a01, fmaf(w4, a, fmaf(w8, ab, w16 * ab16)));
-      const float s1 = fmaf(w2, a01, fmaf(w4, bs, fmaf(w8, ab, w16 * ab16)));
-      const float scale = kLog2e / (float)Ch;
-      er[0][s] = exp2_hw(fminf(fmaf(s0, scale, -m[s]), 64.f));
-      er[1][s] = exp2_hw(fminf(fmaf(s1, scale, -m[s]), 64.f));
+      rs[0][s] = fmaf(w2, a01, fmaf(w4, a, fmaf(w8, ab, w16 * ab16)));
+      rs[1][s] = fmaf(w2, a01, fmaf(w4, bs, fmaf(w8, ab, w16 * ab16)));
     }
+  };
+  // log-count bias of the child logits of tile pair b, in place: T + ln n,
+  // -inf for empty children and padding rows (App. D: the running max is
+  // taken over non-empty codes only)
+  auto child_bias = [&](const unsigned char* B, int b, f32x4 (&S)[2][QS]) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const f32x4 l4 = info4(B, 2 * b + h2, 1);
+#pragma unroll
+      for (int s = 0; s < QS; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S[h2][s][r] += l4[r];
+    }
+  };
+  // correcting weights exp(T + ln n - m) - n exp(Srec - m) of tile pair b
+  // (biased logits in S, recovered sums in rs), in place. Empty children and
+  // padding: exp2(-inf) = 0 and n = 0, so the weight is exactly 0; the
+  // recovered term is clamped below 2^64, so 0 times it stays 0.
+  auto child_weights = [&](const unsigned char* B, int b, f32x4 (&S)[2][QS],
+                           const float (&rs)[2][QS]) {
+    const float scale = kLog2e / (float)Ch;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       const f32x4 n4 = info4(B, 2 * b + h2, 0);
 #pragma unroll
-      for (int s = 0; s < QS; ++s)
+      for (int s = 0; s < QS; ++s) {
+        const float er = exp2_hw(fminf(fmaf(rs[h2][s], scale, -m[s]), 64.f));
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          S[h2][s][r] = n4[r] * (exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])) - er[h2][s]);
+          S[h2][s][r] = fmaf(-n4[r], er, exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])));
+      }
     }
   };
   // logits of the chunk's two tile pairs; parents start from ln n
@@ -739,11 +762,16 @@ void attention_kernel(AttnArgs args) {
       const unsigned char* B = buffer(k % Cfg::NBUF);
       if (has_rows) {
         f32x4 S0[2][QS], S1[2][QS];
+        float rs0[2][QS], rs1[2][QS];
         chunk_logits(B, false, S0, S1);
+        child_recover(S0, rs0);
+        child_recover(S1, rs1);
+        child_bias(B, 0, S0);
+        child_bias(B, 1, S1);
         check_chunk(S0, S1);
-        child_weights(B, 0, S0);
+        child_weights(B, 0, S0, rs0);
         accumulate_pair(B, 0, S0);
-        child_weights(B, 1, S1);
+        child_weights(B, 1, S1, rs1);
         accumulate_pair(B, 1, S1);
       }
       if (Cfg::NBUF == 1 && k + 1 < n_cchunks) {  // one buffer: refill it when all are done

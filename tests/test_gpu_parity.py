@@ -7,9 +7,7 @@ decisions, Vbar within the fp32 summation bound, importance within eps_w,
 and Y per row within 1e-4 (fp32) / 2e-2 (bf16) relative to max|Y*|.
 
 The five evaluation workloads run at their full sizes in the same launch
-configuration as the benchmark; for the two largest, the oracle evaluates a
-sample of query tiles per head (plus the first and last), all keys' codes
-and all aggregates.
+configuration as the benchmark, every query tile of every head compared.
 """
 import sys
 
@@ -126,6 +124,39 @@ def test_children_equal_parent_gives_vq_attention():
     y_ref = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q)
     y0 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, 0, w.block_q)
     assert torch.equal(y_ref, y0)
+
+
+@pytest.mark.parametrize("dtype,P", [("bf16", 16), ("f32", 16), ("bf16", 6)])
+def test_empty_far_children(dtype, P):
+    """App. D: two children of a parent that the tiles select lie 100 units
+    out on either side of it along the first axis, where every query has
+    component +-3, so no key moves to them and one of them has a logit about
+    300 natural units above every non-empty code's. The running max must skip
+    empty children and their correcting weights must be exactly zero;
+    otherwise the rescale underflows the accumulators and Y = 0/0."""
+    import oracle
+    w = small(dtype=dtype, M0=16, Ch=8, P=P, N=600, B=1, H=2)
+    banner(f"empty_far_children_{dtype}_P{P}", w)
+    x = inputs.generate(w)
+    Q = x["Q"].clone()
+    sign = torch.where(torch.arange(w.N) % 2 == 0, 3.0, -3.0)
+    Q[..., 0] = sign.to(Q.dtype)
+    x = dict(x, Q=Q.contiguous())
+    # the parent selected most often (importance does not depend on the children)
+    o0 = oracle.forward(x["Q"], x["K"], x["V"], x["Cp"], x["Cc"], w.P, w.block_q)
+    p = int(np.bincount(o0["selection"].reshape(-1), minlength=w.M0).argmax())
+    Cc = x["Cc"].clone()
+    far = torch.zeros(w.d, dtype=Cc.dtype)
+    far[0] = 100.0
+    Cc[:, p, 0] = x["Cp"][:, p] + far
+    Cc[:, p, 1] = x["Cp"][:, p] - far
+    x = dict(x, Cc=Cc.contiguous())
+    res = parity.compare(x, w)
+    report(res)
+    o = res["oracle"]
+    first = w.M0 + p * w.Ch
+    assert (o["counts"][:, :, first:first + 2] == 0).all()  # both far children are empty
+    assert (o["selection"] == p).any(axis=-1).sum() >= 2, "the far children's parent is not selected"
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -278,17 +309,16 @@ def test_order_entries_out_of_range_are_skipped():
     assert (y1[:, :, 17] == 7.0).all() and (y1[:, :, 300] == 7.0).all()
 
 
-SAMPLE = {"c1": None, "c2": None, "c3": None, "c4": 12, "c5": 4}
-
-
-# The five evaluation workloads run last (largest oracle work).
+# The five evaluation workloads run last (largest oracle work): every tile.
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
 def test_workload(name):
     w = inputs.WORKLOADS[name]
     banner(name, w)
     x = inputs.generate(w)
-    res = parity.compare(x, w, tiles_per_head=SAMPLE[name])
+    res = parity.compare(x, w)
     report(res)
+    assert res["output"]["rows"] == w.B * w.H * w.N
+    assert res["topp"]["tiles"] == w.B * w.H * w.n_tiles
 
 
 @pytest.mark.parametrize("Ch", [0, 4])
@@ -318,3 +348,69 @@ def test_aggregate_ignores_out_of_range_codes(Ch):
             exp_V[b, h], exp_n[b, h] = rv[0, 0], rn[0, 0]
     np.testing.assert_array_equal(counts.cpu().numpy(), exp_n)
     np.testing.assert_allclose(Vbar.cpu().numpy(), exp_V, rtol=1e-5, atol=1e-4)
+
+
+@pytest.mark.parametrize("dtype,Ch,d", [("bf16", 8, 128), ("f32", 4, 64), ("bf16", 0, 64),
+                                        ("bf16", 16, 64), ("f32", 2, 128)])
+def test_pack_aggregates_path(dtype, Ch, d):
+    """Alg. 2 takes the aggregates as (Vbar, n): avq_aggregate's fp32 sums and
+    counts packed by avq_pack_aggregates give exactly the bytes of its own
+    packed output, and the attention from them is bit-equal and passes parity
+    against the oracle."""
+    import oracle
+    from paper_2607_12789_amd import avq
+    w = small(dtype=dtype, Ch=Ch, d=d, P=0 if Ch == 0 else 5, M0=40)
+    banner(f"pack_aggregates_{dtype}_ch{Ch}_d{d}", w)
+    x = inputs.generate(w)
+    xd = parity.to_gpu(x)
+    par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+    packed, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
+    packed2 = avq.pack_aggregates(Vbar, counts, w.M0, w.Ch, w.torch_dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(packed, packed2)
+    y1, t1, i1 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q, debug=True)
+    y2, t2, i2 = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed2, w.P, w.block_q,
+                                   debug=True)
+    assert torch.equal(y1, y2) and torch.equal(t1, t2) and torch.equal(i1, i2)
+    # the packed path's own output against the oracle on the same codes and
+    # selection (the certification of both is the general parity test's)
+    res = parity.compare(x, w)
+    report(res)
+    g = dict(parent_idx=par.cpu(), code_idx=code.cpu(), topp=t2.cpu(), Y=y2.cpu())
+    mask = np.ones((w.B, w.H, w.n_tiles), np.uint8)
+    o = parity.oracle_on_gpu_codes(x, w, g, mask, True, None)
+    sel = g["topp"].numpy() if w.P > 0 else o["selection"]
+    oY, _ = oracle.output(x["Q"], x["Cp"], x["Cc"], o["Vbar"], o["counts"], sel, w.block_q)
+    ry = parity.check_output(x, w, g, dict(o, Y=oY), mask.astype(bool))
+    print(f"  pack path output: {ry.line()}", flush=True)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_pack_aggregates_caller_values(dtype):
+    """Aggregates from the caller (random sums, counts with zeros and negative
+    entries): every mean is fl(fl(Vbar) * fl(1/n)) rounded to the storage type
+    (numpy fp32 arithmetic, then torch's round to nearest even), n exact,
+    ln n within a few ulp, empty codes and padding 0 and -inf."""
+    from paper_2607_12789_amd import avq
+    B, H, M0, Ch, d = 2, 3, 37, 4, 64
+    Mtot = M0 * (1 + Ch)
+    rng = np.random.default_rng(11)
+    Vbar = (rng.standard_normal((B, H, Mtot, d)) * 50).astype(np.float32)
+    counts = rng.integers(-3, 300, size=(B, H, Mtot)).astype(np.int32)
+    counts[rng.random((B, H, Mtot)) < 0.2] = 0
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    pk = avq.pack_aggregates(torch.from_numpy(Vbar).cuda(), torch.from_numpy(counts).cuda(), M0,
+                             Ch, tdt)
+    torch.cuda.synchronize()
+    means, n_pk, ln_pk, pad = parity.unpack_packed(pk.cpu().numpy(), M0, Ch, d, dtype)
+    n = np.maximum(counts, 0)
+    inv = np.where(n > 0, np.float32(1) / np.maximum(n, 1).astype(np.float32), np.float32(0))
+    m32 = (Vbar * inv[..., None].astype(np.float32)).astype(np.float32)
+    expect = torch.from_numpy(m32).to(tdt).double().numpy()
+    np.testing.assert_array_equal(means, expect)
+    np.testing.assert_array_equal(n_pk, n.astype(np.float32))
+    nz = n > 0
+    assert np.isneginf(ln_pk[~nz]).all()
+    err = np.abs(ln_pk[nz].astype(np.float64) - np.log(n[nz]))
+    assert (err <= 8 * 2.0 ** -24 * np.maximum(np.log(n[nz]), 1)).all()
+    assert (pad["means"] == 0).all() and (pad["n"] == 0).all() and np.isneginf(pad["ln"]).all()
