@@ -10,6 +10,8 @@
  *                      parent (Sec. 4.2, Alg. 1)
  *   avq_aggregate      per-codeword key counts and value sums
  *                      (Eq. (aggregates), Alg. 1)
+ *   avq_pack_aggregates  value sums and counts held by the caller, in the
+ *                      operand layout of the attention kernel
  *   avq_attention_fwd  parent attention, per-query-tile importance, top-P
  *                      parent selection, child refinement with correcting
  *                      attention and normalisation (Sec. 4.3,
@@ -142,6 +144,29 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
                            float* Vbar, int32_t* counts, void* packed, void* stream);
 
 /*
+ * avq_pack_aggregates - the aggregates in the form Alg. 2 takes them (its
+ * input: the value sum Vbar and the count n of every code, Eq. (aggregates))
+ * packed into the operand layout that avq_attention_fwd reads (the packed
+ * buffer described under avq_aggregate). A caller that holds (Vbar, n) from
+ * elsewhere reaches the attention kernel through this call.
+ *
+ * For every code x with n = max(counts[x], 0): mean = Vbar[x] * fl(1/n) in
+ * fp32 (0 for n = 0), rounded once to dtype; info n (as a float) and
+ * ln n = log2(n) ln 2 (-inf for n = 0); padding slots and the empty octet as
+ * in avq_aggregate. This is the aggregation's own arithmetic: the Vbar and
+ * counts that avq_aggregate writes pack into exactly its packed output.
+ *
+ *   Vbar     [B][H][Mtot][d]  fp32, rows as in avq_aggregate (parent rows the
+ *                             whole cell, child rows the keys moved there)
+ *   counts   [B][H][Mtot]     int32 (negative entries count as 0)
+ *   packed   [B][H][E] bytes, out; E = avq_packed_bytes(dtype, M0, Ch, d)
+ * Sizes as for avq_aggregate (N does not apply).
+ */
+avq_status_t avq_pack_aggregates(avq_dtype_t dtype, int32_t B, int32_t H, int32_t d,
+                                 int32_t M0, int32_t Ch, const float* Vbar,
+                                 const int32_t* counts, void* packed, void* stream);
+
+/*
  * avq_attention_fwd - the fused refined-codebook attention (Alg. 2).
  *
  * Queries are taken in tiles of block_q consecutive tokens (the last tile may
@@ -167,7 +192,8 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
  *                and top-P are computed per tile of block_q tokens)
  *   Q            [B][H][N][d]    dtype
  *   Cp, Cc       as in avq_assign (Cc NULL allowed when Ch = 0)
- *   packed       the packed aggregates written by avq_aggregate (required)
+ *   packed       the packed aggregates written by avq_aggregate or by
+ *                avq_pack_aggregates (required)
  *   Y            [B][H][N][d]    dtype, out
  *   topp_idx     [B][H][T][P]    int32, out, nullable; T = ceil(N / block_q);
  *                the selected parents in the order importance descending,

@@ -22,7 +22,8 @@ AVQ_F32, AVQ_BF16 = 0, 1
 _DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
 SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_bytes", "avq_assign",
            "avq_aggregate", "avq_attention_fwd", "avq_attention_fwd_tiled",
-           "avq_codebook_update", "avq_attention_fwd_ordered", "avq_gilbert_order")
+           "avq_codebook_update", "avq_attention_fwd_ordered", "avq_gilbert_order",
+           "avq_pack_aggregates")
 IMPORTANCE_TILE = 64  # parents per codeword tile of attention_fwd(tiled_importance=True)
 
 
@@ -60,7 +61,8 @@ def lib():
         L.avq_gilbert_order.argtypes = [i32, i32, vp, vp]
         L.avq_codebook_update.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, ctypes.c_float,
                                           vp, vp, vp, vp, vp, vp, vp]
-        for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd",
+        L.avq_pack_aggregates.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, vp, vp, vp, vp]
+        for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd", "avq_pack_aggregates",
                      "avq_attention_fwd_tiled", "avq_codebook_update",
                      "avq_attention_fwd_ordered", "avq_gilbert_order"):
             getattr(L, name).restype = ctypes.c_int
@@ -154,6 +156,24 @@ def aggregate(V, code_idx, M0: int, Ch: int, packed=None, counts=None, Vbar=None
     _check(lib().avq_aggregate(_dtype_code(V), B, H, N, d, M0, Ch, _ptr(V), _ptr(code_idx),
                                _ptr(Vbar), _ptr(counts), _ptr(packed), _stream(stream)))
     return packed, counts, Vbar
+
+
+def pack_aggregates(Vbar, counts, M0: int, Ch: int, dtype, packed=None, stream=None):
+    """The paper's aggregates (Vbar fp32 [B, H, Mtot, d], counts int32
+    [B, H, Mtot]) in the operand layout ``attention_fwd`` reads
+    (``avq_pack_aggregates``). Returns packed (uint8 [B, H, packed_bytes])."""
+    B, H, Mtot, d = Vbar.shape
+    if Mtot != M0 * (1 + Ch):
+        raise ValueError(f"Vbar holds {Mtot} codes, expected M0 * (1 + Ch) = {M0 * (1 + Ch)}")
+    _dev(Vbar, "Vbar", torch.float32)
+    _dev(counts, "counts", torch.int32, (B, H, Mtot))
+    E = packed_bytes(dtype, M0, Ch, d)
+    if packed is None:
+        packed = torch.empty((B, H, E), dtype=torch.uint8, device=Vbar.device)
+    _dev(packed, "packed", torch.uint8, (B, H, E))
+    _check(lib().avq_pack_aggregates(_DTYPES[dtype], B, H, d, M0, Ch, _ptr(Vbar), _ptr(counts),
+                                     _ptr(packed), _stream(stream)))
+    return packed
 
 
 def attention_fwd(Q, Cp, Cc, packed, P: int, block_q: int, Y=None, topp_idx=None,

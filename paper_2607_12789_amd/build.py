@@ -24,7 +24,7 @@ ROOT = PKG.parent
 CSRC = PKG / "csrc"
 LIB = PKG / "libavq.so"
 SOURCES = ["avq_api.hip", "avq_assign.hip", "avq_aggregate.hip", "avq_attention.hip",
-           "avq_codebook.hip", "avq_order.hip"]
+           "avq_codebook.hip", "avq_order.hip", "avq_pack.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 COMPILE_FLAGS = [

@@ -27,6 +27,9 @@ hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int blo
                             hipStream_t stream);
 long long gilbert_order(int width, int height, int32_t* order);
 template <typename T>
+hipError_t launch_pack(int BH, int M0, int Ch, int D, const float* Vbar, const int32_t* counts,
+                       void* packed, hipStream_t stream);
+template <typename T>
 hipError_t launch_codebook_update(int B, int H, int d, int M0, int Ch, float lam,
                                   const float* sums, const int32_t* counts, float* S,
                                   float* Nema, void* Cp_out, void* Cc_out, hipStream_t stream);
@@ -174,6 +177,23 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
           ? avq::launch_aggregate<avq::bf16>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, s)
           : avq::launch_aggregate<float>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, s);
   return from_hip(e, "avq_aggregate launch");
+}
+
+avq_status_t avq_pack_aggregates(avq_dtype_t dtype, int32_t B, int32_t H, int32_t d,
+                                 int32_t M0, int32_t Ch, const float* Vbar,
+                                 const int32_t* counts, void* packed, void* stream) {
+  avq_status_t st = check_common(dtype, B, H, 1, d, M0, Ch);
+  if (st != AVQ_OK) return st;
+  if (!Vbar || !counts || !packed)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_pack_aggregates: null pointer argument");
+  if (!aligned16(Vbar) || !aligned16(counts) || !aligned16(packed))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_pack_aggregates: arrays must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int BH = B * H;
+  hipError_t e = dtype == AVQ_BF16
+                     ? avq::launch_pack<avq::bf16>(BH, M0, Ch, d, Vbar, counts, packed, s)
+                     : avq::launch_pack<float>(BH, M0, Ch, d, Vbar, counts, packed, s);
+  return from_hip(e, "avq_pack_aggregates launch");
 }
 
 }  // extern "C"

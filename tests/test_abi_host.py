@@ -191,3 +191,23 @@ def test_ordered_attention_validation(L):
     assert ordered(d=96) == UNSUPPORTED
     assert ordered(P=9) == INVALID
 
+
+
+def pack(L, dtype=BF16, B=1, H=1, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 3):
+    return L.avq_pack_aggregates(dtype, B, H, d, M0, Ch, *ptrs, NULL)
+
+
+def test_pack_aggregates_validation(L):
+    for i in range(3):
+        ptrs = [FAKE] * 3
+        ptrs[i] = NULL
+        assert pack(L, ptrs=ptrs) == INVALID
+        assert "null" in L.avq_last_error().decode()
+    assert pack(L, ptrs=(FAKE, ctypes.c_void_p(24), FAKE)) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
+    assert pack(L, dtype=7) == INVALID
+    assert pack(L, B=0) == INVALID
+    assert pack(L, M0=0) == INVALID
+    assert pack(L, d=96) == UNSUPPORTED
+    assert pack(L, Ch=3) == UNSUPPORTED
+    assert pack(L, M0=513) == UNSUPPORTED
