@@ -70,7 +70,11 @@ typedef enum {
   AVQ_ERR_DEVICE = 3       /* the HIP runtime rejected a launch */
 } avq_status_t;
 
-typedef enum { AVQ_F32 = 0, AVQ_BF16 = 1 } avq_dtype_t;
+/* Element type of the dtype arguments. A plain 32-bit integer rather than an
+ * enum type, so that any value a caller passes is well defined on arrival:
+ * values other than these two are rejected with AVQ_ERR_INVALID_ARG. */
+typedef int32_t avq_dtype_t;
+enum { AVQ_F32 = 0, AVQ_BF16 = 1 };
 
 /* Version of this ABI (major * 100 + minor). */
 int avq_version(void);

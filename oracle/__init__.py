@@ -21,6 +21,8 @@ import numpy as np
 _DIR = Path(__file__).resolve().parent
 _SRC = _DIR / "avq_oracle.c"
 _LIB = _DIR / "libavq_oracle.so"
+# AVQ_ORACLE_LIB: an already built copy to load instead (the sanitizer build)
+_LIB_OVERRIDE = os.environ.get("AVQ_ORACLE_LIB")
 _lib = None
 
 _f64p = ctypes.POINTER(ctypes.c_double)
@@ -42,6 +44,9 @@ def build(force: bool = True) -> Path:
 def _load():
     global _lib
     if _lib is None:
+        if _LIB_OVERRIDE:
+            _lib = open_library(_LIB_OVERRIDE)
+            return _lib
         if not _LIB.exists() or _LIB.stat().st_mtime < _SRC.stat().st_mtime:
             build(force=True)
         _lib = open_library(_LIB)

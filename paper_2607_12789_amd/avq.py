@@ -9,12 +9,15 @@ built, every call raises.
 from __future__ import annotations
 
 import ctypes
+import os
 from pathlib import Path
 from typing import Optional
 
 import torch
 
-_LIB_PATH = Path(__file__).resolve().parent / "libavq.so"
+# AVQ_LIB names another build of the same library (a sanitizer build of the
+# host code, for instance); by default the in-tree build is loaded
+_LIB_PATH = Path(os.environ.get("AVQ_LIB") or Path(__file__).resolve().parent / "libavq.so")
 _lib = None
 
 AVQ_OK, AVQ_ERR_INVALID_ARG, AVQ_ERR_UNSUPPORTED, AVQ_ERR_DEVICE = 0, 1, 2, 3
