@@ -5,7 +5,9 @@
     python bench.py --codebook-update [--steps K] [--warmup W]
 
 One step is the whole forward pass over one batch of synthetic inputs
-already resident in HBM: avq_assign -> avq_aggregate -> avq_attention_fwd.
+already resident in HBM: avq_assign_aggregate (the precompute of Alg. 1) ->
+avq_attention_fwd (--unfused-precompute: avq_assign -> avq_aggregate for the
+first).
 The workload is the N = 16384 one (B=2, H=16, d=128, M0=256 parents with 8
 children each, P=32, query block 128, bf16). Prints one JSON line:
 
@@ -93,10 +95,10 @@ class Runner:
     """Device buffers of one workload and its timed step (the three entry
     points on torch's current stream)."""
 
-    def __init__(self, w, x, dev, tiled=False, order=None):
+    def __init__(self, w, x, dev, tiled=False, order=None, fused=True):
         import torch
         from paper_2607_12789_amd import avq
-        self.avq, self.w, self.tiled = avq, w, tiled
+        self.avq, self.w, self.tiled, self.fused = avq, w, tiled, fused
         self.order = None if order is None else order.to(dev)
         self.xd = {k: v.to(dev) for k, v in x.items()}
         B, H, N, d = w.B, w.H, w.N, w.d
@@ -106,34 +108,44 @@ class Runner:
                                   dtype=torch.uint8, device=dev)
         self.counts = torch.empty((B, H, w.Mtot), dtype=torch.int32, device=dev)
         self.Y = torch.empty_like(self.xd["Q"])
+        # the step's entry points in order, each timed by the events around it
+        self.stages = (["assign_aggregate"] if fused else ["assign", "aggregate"]) + \
+            ["attention_fwd"]
 
     def step(self, ev=None):
-        # ev: four events bracketing the three launches (HIP events on the
-        # stream the kernels are launched on, which is torch's current one)
+        # ev: events bracketing the entry points (HIP events on the stream
+        # the kernels are launched on, which is torch's current one)
         avq, w, xd = self.avq, self.w, self.xd
+        k = 0
         if ev: ev[0].record()
-        avq.assign(xd["K"], xd["Cp"], xd["Cc"], self.par, self.code)
-        if ev: ev[1].record()
-        avq.aggregate(xd["V"], self.code, w.M0, w.Ch, self.packed, self.counts)
-        if ev: ev[2].record()
+        if self.fused:
+            avq.assign_aggregate(xd["K"], xd["V"], xd["Cp"], xd["Cc"], self.par, self.code,
+                                 self.packed, self.counts)
+        else:
+            avq.assign(xd["K"], xd["Cp"], xd["Cc"], self.par, self.code)
+            if ev: ev[1].record()
+            avq.aggregate(xd["V"], self.code, w.M0, w.Ch, self.packed, self.counts)
+        k = len(self.stages) - 1
+        if ev: ev[k].record()
         avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], self.packed, w.P, w.block_q, Y=self.Y,
                           tiled_importance=self.tiled, query_order=self.order)
-        if ev: ev[3].record()
+        if ev: ev[k + 1].record()
 
     def timed(self, steps: int, warmup: int):
         """Runs warmup + steps steps; returns (wall ms per step, per-step event
-        durations [steps][3] in ms: assign, aggregate, attention)."""
+        durations [steps][len(stages)] in ms)."""
         import torch
         for _ in range(warmup):
             self.step()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        n = len(self.stages)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(steps)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(steps):
             self.step(evs[i])
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t0) * 1e3 / steps
-        return wall, [[ev[k].elapsed_time(ev[k + 1]) for k in range(3)] for ev in evs]
+        return wall, [[ev[k].elapsed_time(ev[k + 1]) for k in range(n)] for ev in evs]
 
 
 def _median(v):
@@ -167,13 +179,13 @@ def sweep(args):
         r = Runner(w, x, dev)
         wall, per = r.timed(args.steps, args.warmup)
         step_ms = _median([sum(p) for p in per])
-        k = [_median([p[i] for p in per]) for i in range(3)]
+        k = {name: _median([p[i] for p in per]) for i, name in enumerate(r.stages)}
         qh = w.B * w.H * w.N
         row = {"sweep": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "M0": w.M0, "Ch": w.Ch,
                "P": w.P, "block_q": w.block_q, "dtype": w.dtype,
                "codes_precompute": w.M0 * (1 + w.Ch), "codes_attention": w.M0 + w.P * w.Ch,
                "ms_median": step_ms, "ms_wall_mean": wall, "qh_per_s": qh / (step_ms * 1e-3),
-               "kernels_ms_median": {"assign": k[0], "aggregate": k[1], "attention_fwd": k[2]},
+               "kernels_ms_median": k,
                "steps": args.steps, "warmup": args.warmup}
         rows.append(row)
         print(json.dumps(row), flush=True)
@@ -273,6 +285,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also launch one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--unfused-precompute", action="store_true",
+                    help="run the precompute as avq_assign then avq_aggregate instead of the "
+                         "one-pass avq_assign_aggregate")
     ap.add_argument("--tiled-importance", action="store_true",
                     help="use the App. B importance (one parent sweep) instead of the exact one")
     ap.add_argument("--query-order", choices=["token", "gilbert", "random"], default="token",
@@ -319,10 +334,12 @@ def main():
         order = avq.gilbert_order(side, side)[0]
     elif args.query_order == "random":
         order = torch.randperm(w.N, generator=torch.Generator().manual_seed(0)).to(torch.int32)
-    ms_per_step, per = Runner(w, x, dev, args.tiled_importance, order).timed(args.steps,
-                                                                            args.warmup)
-    # per-kernel average launch duration over the timed steps
-    t_assign, t_agg, t_attn = (sum(p[i] for p in per) / max(len(per), 1) for i in range(3))
+    runner = Runner(w, x, dev, args.tiled_importance, order, not args.unfused_precompute)
+    ms_per_step, per = runner.timed(args.steps, args.warmup)
+    # per-entry-point average duration over the timed steps
+    stage_ms = {name: sum(p[i] for p in per) / max(len(per), 1)
+                for i, name in enumerate(runner.stages)}
+    t_attn = stage_ms["attention_fwd"]
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -350,8 +367,11 @@ def main():
         "config": {"workload": f"{w.name}: {w.describe()}", "B": B, "H": H, "N": N, "d": d,
                    "M0": M0, "Ch": Ch, "P": P, "block_q": w.block_q,
                    "importance": "tiled (App. B, 64-parent tiles)" if args.tiled_importance
-                   else "exact", "query_order": args.query_order},
-        "kernels_ms": {"assign": t_assign, "aggregate": t_agg, "attention_fwd": t_attn},
+                   else "exact", "query_order": args.query_order,
+                   "precompute": "avq_assign + avq_aggregate" if args.unfused_precompute
+                   else "avq_assign_aggregate (Alg. 1, one pass)"},
+        "kernels_ms": stage_ms,
+        "ms_per_step_median": _median([sum(p) for p in per]),
         "roofline": {"kernel": ("avq_attention_fwd_ordered" if order is not None else
                                 "avq_attention_fwd_tiled" if args.tiled_importance
                                 else "avq_attention_fwd"), "bound": "mfma", "achieved": achieved,

@@ -148,6 +148,34 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
                            float* Vbar, int32_t* counts, void* packed, void* stream);
 
 /*
+ * avq_assign_aggregate - Alg. 1 as one precompute: the tree quantisation of
+ * avq_assign and the counts and sums of avq_aggregate, with the child compare
+ * and the value sums in one pass over each head's keys (Sec. 4.2: the
+ * aggregates are formed in the same pass that assigns the keys).
+ *
+ * Outputs are those of avq_assign followed by avq_aggregate on its codes:
+ * parent_idx and code_idx exactly (the same compare routine), counts exactly,
+ * Vbar and packed within fp32 summation-order rounding. Two launches: the
+ * parent assignment (it writes parent_idx, which the second launch reads),
+ * then the child compare and aggregation per (batch, head, range of parent
+ * families). Ch = 0 and Ch = 16 run avq_assign's two kernels and then
+ * avq_aggregate's.
+ *
+ *   K, V         [B][H][N][d]   dtype
+ *   Cp           [H][M0][d]     dtype
+ *   Cc           [H][M0][Ch][d] dtype (NULL allowed when Ch = 0)
+ *   parent_idx   [B][H][N]      int32, out
+ *   code_idx     [B][H][N]      int32, out
+ *   Vbar, counts, packed        as for avq_aggregate (Vbar or packed may be
+ *                               NULL, not both)
+ */
+avq_status_t avq_assign_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                                  int32_t d, int32_t M0, int32_t Ch, const void* K,
+                                  const void* V, const void* Cp, const void* Cc,
+                                  int32_t* parent_idx, int32_t* code_idx, float* Vbar,
+                                  int32_t* counts, void* packed, void* stream);
+
+/*
  * avq_pack_aggregates - the aggregates in the form Alg. 2 takes them (its
  * input: the value sum Vbar and the count n of every code, Eq. (aggregates))
  * packed into the operand layout that avq_attention_fwd reads (the packed

@@ -26,7 +26,7 @@ _DTYPES = {torch.float32: AVQ_F32, torch.bfloat16: AVQ_BF16}
 SYMBOLS = ("avq_version", "avq_last_error", "avq_packed_bytes", "avq_assign",
            "avq_aggregate", "avq_attention_fwd", "avq_attention_fwd_tiled",
            "avq_codebook_update", "avq_attention_fwd_ordered", "avq_gilbert_order",
-           "avq_pack_aggregates")
+           "avq_pack_aggregates", "avq_assign_aggregate")
 IMPORTANCE_TILE = 64  # parents per codeword tile of attention_fwd(tiled_importance=True)
 
 
@@ -65,7 +65,10 @@ def lib():
         L.avq_codebook_update.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, ctypes.c_float,
                                           vp, vp, vp, vp, vp, vp, vp]
         L.avq_pack_aggregates.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, vp, vp, vp, vp]
+        L.avq_assign_aggregate.argtypes = [ctypes.c_int, i32, i32, i32, i32, i32, i32,
+                                           vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         for name in ("avq_assign", "avq_aggregate", "avq_attention_fwd", "avq_pack_aggregates",
+                     "avq_assign_aggregate",
                      "avq_attention_fwd_tiled", "avq_codebook_update",
                      "avq_attention_fwd_ordered", "avq_gilbert_order"):
             getattr(L, name).restype = ctypes.c_int
@@ -159,6 +162,43 @@ def aggregate(V, code_idx, M0: int, Ch: int, packed=None, counts=None, Vbar=None
     _check(lib().avq_aggregate(_dtype_code(V), B, H, N, d, M0, Ch, _ptr(V), _ptr(code_idx),
                                _ptr(Vbar), _ptr(counts), _ptr(packed), _stream(stream)))
     return packed, counts, Vbar
+
+
+def assign_aggregate(K, V, Cp, Cc, parent_idx=None, code_idx=None, packed=None, counts=None,
+                     Vbar=None, sums: bool = False, stream=None):
+    """Alg. 1 as one precompute (``avq_assign_aggregate``): the codes of
+    ``assign`` and the aggregates of ``aggregate``, with the child compare and
+    the value sums in one pass. Returns (parent_idx, code_idx, packed, counts,
+    Vbar); Vbar is None unless ``sums`` is set or a buffer is given."""
+    B, H, N, d = K.shape
+    M0, Ch = Cc.shape[1], Cc.shape[2]
+    Mtot = M0 * (1 + Ch)
+    _dev(K, "K")
+    _dev(V, "V", K.dtype, (B, H, N, d))
+    _dev(Cp, "Cp", K.dtype, (H, M0, d))
+    _dev(Cc, "Cc", K.dtype, (H, M0, Ch, d))
+    dev = K.device
+    if parent_idx is None:
+        parent_idx = torch.empty((B, H, N), dtype=torch.int32, device=dev)
+    if code_idx is None:
+        code_idx = torch.empty((B, H, N), dtype=torch.int32, device=dev)
+    E = packed_bytes(K.dtype, M0, Ch, d)
+    if packed is None:
+        packed = torch.empty((B, H, E), dtype=torch.uint8, device=dev)
+    if counts is None:
+        counts = torch.empty((B, H, Mtot), dtype=torch.int32, device=dev)
+    if Vbar is None and sums:
+        Vbar = torch.empty((B, H, Mtot, d), dtype=torch.float32, device=dev)
+    _dev(parent_idx, "parent_idx", torch.int32, (B, H, N))
+    _dev(code_idx, "code_idx", torch.int32, (B, H, N))
+    _dev(packed, "packed", torch.uint8, (B, H, E))
+    _dev(counts, "counts", torch.int32, (B, H, Mtot))
+    if Vbar is not None:
+        _dev(Vbar, "Vbar", torch.float32, (B, H, Mtot, d))
+    _check(lib().avq_assign_aggregate(_dtype_code(K), B, H, N, d, M0, Ch, _ptr(K), _ptr(V),
+                                      _ptr(Cp), _ptr(Cc), _ptr(parent_idx), _ptr(code_idx),
+                                      _ptr(Vbar), _ptr(counts), _ptr(packed), _stream(stream)))
+    return parent_idx, code_idx, packed, counts, Vbar
 
 
 def pack_aggregates(Vbar, counts, M0: int, Ch: int, dtype, packed=None, stream=None):

@@ -26,7 +26,9 @@
 // mean value (sum / count) of every code rounded to the input type, in octets
 // of 8 codes laid out as the attention kernel's MFMA operands, [octet][d][8],
 // with n and ln n per code.
+#include "avq_child.hpp"
 #include "avq_common.hpp"
+#include "avq_launch.hpp"
 #include "avq_packed.hpp"
 
 namespace avq {
@@ -52,6 +54,9 @@ struct AggLds {
   int start[kMaxRows + 1];   // bucket starts
   int cursor[kMaxRows];      // scatter cursors
   int total[kMaxRows];       // keys per row over all flushes (the counts)
+  int fstart[kFamilies + 1];      // fused: family buckets of the queue
+  int fcursor[kFamilies];
+  int item_start[kFamilies + 1];  // fused: first group of 16 keys of each family
   int wave_count[kCodesPerThread][kAggWaves];  // queued keys per (round slot, wave)
   int wave_off[kCodesPerThread][kAggWaves];    // their queue offsets in this round
   int round_total;
@@ -92,13 +97,31 @@ __device__ __forceinline__ void pin_words(R& r) {
 // and the shares are added in a fixed order at the end. More than one for
 // heads with many keys per parent, where one half wave's chain of loads
 // would set the time.
-template <typename T, int D, int CHM, int SPLIT>
+//
+// FUSED (the child compare of Alg. 1 inside the same pass, Ch >= 1): the
+// input is the parent index of every key instead of its code. Each flush
+// first buckets the queued keys by family, then the waves take groups of 16
+// keys of one family and run the child compare on them (the key rows are
+// read here; the candidate rows stay in registers while a wave's groups share
+// the family), write the code of every key and re-queue the keys with their
+// rows; the flush then goes on as above. Keys, and so the K rows, are read
+// once per head; no code round trip between two kernels.
+struct FusedArgs {
+  const void* K;   // [B][H][N][d]
+  const void* Cp;  // [H][M0][d]
+  const void* Cc;  // [H][M0][Ch][d]
+  int32_t* code_idx;  // out: [B][H][N]
+  int H;
+};
+
+template <typename T, int D, int CHM, int SPLIT, bool FUSED>
 __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restrict__ V,
                                                                 const int32_t* __restrict__ code_idx,
                                                                 float* __restrict__ Vbar,
                                                                 int32_t* __restrict__ counts,
                                                                 unsigned char* __restrict__ packed,
-                                                                int N, int M0, int Ch, int ranges) {
+                                                                int N, int M0, int Ch, int ranges,
+                                                                FusedArgs fa) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   AggLds& L = *reinterpret_cast<AggLds*>(lds_raw);
   constexpr int CPL = D / kFamLanes;  // columns per lane
@@ -118,8 +141,9 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
 
   for (int r = tid; r < kMaxRows; r += kAggThreads) L.total[r] = 0;
 
-  const int32_t* codes = code_idx + (size_t)bh * N;
+  const int32_t* codes = code_idx + (size_t)bh * N;  // FUSED: parent indices
   const T* vhead = V + (size_t)bh * N * D;
+  static_assert(!FUSED || CHM == 8, "the fused child compare holds one 16-row candidate tile");
 
   // the family table of this half wave: row 0 = stay, row 1 + c = child c
   float acc[1 + CHM][CPL];
@@ -127,6 +151,107 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   for (int r = 0; r <= CHM; ++r)
 #pragma unroll
     for (int i = 0; i < CPL; ++i) acc[r][i] = 0.f;
+
+  // FUSED: the queue holds (key, family); bucket it by family, compare each
+  // group of 16 keys with its family's candidates, and leave the queue as
+  // (key, row) in family order, the code of every key written
+  auto child_step = [&](int qlen) {
+    constexpr int NT = 1;
+    using CT = ChildTile<T, D, NT>;
+    constexpr int KQ = CT::KQ;
+    using Frag = typename CT::Frag;
+    // at d = 64 the next group's key fragments stay in flight; at d = 128
+    // they load when they are used (the family table, the candidate rows and
+    // two sets of key fragments would pass the 128 registers of a lane)
+    constexpr bool kPrefetch = D == 64;
+    const int h = bh % fa.H;
+    const T* kh = static_cast<const T*>(fa.K) + (size_t)bh * N * D;
+    if (tid < kFamilies) L.hist[tid] = 0;
+    __syncthreads();
+    for (int e = tid; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
+    __syncthreads();
+    if (wave == 0) {  // family starts and group starts (nfam <= 32 lanes)
+      const int v = lane < nfam ? L.hist[lane] : 0;
+      const int gv = (v + 15) / 16;
+      int incl = v, gincl = gv;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        const int gy = __shfl_up(gincl, off, kWave);
+        if (lane >= off) {
+          incl += y;
+          gincl += gy;
+        }
+      }
+      if (lane < nfam) {
+        L.fstart[lane] = incl - v;
+        L.fcursor[lane] = incl - v;
+        L.item_start[lane] = gincl - gv;
+      }
+      if (lane == nfam - 1) {
+        L.fstart[nfam] = incl;
+        L.item_start[nfam] = gincl;
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < qlen; e += kAggThreads)
+      L.skey[atomicAdd(&L.fcursor[L.qrow[e]], 1)] = L.qkey[e];
+    __syncthreads();
+    // each wave a contiguous run of groups (consecutive groups mostly share
+    // the family, whose candidate rows stay in registers)
+    const int g = lane / 16, c = lane % 16;
+    const int n_items = L.item_start[nfam];
+    const int per_wave = (n_items + kAggWaves - 1) / kAggWaves;
+    const int it_begin = wave * per_wave, it_end = min(n_items, it_begin + per_wave);
+    auto group_keys = [&](int f, int it, Frag (&kf)[KQ], int& pos, bool& valid) {
+      const int kb = L.fstart[f] + 16 * (it - L.item_start[f]);
+      valid = kb + c < L.fstart[f + 1];
+      pos = valid ? kb + c : kb;
+      child_key<T, D, NT>(kh + (size_t)L.skey[pos] * D, g, kf);
+    };
+    Frag cf[NT][KQ];
+    f32x4 cn[NT];
+    Frag kf[KQ];
+    int cur_f = -1, f = 0, pos = 0;
+    bool valid = false;
+    if (it_begin < it_end) {
+      while (L.item_start[f + 1] <= it_begin) ++f;  // wave-uniform
+      group_keys(f, it_begin, kf, pos, valid);
+    }
+    for (int it = it_begin; it < it_end; ++it) {
+      Frag kn[KQ];
+      int fn = f, pos_n = 0;
+      bool valid_n = false;
+      if (it + 1 < it_end) {
+        while (L.item_start[fn + 1] <= it + 1) ++fn;  // wave-uniform
+        if constexpr (kPrefetch) group_keys(fn, it + 1, kn, pos_n, valid_n);
+      }
+      if constexpr (!kPrefetch) {
+        if (it > it_begin) group_keys(f, it, kf, pos, valid);
+      }
+      const int p = p0 + f;
+      if (f != cur_f) {
+        child_rows<T, D, NT>(static_cast<const T*>(fa.Cp), static_cast<const T*>(fa.Cc), h, M0,
+                             Ch, p, g, c, cf, cn);
+        cur_f = f;
+      }
+      const int r = child_pick<T, D, NT>(cf, cn, kf, Ch, g, c);
+      if (g == 0 && valid) {
+        const int key = L.skey[pos];
+        fa.code_idx[(size_t)bh * N + key] = r > 0 ? M0 + p * Ch + r - 1 : p;
+        L.qkey[pos] = key;
+        L.qrow[pos] = (uint16_t)(f * (1 + Ch) + r);
+      }
+      if constexpr (kPrefetch) {
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) kf[kq] = kn[kq];
+        pos = pos_n;
+        valid = valid_n;
+      }
+      f = fn;
+    }
+    __syncthreads();
+  };
 
   // 1. scan the head's codes and queue the keys of this range; bucket and
   //    sum the queue when it would overflow and once the codes are exhausted
@@ -147,7 +272,9 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       for (int k = 0; k < kCodesPerThread; ++k) {
         const int code = next[k];
         row[k] = -1;
-        if (code >= 0 && code < Mtot) {
+        if constexpr (FUSED) {  // the family; its row comes from the child compare
+          if (code >= p0 && code < p0 + nfam) row[k] = code - p0;
+        } else if (code >= 0 && code < Mtot) {
           // Ch is a power of two: child code M0 + p Ch + c
           const int p = code < M0 ? code : (code - M0) >> ch_shift;
           if (p >= p0 && p < p0 + nfam)
@@ -176,6 +303,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
     // uniform across the workgroup
     const bool flush = done ? qlen > 0 : qlen + round_total > kQueueCap;
     if (flush) {
+      if constexpr (FUSED) child_step(qlen);
       for (int r = tid; r < rows; r += kAggThreads) L.hist[r] = 0;
       __syncthreads();
       for (int e = tid; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
@@ -470,10 +598,10 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   }
 }
 
-template <typename T, int D, int CHM, int SPLIT>
+template <typename T, int D, int CHM, int SPLIT, bool FUSED>
 hipError_t launch_aggregate_dcs(int BH, int N, int M0, int Ch, const void* V,
                                 const int32_t* code_idx, float* Vbar, int32_t* counts,
-                                void* packed, hipStream_t stream) {
+                                void* packed, const FusedArgs& fa, hipStream_t stream) {
   // one range of kFamilies / SPLIT parents per workgroup: ranges start at
   // multiples of 8 parents, so each packed octet of parent means is written
   // by one workgroup
@@ -484,15 +612,17 @@ hipError_t launch_aggregate_dcs(int BH, int N, int M0, int Ch, const void* V,
   const int lds = (int)sizeof(AggLds);
   constexpr int chm_i = CHM == 0 ? 0 : CHM == 8 ? 1 : 2;
   constexpr int split_i = SPLIT == 1 ? 0 : SPLIT == 2 ? 1 : 2;
-  constexpr int slot =
-      64 + (((Elem<T>::kBf16 ? 0 : 1) * 2 + (D == 128 ? 1 : 0)) * 3 + chm_i) * 3 + split_i;
-  hipError_t e = ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM, SPLIT>, lds, slot);
+  constexpr int slot = (FUSED ? 128 : 64) +
+                       (((Elem<T>::kBf16 ? 0 : 1) * 2 + (D == 128 ? 1 : 0)) * 3 + chm_i) * 3 +
+                       split_i;
+  hipError_t e =
+      ensure_dynamic_lds((const void*)aggregate_kernel<T, D, CHM, SPLIT, FUSED>, lds, slot);
   if (e != hipSuccess) return e;
   const long long grid = (long long)BH * ranges;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((aggregate_kernel<T, D, CHM, SPLIT>), dim3((unsigned)grid), dim3(kAggThreads),
-                     lds, stream, static_cast<const T*>(V), code_idx, Vbar, counts,
-                     static_cast<unsigned char*>(packed), N, M0, Ch, ranges);
+  hipLaunchKernelGGL((aggregate_kernel<T, D, CHM, SPLIT, FUSED>), dim3((unsigned)grid),
+                     dim3(kAggThreads), lds, stream, static_cast<const T*>(V), code_idx, Vbar,
+                     counts, static_cast<unsigned char*>(packed), N, M0, Ch, ranges, fa);
   return hipGetLastError();
 }
 
@@ -502,10 +632,10 @@ hipError_t launch_aggregate_dcs(int BH, int N, int M0, int Ch, const void* V,
 // chain of value loads (at least 256 keys per parent) while fewer than half
 // the CUs have a workgroup (few heads, few parents). Then the fewest half
 // waves (2 or 4) that give half the CUs a workgroup.
-template <typename T, int D, int CHM>
+template <typename T, int D, int CHM, bool FUSED>
 hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
                                const int32_t* code_idx, float* Vbar, int32_t* counts,
-                               void* packed, hipStream_t stream) {
+                               void* packed, const FusedArgs& fa, hipStream_t stream) {
   DeviceInfo dev;
   hipError_t e = device_info(&dev);
   if (e != hipSuccess) return e;
@@ -516,25 +646,29 @@ hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
   };
   const bool long_chains = (long long)N >= 256LL * M0;
   if (!long_chains || grid(1) >= half_cus)
-    return launch_aggregate_dcs<T, D, CHM, 1>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
-                                              stream);
+    return launch_aggregate_dcs<T, D, CHM, 1, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
+                                                     packed, fa, stream);
   if (grid(2) >= half_cus)
-    return launch_aggregate_dcs<T, D, CHM, 2>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
-                                              stream);
-  return launch_aggregate_dcs<T, D, CHM, 4>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
-                                            stream);
+    return launch_aggregate_dcs<T, D, CHM, 2, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
+                                                     packed, fa, stream);
+  return launch_aggregate_dcs<T, D, CHM, 4, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
+                                                   packed, fa, stream);
 }
 
 template <typename T, int D>
 hipError_t launch_aggregate_d(int BH, int N, int M0, int Ch, const void* V,
                               const int32_t* code_idx, float* Vbar, int32_t* counts,
                               void* packed, hipStream_t stream) {
+  const FusedArgs none{};
   if (Ch == 0)  // flat codebook: a family is one parent
-    return launch_aggregate_dc<T, D, 0>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
+    return launch_aggregate_dc<T, D, 0, false>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
+                                               none, stream);
   if (Ch <= 8)
-    return launch_aggregate_dc<T, D, 8>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
+    return launch_aggregate_dc<T, D, 8, false>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed,
+                                               none, stream);
   if (Ch <= 16)
-    return launch_aggregate_dc<T, D, 16>(BH, N, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
+    return launch_aggregate_dc<T, D, 16, false>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
+                                                packed, none, stream);
   return hipErrorInvalidValue;
 }
 
@@ -549,9 +683,46 @@ hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
   return hipErrorInvalidValue;
 }
 
+// Alg. 1 in two launches: the parent assignment (it reads K once and writes
+// parent_idx), then the fused child compare + aggregation (bf16, 1 <= Ch <=
+// 8). Ch = 0 (the parent is the code), Ch = 16 (two candidate tiles) and fp32
+// (its fragments, the family table and the candidate rows pass the registers
+// of a 1024-thread workgroup) take the parent and child kernels of the
+// assignment and then the plain aggregation.
+template <typename T>
+hipError_t launch_assign_aggregate(int BH, int H, int N, int d, int M0, int Ch, const void* K,
+                                   const void* V, const void* Cp, const void* Cc,
+                                   int32_t* parent_idx, int32_t* code_idx, float* Vbar,
+                                   int32_t* counts, void* packed, hipStream_t stream) {
+  const bool fused = Elem<T>::kBf16 && Ch >= 1 && Ch <= 8;
+  hipError_t e = d == 64 ? launch_assign<T, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx,
+                                                !fused, stream)
+                         : launch_assign<T, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx,
+                                                 code_idx, !fused, stream);
+  if (e != hipSuccess) return e;
+  if (!fused) return launch_aggregate<T>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, stream);
+  FusedArgs fa{K, Cp, Cc, code_idx, H};
+  if constexpr (Elem<T>::kBf16) {
+    if (d == 64)
+      return launch_aggregate_dc<T, 64, 8, true>(BH, N, M0, Ch, V, parent_idx, Vbar, counts,
+                                                 packed, fa, stream);
+    return launch_aggregate_dc<T, 128, 8, true>(BH, N, M0, Ch, V, parent_idx, Vbar, counts,
+                                                packed, fa, stream);
+  }
+  return hipErrorInvalidValue;  // not reached: fp32 takes the unfused path
+}
+
 template hipError_t launch_aggregate<bf16>(int, int, int, int, int, const void*, const int32_t*,
                                            float*, int32_t*, void*, hipStream_t);
 template hipError_t launch_aggregate<float>(int, int, int, int, int, const void*, const int32_t*,
                                             float*, int32_t*, void*, hipStream_t);
+template hipError_t launch_assign_aggregate<bf16>(int, int, int, int, int, int, const void*,
+                                                  const void*, const void*, const void*,
+                                                  int32_t*, int32_t*, float*, int32_t*, void*,
+                                                  hipStream_t);
+template hipError_t launch_assign_aggregate<float>(int, int, int, int, int, int, const void*,
+                                                   const void*, const void*, const void*,
+                                                   int32_t*, int32_t*, float*, int32_t*, void*,
+                                                   hipStream_t);
 
 }  // namespace avq

@@ -10,35 +10,12 @@
 #include "avq_common.hpp"
 #include "avq_packed.hpp"
 
-namespace avq {
-template <typename T, int D>
-hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, const void* Cp,
-                         const void* Cc, int32_t* parent_idx, int32_t* code_idx,
-                         hipStream_t stream);
-template <typename T>
-hipError_t launch_aggregate(int BH, int N, int d, int M0, int Ch, const void* V,
-                            const int32_t* code_idx, float* Vbar, int32_t* counts, void* packed,
-                            hipStream_t stream);
-template <typename T, int D>
-hipError_t launch_attention(int BH, int H, int N, int M0, int Ch, int P, int block_q,
-                            const void* Q, const void* Cp, const void* Cc, const void* packed,
-                            void* Y, int32_t* topp_idx,
-                            float* importance, bool tiled, const int32_t* order,
-                            hipStream_t stream);
-long long gilbert_order(int width, int height, int32_t* order);
-template <typename T>
-hipError_t launch_pack(int BH, int M0, int Ch, int D, const float* Vbar, const int32_t* counts,
-                       void* packed, hipStream_t stream);
-template <typename T>
-hipError_t launch_codebook_update(int B, int H, int d, int M0, int Ch, float lam,
-                                  const float* sums, const int32_t* counts, float* S,
-                                  float* Nema, void* Cp_out, void* Cc_out, hipStream_t stream);
-}  // namespace avq
+#include "avq_launch.hpp"
 
 namespace avq {
 
 constexpr int kMaxDevices = 64;
-constexpr int kMaxSlots = 128;
+constexpr int kMaxSlots = 256;
 
 hipError_t device_info(DeviceInfo* out) {
   static DeviceInfo cache[kMaxDevices];
@@ -150,11 +127,11 @@ avq_status_t avq_assign(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, int3
   const int BH = B * H;
   hipError_t e;
   if (dtype == AVQ_BF16)
-    e = d == 64 ? avq::launch_assign<avq::bf16, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s)
-                : avq::launch_assign<avq::bf16, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s);
+    e = d == 64 ? avq::launch_assign<avq::bf16, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, true, s)
+                : avq::launch_assign<avq::bf16, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, true, s);
   else
-    e = d == 64 ? avq::launch_assign<float, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s)
-                : avq::launch_assign<float, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, s);
+    e = d == 64 ? avq::launch_assign<float, 64>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, true, s)
+                : avq::launch_assign<float, 128>(BH, H, N, M0, Ch, K, Cp, Cc, parent_idx, code_idx, true, s);
   return from_hip(e, "avq_assign launch");
 }
 
@@ -177,6 +154,32 @@ avq_status_t avq_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N, i
           ? avq::launch_aggregate<avq::bf16>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, s)
           : avq::launch_aggregate<float>(BH, N, d, M0, Ch, V, code_idx, Vbar, counts, packed, s);
   return from_hip(e, "avq_aggregate launch");
+}
+
+avq_status_t avq_assign_aggregate(avq_dtype_t dtype, int32_t B, int32_t H, int32_t N,
+                                  int32_t d, int32_t M0, int32_t Ch, const void* K,
+                                  const void* V, const void* Cp, const void* Cc,
+                                  int32_t* parent_idx, int32_t* code_idx, float* Vbar,
+                                  int32_t* counts, void* packed, void* stream) {
+  avq_status_t st = check_common(dtype, B, H, N, d, M0, Ch);
+  if (st != AVQ_OK) return st;
+  if (!K || !V || !Cp || (!Cc && Ch > 0) || !parent_idx || !code_idx || !counts)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_assign_aggregate: null pointer argument");
+  if (!Vbar && !packed)
+    return fail(AVQ_ERR_INVALID_ARG, "avq_assign_aggregate: Vbar and packed are both null");
+  if (!aligned16(K) || !aligned16(V) || !aligned16(Cp) || !aligned16(Cc) ||
+      !aligned16(parent_idx) || !aligned16(code_idx) || !aligned16(Vbar) || !aligned16(counts) ||
+      !aligned16(packed))
+    return fail(AVQ_ERR_INVALID_ARG, "avq_assign_aggregate: arrays must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int BH = B * H;
+  hipError_t e =
+      dtype == AVQ_BF16
+          ? avq::launch_assign_aggregate<avq::bf16>(BH, H, N, d, M0, Ch, K, V, Cp, Cc, parent_idx,
+                                                    code_idx, Vbar, counts, packed, s)
+          : avq::launch_assign_aggregate<float>(BH, H, N, d, M0, Ch, K, V, Cp, Cc, parent_idx,
+                                                code_idx, Vbar, counts, packed, s);
+  return from_hip(e, "avq_assign_aggregate launch");
 }
 
 avq_status_t avq_pack_aggregates(avq_dtype_t dtype, int32_t B, int32_t H, int32_t d,

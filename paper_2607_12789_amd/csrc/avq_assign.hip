@@ -31,6 +31,7 @@
 // routine, so a child equal to its parent has exactly the parent's distance.
 // The nearest child (strict <, lowest index) replaces the parent only if its
 // distance is strictly smaller.
+#include "avq_child.hpp"
 #include "avq_common.hpp"
 
 #include <algorithm>
@@ -71,31 +72,6 @@ struct AssignCfg {
   static constexpr int LDS_BYTES = 2 * BUF_BYTES + M0MAX * 4;  // two chunks + all norms
   static_assert(COPIES % kWaves == 0, "copies split evenly over the waves");
 };
-
-// Sum of squares of the 8 (bf16) or 1 (fp32) values of a fragment, in order.
-template <typename T>
-__device__ __forceinline__ float frag_sq(const typename std::conditional<Elem<T>::kBf16, bf16x8, float>::type& v,
-                                         float acc) {
-  if constexpr (Elem<T>::kBf16) {
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-      const bf16x2 p = {v[i], v[i + 1]};
-      acc = __builtin_amdgcn_fdot2_f32_bf16(p, p, acc, false);
-    }
-    return acc;
-  } else {
-    return fmaf(v, v, acc);
-  }
-}
-
-// -2 x, exactly (a power-of-two scale)
-__device__ __forceinline__ bf16x8 times_minus2(const bf16x8& v) {
-  bf16x8 r;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = (bf16)(-2.f * (float)v[i]);
-  return r;
-}
-__device__ __forceinline__ float times_minus2(float v) { return -2.f * v; }
 
 // ||row||^2 of a codebook row in one fixed order (consecutive pairs of d)
 template <typename T, int D>
@@ -512,61 +488,12 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
   Frag cf[NT][KQ];
   f32x4 cn[NT];
 
-  // candidate rows of a family (A operand): lane (g, c) holds row c of each
-  // tile; row 0 = the parent, row 1 + j = child j (rows past Ch repeat the
-  // last child and are ignored)
-  auto load_rows = [&](int p, Frag (&cf)[NT][KQ]) {
-#pragma unroll
-    for (int t2 = 0; t2 < NT; ++t2) {
-      {
-        const int cand = 16 * t2 + c;
-        const T* row = cand == 0 ? Cp + ((size_t)h * M0 + p) * D
-                                 : Cc + (((size_t)h * M0 + p) * Ch + min(cand - 1, Ch - 1)) * D;
-#pragma unroll
-        for (int kq = 0; kq < KQ; ++kq) {
-          if constexpr (kB)
-            cf[t2][kq] = *reinterpret_cast<const bf16x8*>(row + 32 * kq + 8 * g);
-          else
-            cf[t2][kq] = row[4 * kq + g];
-        }
-      }
-    }
-  };
-  // ||c||^2 of the lane's rows 4 g + r of each tile: each lane sums its
-  // quarter of row c in order, the quarters are combined in a fixed order,
-  // then the rows are moved to the lanes that hold their products. The rows
-  // are then scaled by -2 (exact), so that the product accumulated onto
-  // ||c||^2 is the distance.
-  auto row_norms = [&](Frag (&cf)[NT][KQ], f32x4 (&cn)[NT]) {
-#pragma unroll
-    for (int t2 = 0; t2 < NT; ++t2) {
-      {
-        float part = 0.f;
-#pragma unroll
-        for (int kq = 0; kq < KQ; ++kq) part = frag_sq<T>(cf[t2][kq], part);
-        const float p01 = part + shfl_xor(part, 16);
-        const float p23 = shfl_xor(p01, 32);
-        const float nrm = (g < 2) ? p01 + p23 : p23 + p01;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) cn[t2][r] = __shfl(nrm, 4 * g + r, kWave);
-#pragma unroll
-        for (int kq = 0; kq < KQ; ++kq) cf[t2][kq] = times_minus2(cf[t2][kq]);
-      }
-    }
-  };
   // the 16 keys of group it (B operand); key index of lane c
   auto load_keys = [&](int f, int it, Frag (&kf)[KQ], int& key, bool& valid) {
     const int kb = L.start[f] + 16 * (it - L.item_start[f]);
     valid = kb + c < L.start[f + 1];
     key = L.skey[valid ? kb + c : kb];
-    const T* krow = kh + (size_t)key * D;
-#pragma unroll
-    for (int kq = 0; kq < KQ; ++kq) {
-      if constexpr (kB)
-        kf[kq] = *reinterpret_cast<const bf16x8*>(krow + 32 * kq + 8 * g);
-      else
-        kf[kq] = krow[4 * kq + g];
-    }
+    child_key<T, D, NT>(kh + (size_t)key * D, g, kf);
   };
 
   for (int base = kbegin; base < kend; base += kChildRound) {
@@ -663,49 +590,11 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
         if (it > it_begin) load_keys(f, it, kf, key, valid);
       }
       if (p != cur_fam) {
-        load_rows(p, cf);
-        row_norms(cf, cn);
+        child_rows<T, D, NT>(Cp, Cc, h, M0, Ch, p, g, c, cf, cn);
         cur_fam = p;
       }
-      // distances (accumulators start at ||c||^2, rows enter as -2 c)
-      float dpar = 0.f, dch = __builtin_inff();
-      int cbest = 0;
-#pragma unroll
-      for (int t2 = 0; t2 < NT; ++t2) {
-        {
-          f32x4 acc = cn[t2];
-#pragma unroll
-          for (int kq = 0; kq < KQ; ++kq) {
-            if constexpr (kB)
-              acc = mfma_bf16(cf[t2][kq], kf[kq], acc);
-            else
-              acc = mfma_f32(cf[t2][kq], kf[kq], acc);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int cand = 16 * t2 + 4 * g + r;
-            if (cand == 0) dpar = acc[r];
-            if (cand >= 1 && cand <= Ch && acc[r] < dch) {
-              dch = acc[r];
-              cbest = cand - 1;
-            }
-          }
-        }
-      }
-      // merge the lane groups: parent distance from group 0, children by
-      // lexicographic (distance, child) minimum
-      dpar = __shfl(dpar, c, kWave);
-#pragma unroll
-      for (int m = 16; m <= 32; m <<= 1) {
-        const float ob = shfl_xor(dch, m);
-        const int oi = shfl_xor(cbest, m);
-        if (ob < dch || (ob == dch && oi < cbest)) {
-          dch = ob;
-          cbest = oi;
-        }
-      }
-      if (g == 0 && valid)
-        code_idx[(size_t)bh * N + key] = (dch < dpar) ? (M0 + p * Ch + cbest) : p;
+      const int row = child_pick<T, D, NT>(cf, cn, kf, Ch, g, c);
+      if (g == 0 && valid) code_idx[(size_t)bh * N + key] = row > 0 ? M0 + p * Ch + row - 1 : p;
 #pragma unroll
       for (int kq = 0; kq < KQ; ++kq) kf[kq] = kn[kq];
       key = key_n;
@@ -719,7 +608,7 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
 template <typename T, int D>
 hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, const void* Cp,
                          const void* Cc, int32_t* parent_idx, int32_t* code_idx,
-                         hipStream_t stream) {
+                         bool with_children, hipStream_t stream) {
   using Cfg = AssignCfg<T, D>;
   using SCfg = StreamCfg<T, D>;
   long long grid;
@@ -758,6 +647,7 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (Ch == 0) return hipSuccess;  // flat codebook: the parent is the code
+  if (!with_children) return hipSuccess;  // the caller runs the child compare
 
   // child compare: F parents per workgroup, and the keys split into chunks
   // of one scan round each (the keys are independent: a workgroup scans only
@@ -785,12 +675,12 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
 }
 
 template hipError_t launch_assign<bf16, 64>(int, int, int, int, int, const void*, const void*,
-                                            const void*, int32_t*, int32_t*, hipStream_t);
+                                            const void*, int32_t*, int32_t*, bool, hipStream_t);
 template hipError_t launch_assign<bf16, 128>(int, int, int, int, int, const void*, const void*,
-                                             const void*, int32_t*, int32_t*, hipStream_t);
+                                             const void*, int32_t*, int32_t*, bool, hipStream_t);
 template hipError_t launch_assign<float, 64>(int, int, int, int, int, const void*, const void*,
-                                             const void*, int32_t*, int32_t*, hipStream_t);
+                                             const void*, int32_t*, int32_t*, bool, hipStream_t);
 template hipError_t launch_assign<float, 128>(int, int, int, int, int, const void*, const void*,
-                                              const void*, int32_t*, int32_t*, hipStream_t);
+                                              const void*, int32_t*, int32_t*, bool, hipStream_t);
 
 }  // namespace avq

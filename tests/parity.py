@@ -48,12 +48,17 @@ def to_gpu(x: dict) -> dict:
     return {k: v.cuda() for k, v in x.items()}
 
 
-def gpu_forward(xd: dict, w, tiled: bool = False, query_order=None) -> dict:
-    """Runs the three entry points and returns every output on the CPU
-    (tiled: the App. B importance entry point; query_order: the ordered entry
-    point, with Y returned in query order)."""
-    par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
-    packed, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
+def gpu_forward(xd: dict, w, tiled: bool = False, query_order=None, fused: bool = True) -> dict:
+    """Runs the precompute and the attention and returns every output on the
+    CPU (fused: the one-pass precompute avq_assign_aggregate, else avq_assign
+    then avq_aggregate; tiled: the App. B importance entry point;
+    query_order: the ordered entry point, with Y returned in query order)."""
+    if fused:
+        par, code, packed, counts, Vbar = avq.assign_aggregate(xd["K"], xd["V"], xd["Cp"],
+                                                               xd["Cc"], sums=True)
+    else:
+        par, code = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+        packed, counts, Vbar = avq.aggregate(xd["V"], code, w.M0, w.Ch, sums=True)
     order = None if query_order is None else torch.as_tensor(query_order, dtype=torch.int32).cuda()
     Y, topp, imp = avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], packed, w.P, w.block_q,
                                      debug=True, tiled_importance=tiled, query_order=order)
@@ -330,7 +335,7 @@ def oracle_on_gpu_codes(x, w, g, mask, recovered, importance_tile) -> dict:
 
 
 def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False,
-            query_order=None) -> dict:
+            query_order=None, fused=True) -> dict:
     """Runs GPU and oracle on the same inputs and checks every output.
 
     tiles_per_head: number of query tiles per head evaluated by the oracle
@@ -338,7 +343,7 @@ def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False,
     App. B importance on both sides (tiles of avq.IMPORTANCE_TILE parents).
     query_order: the GPU takes the queries in this order; the oracle gets Q
     with its rows permuted the same way, and the GPU's Y is compared in that
-    order."""
+    order. fused: which precompute the GPU runs (see gpu_forward)."""
     T = w.n_tiles
     mask = np.ones((w.B, w.H, T), np.uint8)
     if tiles_per_head is not None and tiles_per_head < T:
@@ -349,7 +354,7 @@ def compare(x, w, tiles_per_head=None, seed=0, recovered=True, tiled=False,
                 pick = rng.choice(T, tiles_per_head, replace=False)
                 mask[b, h, pick] = 1
                 mask[b, h, [0, T - 1]] = 1
-    g = gpu_forward(to_gpu(x), w, tiled, query_order)
+    g = gpu_forward(to_gpu(x), w, tiled, query_order, fused)
     if query_order is not None:
         x = dict(x, Q=x["Q"][:, :, torch.as_tensor(query_order, dtype=torch.long)].contiguous())
     itile = avq.IMPORTANCE_TILE if tiled else None

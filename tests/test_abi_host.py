@@ -211,3 +211,35 @@ def test_pack_aggregates_validation(L):
     assert pack(L, d=96) == UNSUPPORTED
     assert pack(L, Ch=3) == UNSUPPORTED
     assert pack(L, M0=513) == UNSUPPORTED
+
+
+def assign_aggregate(L, dtype=BF16, B=1, H=1, N=8, d=64, M0=4, Ch=2, ptrs=(FAKE,) * 9):
+    return L.avq_assign_aggregate(dtype, B, H, N, d, M0, Ch, *ptrs, NULL)
+
+
+def test_assign_aggregate_validation(L):
+    # K, V, Cp, Cc, parent_idx, code_idx, Vbar, counts, packed: each required
+    # one null at a time (Vbar and packed may each be null, not both; Cc only
+    # when Ch = 0)
+    # (a call that passes validation would launch: every call here fails it)
+    names = ["K", "V", "Cp", "Cc", "parent_idx", "code_idx", "Vbar", "counts", "packed"]
+    for i, name in enumerate(names):
+        if name in ("Vbar", "packed"):
+            continue
+        ptrs = [FAKE] * 9
+        ptrs[i] = NULL
+        assert assign_aggregate(L, ptrs=ptrs) == INVALID, name
+        assert "null" in L.avq_last_error().decode()
+    ptrs = [FAKE] * 9
+    ptrs[6] = ptrs[8] = NULL
+    assert assign_aggregate(L, ptrs=ptrs) == INVALID
+    assert "both null" in L.avq_last_error().decode()
+    ptrs = [FAKE] * 9
+    ptrs[1] = ctypes.c_void_p(24)
+    assert assign_aggregate(L, ptrs=ptrs) == INVALID
+    assert "aligned" in L.avq_last_error().decode()
+    assert assign_aggregate(L, dtype=7) == INVALID
+    assert assign_aggregate(L, N=0) == INVALID
+    assert assign_aggregate(L, d=96) == UNSUPPORTED
+    assert assign_aggregate(L, Ch=3) == UNSUPPORTED
+    assert assign_aggregate(L, M0=513) == UNSUPPORTED

@@ -1,8 +1,8 @@
 """Parity of the HIP path (through the C ABI) with the fp64 oracle.
 
-Every case draws seeded inputs, runs avq_assign -> avq_aggregate ->
-avq_attention_fwd on the GPU and the oracle on the CPU, and compares (see
-tests/parity.py): assignments, counts and top-P sets exactly on certified
+Every case draws seeded inputs, runs the precompute (avq_assign_aggregate,
+or avq_assign -> avq_aggregate) and avq_attention_fwd on the GPU and the
+oracle on the CPU, and compares (see tests/parity.py): assignments, counts and top-P sets exactly on certified
 decisions, Vbar within the fp32 summation bound, importance within eps_w,
 and Y per row within 1e-4 (fp32) / 2e-2 (bf16) relative to max|Y*|.
 
@@ -104,6 +104,55 @@ def test_edge_case(name):
     x = inputs.generate(w)
     res = parity.compare(x, w)
     report(res)
+
+
+# the two-kernel precompute (avq_assign, then avq_aggregate) on cases that
+# cover its paths; every other case runs the fused one
+UNFUSED = ["ragged_n", "ch1", "ch2", "m0_37_ch16_d128", "fp32_d128", "m0_512_bq256",
+           "agg_split4", "agg_queue_overflow", "flat", "dirichlet_sparse"]
+
+
+@pytest.mark.parametrize("name", UNFUSED)
+def test_edge_case_unfused(name):
+    w = EDGE[name]
+    banner(name + " (unfused)", w)
+    res = parity.compare(inputs.generate(w), w, fused=False)
+    report(res)
+
+
+@pytest.mark.parametrize("name", ["ragged_n", "ch1", "ch2", "ch8_bq200", "m0_512_bq256",
+                                  "agg_split2", "agg_split4", "agg_queue_overflow",
+                                  "dirichlet_sparse", "keys_stay", "large_logits"])
+def test_fused_equals_unfused(name):
+    """avq_assign_aggregate gives avq_assign's indices and avq_aggregate's
+    counts exactly (the same child compare routine on the same inputs), and
+    the sums within fp32 summation-order rounding: each is a sum of the same
+    values, so |a - b| <= 2 gamma_n sum |v| per element."""
+    from paper_2607_12789_amd import avq
+    w = EDGE[name]
+    banner(name + " (fused vs unfused)", w)
+    xd = parity.to_gpu(inputs.generate(w))
+    p1, c1, pk1, n1, vb1 = avq.assign_aggregate(xd["K"], xd["V"], xd["Cp"], xd["Cc"], sums=True)
+    p2, c2 = avq.assign(xd["K"], xd["Cp"], xd["Cc"])
+    pk2, n2, vb2 = avq.aggregate(xd["V"], c2, w.M0, w.Ch, sums=True)
+    torch.cuda.synchronize()
+    assert torch.equal(p1, p2) and torch.equal(c1, c2) and torch.equal(n1, n2)
+    # |v| summed per code with the GPU's codes (fp64 on the CPU)
+    V = xd["V"].double().cpu()
+    code = c1.long().cpu()
+    Mtot = w.M0 * (1 + w.Ch)
+    absum = torch.zeros((w.B, w.H, Mtot, w.d), dtype=torch.float64)
+    absum.scatter_add_(2, code[..., None].expand(-1, -1, -1, w.d), V.abs())
+    if w.Ch > 0:  # parent rows cover the whole cell
+        par = torch.where(code < w.M0, code, (code - w.M0) // w.Ch)
+        cell = torch.zeros_like(absum)
+        cell.scatter_add_(2, par[..., None].expand(-1, -1, -1, w.d), V.abs())
+        absum[:, :, :w.M0] = cell[:, :, :w.M0]
+    bound = 2 * parity.gamma(w.N) * absum + 1e-30
+    diff = (vb1.double().cpu() - vb2.double().cpu()).abs()
+    assert (diff <= bound).all(), float((diff / bound).max())
+    print(f"  indices, counts equal; Vbar max |diff|/bound = {float((diff / bound).max()):.3g}",
+          flush=True)
 
 
 def test_children_equal_parent_gives_vq_attention():
