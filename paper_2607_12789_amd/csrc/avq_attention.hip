@@ -26,8 +26,10 @@
 // (-inf) take no part in the running max (App. D), and their correcting weight
 // exp(T_c + ln n_c - m) - n_c exp(Srec - m), Eq. (correcting_attention) times
 // n_c, is exactly zero for them however far their logits lie. The denominator
-// comes out of the value MFMA through one extra d-tile whose first row is all
-// ones, so numerator and denominator use the same rounded weights.
+// Z is the fp32 sum of the same weights, per lane over its codes and then
+// over the four lane groups (bf16: the value product takes the weights
+// rounded to bf16, so numerator and denominator differ by that rounding, a
+// relative 2^-9 per weight).
 //
 // Running max (in log2 units): it only moves when a chunk's logits exceed it
 // by more than kLazy, so the rescaling of the accumulators and the reduction
@@ -73,7 +75,6 @@ struct AttnCfg {
   static constexpr int TPC = CW / 16;             // 16-row tiles per chunk
   static constexpr int KQ = kB ? D / 32 : D / 4;  // MFMA k-steps over d
   static constexpr int DT = D / 16;               // d tiles of Xbar
-  static constexpr int XT = DT + 1;               // plus the denominator tile
   static constexpr int ESZ = sizeof(T);
   static constexpr int EPU = 16 / ESZ;            // elements per 16-byte unit
   static constexpr int U = D * ESZ / 16;          // 16-byte units per codeword row
@@ -138,7 +139,7 @@ void attention_kernel(AttnArgs args) {
   using Cfg = AttnCfg<T, D, MAXW>;
   constexpr bool kB = Cfg::kB;
   constexpr int QS = Cfg::QS, CW = Cfg::CW, TPC = Cfg::TPC, KQ = Cfg::KQ, DT = Cfg::DT,
-                XT = Cfg::XT, U = Cfg::U, EPU = Cfg::EPU, CPW = Cfg::CPW,
+                U = Cfg::U, EPU = Cfg::EPU, CPW = Cfg::CPW,
                 OCPY = Cfg::OCPY, OCT_ELEMS = Cfg::OCT_ELEMS;
   using QFrag = typename std::conditional<kB, bf16x8, float>::type;
   constexpr float kLn2 = 0.6931471805599453f;
@@ -303,10 +304,10 @@ void attention_kernel(AttnArgs args) {
     return *reinterpret_cast<const f32x4*>(&li[(4 * (tt / 2) + g) * 16 + 8 * part + 4 * (tt % 2)]);
   };
 
-  // ---- Xbar^T += Vmean^T . W^T; the extra tile DT has an all-ones first row
-  f32x4 X[XT][QS];
+  // ---- Xbar^T += Vmean^T . W^T ---------------------------------------------
+  f32x4 X[DT][QS];
 #pragma unroll
-  for (int dt = 0; dt < XT; ++dt)
+  for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int s = 0; s < QS; ++s) X[dt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -331,10 +332,6 @@ void attention_kernel(AttnArgs args) {
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(a[dt], bw[s], X[dt][s]);
-    const bf16 one = (bf16)(c == 0 ? 1.f : 0.f);
-    const bf16x8 ones = {one, one, one, one, one, one, one, one};
-#pragma unroll
-    for (int s = 0; s < QS; ++s) X[DT][s] = mfma_bf16(ones, bw[s], X[DT][s]);
   };
   // fp32: the r-th product of tile tt takes row r of the lane's half octet
   // as k-slot g
@@ -352,11 +349,6 @@ void attention_kernel(AttnArgs args) {
         X[dt][s] = mfma_f32(a.w, w0[s][3], X[dt][s]);
       }
     }
-    const float one = c == 0 ? 1.f : 0.f;
-#pragma unroll
-    for (int s = 0; s < QS; ++s)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) X[DT][s] = mfma_f32(one, w0[s][r], X[DT][s]);
   };
   auto accumulate_pair = [&](const unsigned char* B, int b, const f32x4 (&W)[2][QS]) {
     if constexpr (kB) {
@@ -370,7 +362,7 @@ void attention_kernel(AttnArgs args) {
   // Per-lane softmax state for query columns c + 16 s: m is the running max
   // in log2 units (lagging by at most kLazy), thr the raw logit (natural
   // units) that would pass m + kLazy, zp this lane group's partial fp32 sum of
-  // the parent weights (for importance).
+  // the weights (the parents' alone for importance, then the denominator).
   float m[QS], thr[QS], zp[QS];
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
@@ -404,7 +396,7 @@ void attention_kernel(AttnArgs args) {
       const float scs = exp2_hw(m[s] - mnew);
       zp[s] *= scs;
 #pragma unroll
-      for (int dt = 0; dt < XT; ++dt) X[dt][s] *= scs;
+      for (int dt = 0; dt < DT; ++dt) X[dt][s] *= scs;
       m[s] = mnew;
       thr[s] = (mnew + kLazy) * kLn2;
     }
@@ -473,8 +465,11 @@ void attention_kernel(AttnArgs args) {
       for (int s = 0; s < QS; ++s) {
         const float er = exp2_hw(fminf(fmaf(rs[h2][s], scale, -m[s]), 64.f));
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          S[h2][s][r] = fmaf(-n4[r], er, exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])));
+        for (int r = 0; r < 4; ++r) {
+          const float w = fmaf(-n4[r], er, exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])));
+          S[h2][s][r] = w;
+          zp[s] += w;
+        }
       }
     }
   };
@@ -781,10 +776,12 @@ void attention_kernel(AttnArgs args) {
     }
   }
 
-  // ---- phase 5: Y = Xbar / Z (Z from the denominator tile, lane group 0) ------
+  // ---- phase 5: Y = Xbar / Z (Z: the lane groups' partial sums) --------------
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
-    const float z = __shfl(X[DT][s][0], c, kWave);
+    float z = zp[s];
+    z += shfl_xor(z, 16);
+    z += shfl_xor(z, 32);
     if (!qvalid[s]) continue;
     const float rinv = 1.f / z;
     const int i = token_row(row0 + 16 * s + c);
