@@ -222,12 +222,16 @@ void attention_kernel(AttnArgs args) {
   // octets at mbase (means) and ibase (count info).
   constexpr uint32_t RowB = D * Cfg::ESZ;
   constexpr uint32_t OctB = OCT_ELEMS * Cfg::ESZ;
+  // skip_pad: the copies that hold only rows 4..7 of their octets (padding
+  // for Ch <= 4, never read) are not made (a copy spans RPC = 64 / U rows)
+  constexpr int RPC = 64 / U;
   auto issue = [&](unsigned char* B, bool with_values, const char* cbase, const char* mbase,
-                   const char* ibase, auto octet_of, auto row_off) {
+                   const char* ibase, auto octet_of, auto row_off, bool skip_pad = false) {
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int j = wave + MAXW * i;
-      if (j < Cfg::COPIES)
+      const bool pad = RPC <= 4 && skip_pad && (RPC * j) % 8 >= 4;
+      if (j < Cfg::COPIES && !pad)
         copy16_to_lds(cbase + (row_off(crow[i]) + (uint32_t)(ccol[i] * Cfg::ESZ)),
                       B + Cfg::OFF_C + 1024 * j);
     }
@@ -258,6 +262,7 @@ void attention_kernel(AttnArgs args) {
   // rows past Ch - 1 the last child
   const int n_child_oct = Ch > 1 ? P * CO : 0;
   const int co_shift = CO == 2 ? 1 : 0;
+  const bool half_child = Ch <= 4;  // rows 4..7 of every child octet are padding
   auto issue_child = [&](int k, unsigned char* B) {
     issue(
         B, true, reinterpret_cast<const char*>(cc_head), reinterpret_cast<const char*>(means),
@@ -273,7 +278,8 @@ void attention_kernel(AttnArgs args) {
           const int sl = o >> co_shift;
           const int cc = min((o - (sl << co_shift)) * 8 + r % 8, Ch - 1);
           return (uint32_t)(lsel[sl] * Ch + cc) * RowB;
-        });
+        },
+        half_child);
   };
   auto wait_chunk = [&]() {
     __builtin_amdgcn_s_waitcnt(0);
@@ -511,6 +517,105 @@ void attention_kernel(AttnArgs args) {
       logits(B, 1, S0[1], init[1]);
       logits(B, 2, S1[0], init[2]);
       logits(B, 3, S1[1], init[3]);
+    }
+  };
+
+  // Child chunk with Ch <= 4: rows 4..7 of every octet are padding, so logit
+  // tiles 1 and 3 (those rows) are never formed, and the valid halves of the
+  // chunk's two pairs share one value product: k-slots 0..3 of lane group g
+  // are codes 0..3 of octet g (pair 0), k-slots 4..7 codes 0..3 of octet
+  // 4 + g (pair 1). Half the MFMAs and exponentials of a full chunk.
+  auto child_chunk_half = [&](const unsigned char* B) {
+    f32x4 S0[2][QS], S1[2][QS];
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    const float ninf = -__builtin_inff();
+    const f32x4 pad = {ninf, ninf, ninf, ninf};
+    if constexpr (kB) {
+      const T* lc = reinterpret_cast<const T*>(B + Cfg::OFF_C);
+      bf16x8 a[2][KQ];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {  // tiles 0 and 2
+        const int r = 32 * h + 8 * (c / 4) + (c % 4);
+        const int sw = row_swizzle<U>(r);
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq)
+          a[h][kq] = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
+      }
+#pragma unroll
+      for (int kq = 0; kq < KQ; ++kq)
+#pragma unroll
+        for (int s = 0; s < QS; ++s) {
+          S0[0][s] = mfma_bf16(a[0][kq], qf[s][kq], kq == 0 ? zero : S0[0][s]);
+          S1[0][s] = mfma_bf16(a[1][kq], qf[s][kq], kq == 0 ? zero : S1[0][s]);
+        }
+    } else {
+      logits(B, 0, S0[0], zero);
+      logits(B, 2, S1[0], zero);
+    }
+    // the recovered sums (Ch = 2, 4: only the even tile's rows enter; the odd
+    // tile is zero here, as 0 * inf would poison the unused cases), then the
+    // odd tiles as -inf: no part in the max
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      S0[1][s] = zero;
+      S1[1][s] = zero;
+    }
+    float rs0[2][QS], rs1[2][QS];
+    child_recover(S0, rs0);
+    child_recover(S1, rs1);
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      S0[1][s] = pad;
+      S1[1][s] = pad;
+    }
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {  // log-count bias of the valid rows
+      const f32x4 l0 = info4(B, 0, 1), l2 = info4(B, 2, 1);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        S0[0][s][r] += l0[r];
+        S1[0][s][r] += l2[r];
+      }
+    }
+    check_chunk(S0, S1);
+    // correcting weights of the valid rows, as child_weights
+    const float scale = kLog2e / (float)Ch;
+    const f32x4 n0 = info4(B, 0, 0), n2 = info4(B, 2, 0);
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      const float e0 = exp2_hw(fminf(fmaf(rs0[0][s], scale, -m[s]), 64.f));
+      const float e1 = exp2_hw(fminf(fmaf(rs1[0][s], scale, -m[s]), 64.f));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float w0 = fmaf(-n0[r], e0, exp2_hw(fmaf(S0[0][s][r], kLog2e, -m[s])));
+        const float w1 = fmaf(-n2[r], e1, exp2_hw(fmaf(S1[0][s][r], kLog2e, -m[s])));
+        S0[0][s][r] = w0;
+        S1[0][s][r] = w1;
+        zp[s] += w0 + w1;
+      }
+    }
+    if constexpr (kB) {
+      bf16x8 bw[QS];
+#pragma unroll
+      for (int s = 0; s < QS; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          bw[s][r] = (bf16)S0[0][s][r];
+          bw[s][4 + r] = (bf16)S1[0][s][r];
+        }
+      const bf16* o0 = reinterpret_cast<const bf16*>(B + Cfg::OFF_V) + g * OCT_ELEMS;
+      const bf16* o1 = reinterpret_cast<const bf16*>(B + Cfg::OFF_V) + (4 + g) * OCT_ELEMS;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(o0 + 8 * (16 * dt + c));
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(o1 + 8 * (16 * dt + c));
+        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+        for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(a, bw[s], X[dt][s]);
+      }
+    } else {
+      accumulate_f(B, 0, S0[0]);
+      accumulate_f(B, 2, S1[0]);
     }
   };
 
@@ -755,7 +860,9 @@ void attention_kernel(AttnArgs args) {
       wait_chunk();
       if (Cfg::NBUF == 2 && k + 1 < n_cchunks) issue_child(k + 1, buffer((k + 1) % 2));
       const unsigned char* B = buffer(k % Cfg::NBUF);
-      if (has_rows) {
+      if (has_rows && half_child) {
+        child_chunk_half(B);
+      } else if (has_rows) {
         f32x4 S0[2][QS], S1[2][QS];
         float rs0[2][QS], rs1[2][QS];
         chunk_logits(B, false, S0, S1);

@@ -175,8 +175,10 @@ def test_children_equal_parent_gives_vq_attention():
     assert torch.equal(y_ref, y0)
 
 
-@pytest.mark.parametrize("dtype,P", [("bf16", 16), ("f32", 16), ("bf16", 6)])
-def test_empty_far_children(dtype, P):
+@pytest.mark.parametrize("dtype,P,Ch", [("bf16", 16, 8), ("f32", 16, 8), ("bf16", 6, 8),
+                                        ("bf16", 16, 4), ("f32", 6, 4), ("bf16", 9, 2),
+                                        ("f32", 9, 2)])
+def test_empty_far_children(dtype, P, Ch):
     """App. D: two children of a parent that the tiles select lie 100 units
     out on either side of it along the first axis, where every query has
     component +-3, so no key moves to them and one of them has a logit about
@@ -184,8 +186,8 @@ def test_empty_far_children(dtype, P):
     empty children and their correcting weights must be exactly zero;
     otherwise the rescale underflows the accumulators and Y = 0/0."""
     import oracle
-    w = small(dtype=dtype, M0=16, Ch=8, P=P, N=600, B=1, H=2)
-    banner(f"empty_far_children_{dtype}_P{P}", w)
+    w = small(dtype=dtype, M0=16, Ch=Ch, P=P, N=600, B=1, H=2)
+    banner(f"empty_far_children_{dtype}_P{P}_Ch{Ch}", w)
     x = inputs.generate(w)
     Q = x["Q"].clone()
     sign = torch.where(torch.arange(w.N) % 2 == 0, 3.0, -3.0)
