@@ -131,10 +131,12 @@ class Runner:
                           tiled_importance=self.tiled, query_order=self.order)
         if ev: ev[k + 1].record()
 
-    def timed(self, steps: int, warmup: int):
+    def timed(self, steps: int, warmup: int, cold: bool = False):
         """Runs warmup + steps steps; returns (wall ms per step, per-step event
-        durations [steps][len(stages)] in ms)."""
+        durations [steps][len(stages)] in ms). cold: a 1 GiB fill before each
+        step (outside the events) evicts the caches."""
         import torch
+        flush = torch.empty(1 << 28, dtype=torch.float32, device=self.Y.device) if cold else None
         for _ in range(warmup):
             self.step()
         n = len(self.stages)
@@ -142,6 +144,8 @@ class Runner:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(steps):
+            if flush is not None:
+                flush.fill_(float(i))
             self.step(evs[i])
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t0) * 1e3 / steps
@@ -283,6 +287,13 @@ def main():
                     help="least wall time the oracle baseline runs for")
     ap.add_argument("--cpu-max-passes", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="threads of the oracle baseline (0: all host cores)")
+    ap.add_argument("--cold", action="store_true",
+                    help="before every step, overwrite a 1 GiB buffer (four times the "
+                         "256 MB last-level cache) outside the timed events, so that each "
+                         "step starts with inputs in HBM only; the step time is then the "
+                         "sum of the event-timed entry points")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also launch one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--unfused-precompute", action="store_true",
@@ -335,7 +346,9 @@ def main():
     elif args.query_order == "random":
         order = torch.randperm(w.N, generator=torch.Generator().manual_seed(0)).to(torch.int32)
     runner = Runner(w, x, dev, args.tiled_importance, order, not args.unfused_precompute)
-    ms_per_step, per = runner.timed(args.steps, args.warmup)
+    ms_per_step, per = runner.timed(args.steps, args.warmup, args.cold)
+    if args.cold:  # the wall clock includes the fills: the steps are the events
+        ms_per_step = sum(sum(p) for p in per) / max(len(per), 1)
     # per-entry-point average duration over the timed steps
     stage_ms = {name: sum(p[i] for p in per) / max(len(per), 1)
                 for i, name in enumerate(runner.stages)}
@@ -369,7 +382,8 @@ def main():
                    "importance": "tiled (App. B, 64-parent tiles)" if args.tiled_importance
                    else "exact", "query_order": args.query_order,
                    "precompute": "avq_assign + avq_aggregate" if args.unfused_precompute
-                   else "avq_assign_aggregate (Alg. 1, one pass)"},
+                   else "avq_assign_aggregate (Alg. 1, one pass)",
+                   "caches": "cold (1 GiB fill before each step)" if args.cold else "warm"},
         "kernels_ms": stage_ms,
         "ms_per_step_median": _median([sum(p) for p in per]),
         "roofline": {"kernel": ("avq_attention_fwd_ordered" if order is not None else
@@ -380,6 +394,9 @@ def main():
                      "flops_per_launch": flops_attn},
     }
     if not args.no_cpu_baseline:
+        if args.cpu_threads > 0:
+            import oracle
+            oracle.set_num_threads(args.cpu_threads)
         line["cpu_baseline"] = cpu_baseline(x, w, args.cpu_seconds, args.cpu_max_passes)
     print(json.dumps(line), flush=True)
 
