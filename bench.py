@@ -45,6 +45,7 @@ sys.path.insert(0, str(ROOT))
 METRIC = "AVQ attention fwd query-tokens·heads/sec at N=16384; % bf16 MFMA peak"
 UNIT = "query-token*heads/s"
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
 KERNEL_SRC = ROOT / "paper_2607_12789_amd" / "csrc" / "avq_attention.hip"
 TRAFFIC_SUMMARY = ROOT / "profiles" / "attention_fwd_c4_traffic.md"
 
@@ -363,6 +364,8 @@ def main():
     qh = B * H * N
     flops_attn = 4.0 * d * (M0 + P * Ch) * qh
     achieved = flops_attn / (t_attn * 1e-3) / 1e12
+    # the MFMA peak of the kernel's own type: bf16 2.5 PFLOP/s, fp32 157.3 TFLOP/s
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     traffic = None if (args.tiled_importance or order is not None) else read_traffic()
     line = {
         "metric": METRIC,
@@ -389,8 +392,8 @@ def main():
         "roofline": {"kernel": ("avq_attention_fwd_ordered" if order is not None else
                                 "avq_attention_fwd_tiled" if args.tiled_importance
                                 else "avq_attention_fwd"), "bound": "mfma", "achieved": achieved,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+                     "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": traffic,
                      "flops_per_launch": flops_attn},
     }
     if not args.no_cpu_baseline:
