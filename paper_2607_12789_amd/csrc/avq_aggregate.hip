@@ -262,25 +262,29 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
     const int j = k * kAggThreads + tid;
     next[k] = j < N ? codes[j] : -1;
   }
+  // family-local row of a code (or, FUSED, the family of a parent index);
+  // -1 outside this range
+  auto row_of = [&](int code) {
+    int r = -1;
+    if constexpr (FUSED) {  // the family; its row comes from the child compare
+      if (code >= p0 && code < p0 + nfam) r = code - p0;
+    } else if (code >= 0 && code < Mtot) {
+      // Ch is a power of two: child code M0 + p Ch + c
+      const int p = code < M0 ? code : (code - M0) >> ch_shift;
+      if (p >= p0 && p < p0 + nfam)
+        r = (p - p0) * (1 + Ch) + (code < M0 ? 0 : 1 + ((code - M0) & (Ch - 1)));
+    }
+    return r;
+  };
   for (int base = 0;; base += kRound) {
     const bool done = base >= N;
-    int row[kCodesPerThread];
-    unsigned long long mask[kCodesPerThread];
+    // this round's codes; their rows and ballots are taken again after a
+    // flush rather than kept in registers through it
+    int cur[kCodesPerThread];
     int round_total = 0;
     if (!done) {
 #pragma unroll
-      for (int k = 0; k < kCodesPerThread; ++k) {
-        const int code = next[k];
-        row[k] = -1;
-        if constexpr (FUSED) {  // the family; its row comes from the child compare
-          if (code >= p0 && code < p0 + nfam) row[k] = code - p0;
-        } else if (code >= 0 && code < Mtot) {
-          // Ch is a power of two: child code M0 + p Ch + c
-          const int p = code < M0 ? code : (code - M0) >> ch_shift;
-          if (p >= p0 && p < p0 + nfam)
-            row[k] = (p - p0) * (1 + Ch) + (code < M0 ? 0 : 1 + ((code - M0) & (Ch - 1)));
-        }
-      }
+      for (int k = 0; k < kCodesPerThread; ++k) cur[k] = next[k];
 #pragma unroll
       for (int k = 0; k < kCodesPerThread; ++k) {  // prefetch the next round
         const int j = base + kRound + k * kAggThreads + tid;
@@ -288,8 +292,8 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       }
 #pragma unroll
       for (int k = 0; k < kCodesPerThread; ++k) {
-        mask[k] = __ballot(row[k] >= 0);
-        if (lane == 0) L.wave_count[k][wave] = __popcll(mask[k]);
+        const unsigned long long mk = __ballot(row_of(cur[k]) >= 0);
+        if (lane == 0) L.wave_count[k][wave] = __popcll(mk);
       }
       __syncthreads();
       if (wave == 0) {
@@ -398,10 +402,13 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
     if (done) break;
 #pragma unroll
     for (int k = 0; k < kCodesPerThread; ++k) {
-      if (row[k] >= 0) {
-        const int slot = qlen + L.wave_off[k][wave] + __popcll(mask[k] & ((1ull << lane) - 1ull));
+      asm volatile("" : "+v"(cur[k]));  // rows from the codes, not held through the flush
+      const int row = row_of(cur[k]);
+      const unsigned long long mk = __ballot(row >= 0);
+      if (row >= 0) {
+        const int slot = qlen + L.wave_off[k][wave] + __popcll(mk & ((1ull << lane) - 1ull));
         L.qkey[slot] = base + k * kAggThreads + tid;
-        L.qrow[slot] = (uint16_t)row[k];
+        L.qrow[slot] = (uint16_t)row;
       }
     }
     qlen += round_total;

@@ -205,81 +205,117 @@ void attention_kernel(AttnArgs args) {
   }
 
   // ---- chunk staging --------------------------------------------------------
-  // Copy i of this wave is wave copy j = wave + MAXW i of each array. For the
-  // codeword rows it covers chunk rows (64 j + lane) / U; their octet
-  // (row / 8) is the same for the whole wave copy.
-  int crow[CPW], ccol[CPW];
-#pragma unroll
-  for (int i = 0; i < CPW; ++i) {
-    const int q = 64 * (wave + MAXW * i) + lane;
-    crow[i] = q / U;
-    ccol[i] = ((q % U) ^ row_swizzle<U>(q / U)) * EPU;
-  }
-  auto buffer = [&](int b) { return lds_raw + b * Cfg::BUF_BYTES; };
-  // Sources are a wave-uniform base plus a 32-bit byte offset per lane (the
-  // loads take the scalar-base form). row_off(r): offset of chunk row r
-  // (0..63) from cbase; octet_of(os): index of chunk octet os among the
-  // octets at mbase (means) and ibase (count info).
+  // Copy i of this wave is wave copy j = wave + MAXW i of each array. A
+  // codeword copy covers RPC = 64 / U consecutive chunk rows, RPC j + lane / U,
+  // inside one octet. Each source address is a wave-uniform base, formed on
+  // the scalar unit per copy, plus a per-lane offset that is the same for
+  // every chunk and is computed here once; the LDS destination is uniform.
   constexpr uint32_t RowB = D * Cfg::ESZ;
   constexpr uint32_t OctB = OCT_ELEMS * Cfg::ESZ;
-  // skip_pad: the copies that hold only rows 4..7 of their octets (padding
-  // for Ch <= 4, never read) are not made (a copy spans RPC = 64 / U rows)
   constexpr int RPC = 64 / U;
-  auto issue = [&](unsigned char* B, bool with_values, const char* cbase, const char* mbase,
-                   const char* ibase, auto octet_of, auto row_off, bool skip_pad = false) {
+  const int lrow = lane / U;  // the lane's row inside its codeword copy
+  uint32_t voff[CPW];         // lane offset of codeword copy i: row and swizzled unit
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int r = RPC * (wave + MAXW * i) + lrow;
+    voff[i] = (uint32_t)(lrow * RowB + ((lane % U) ^ row_swizzle<U>(r)) * EPU * Cfg::ESZ);
+  }
+  const uint32_t moff = 16u * lane;  // lane offset of a mean copy
+  // the wave index in a scalar register: the copy indices derived from it are
+  // then computed on the scalar unit
+  const int cwave = __builtin_amdgcn_readfirstlane(wave);
+  auto buffer = [&](int b) { return lds_raw + b * Cfg::BUF_BYTES; };
+  // a copy from a uniform base: base and LDS offset in scalar registers
+  auto copy_u = [&](const char* base, uint32_t lane_off, uint32_t lds_off) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint64_t ua = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+                        (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+    copy16_to_lds(reinterpret_cast<const char*>(ua) + lane_off,
+                  lds_raw + __builtin_amdgcn_readfirstlane(lds_off));
+  };
+  const char* cp_bytes = reinterpret_cast<const char*>(cp_head);
+  const char* cc_bytes = reinterpret_cast<const char*>(cc_head);
+  const char* mean_bytes = reinterpret_cast<const char*>(means);
+  const char* info_bytes = reinterpret_cast<const char*>(info);
+  // parent chunk k into buffer b: rows past M0 - 1 read row M0 - 1 (only the
+  // last chunk has such rows; its codeword offsets are clamped per lane)
+  auto issue_parent = [&](int k, int b, bool with_values) {
+    const uint32_t B = (uint32_t)(b * Cfg::BUF_BYTES);
+    const char* cb = cp_bytes + (size_t)64 * k * RowB;
+    const bool full = 64 * (k + 1) <= M0;
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
-      const int j = wave + MAXW * i;
-      const bool pad = RPC <= 4 && skip_pad && (RPC * j) % 8 >= 4;
-      if (j < Cfg::COPIES && !pad)
-        copy16_to_lds(cbase + (row_off(crow[i]) + (uint32_t)(ccol[i] * Cfg::ESZ)),
-                      B + Cfg::OFF_C + 1024 * j);
+      const int j = cwave + MAXW * i;
+      if (j >= Cfg::COPIES) continue;
+      if (full) {
+        copy_u(cb + (size_t)RPC * j * RowB, voff[i], B + Cfg::OFF_C + 1024 * j);
+      } else {
+        const int r = min(RPC * j + lrow, M0 - 1 - 64 * k);
+        copy16_to_lds(cb + ((uint32_t)r * RowB + (voff[i] - lrow * RowB)),
+                      lds_raw + B + Cfg::OFF_C + 1024 * j);
+      }
     }
     if (with_values) {
 #pragma unroll
       for (int i = 0; i < CPW; ++i) {
-        const int j = wave + MAXW * i;
+        const int j = cwave + MAXW * i;
         if (j < Cfg::COPIES)
-          copy16_to_lds(mbase + (octet_of(j / OCPY) * OctB + (uint32_t)((j % OCPY) * 1024 + 16 * lane)),
-                        B + Cfg::OFF_V + 1024 * j);
+          copy_u(mean_bytes + (size_t)(8 * k + j / OCPY) * OctB + (j % OCPY) * 1024, moff,
+                 B + Cfg::OFF_V + 1024 * j);
       }
     }
-    if (wave == MAXW - 1 && lane < 32)  // 8 octets x 64 bytes of count info
-      copy16_to_lds(ibase + (octet_of(lane / 4) * 64u + (uint32_t)(16 * (lane % 4))), B + Cfg::OFF_I);
+    if (cwave == MAXW - 1 && lane < 32)  // 8 octets x 64 bytes of count info
+      copy16_to_lds(info_bytes + ((uint32_t)(8 * k + lane / 4) * 64u + (uint32_t)(16 * (lane % 4))),
+                    lds_raw + B + Cfg::OFF_I);
   };
-  // parent chunk k: rows past M0 - 1 read row M0 - 1
-  auto issue_parent = [&](int k, unsigned char* B, bool with_values) {
-    const int lim = M0 - 1 - 64 * k;
-    issue(
-        B, with_values, reinterpret_cast<const char*>(cp_head) + (size_t)64 * k * RowB,
-        reinterpret_cast<const char*>(means) + (size_t)8 * k * OctB,
-        reinterpret_cast<const char*>(info) + (size_t)8 * k * 64,
-        [&](int os) { return (uint32_t)os; },
-        [&](int r) { return (uint32_t)min(r, lim) * RowB; });
-  };
-  // child octet o belongs to selected parent o >> co_shift (CO is 1 or 2);
-  // octets past the last read the empty octet (and the last octet's rows),
-  // rows past Ch - 1 the last child
+  // child chunk k: octet o (o = 8k + os) belongs to selected parent o >> co_shift
+  // (CO is 1 or 2); octets past the last read the empty octet (means and
+  // counts) and the last octet's rows, rows past Ch - 1 the last child.
+  // skip_pad: with Ch <= 4 the copies that hold only rows 4..7 of their octets
+  // (padding, never read) are not made.
   const int n_child_oct = Ch > 1 ? P * CO : 0;
   const int co_shift = CO == 2 ? 1 : 0;
   const bool half_child = Ch <= 4;  // rows 4..7 of every child octet are padding
-  auto issue_child = [&](int k, unsigned char* B) {
-    issue(
-        B, true, reinterpret_cast<const char*>(cc_head), reinterpret_cast<const char*>(means),
-        reinterpret_cast<const char*>(info),
-        [&](int os) {
-          const int o = 8 * k + os;
-          if (o >= n_child_oct) return (uint32_t)ZO;
-          const int sl = o >> co_shift;
-          return (uint32_t)(PO + (lsel[sl] << co_shift) + (o - (sl << co_shift)));
-        },
-        [&](int r) {
-          const int o = min(8 * k + r / 8, n_child_oct - 1);
-          const int sl = o >> co_shift;
-          const int cc = min((o - (sl << co_shift)) * 8 + r % 8, Ch - 1);
-          return (uint32_t)(lsel[sl] * Ch + cc) * RowB;
-        },
-        half_child);
+  auto issue_child = [&](int k, int b) {
+    const uint32_t B = (uint32_t)(b * Cfg::BUF_BYTES);
+    // lane l holds the selected parent of octet 8k + (l mod 8) (clamped to the
+    // last octet); a copy takes the one of its octet with a lane read
+    const int sel_l = lsel[min(8 * k + (lane & 7), n_child_oct - 1) >> co_shift];
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int j = cwave + MAXW * i;
+      const bool pad = RPC <= 4 && half_child && (RPC * j) % 8 >= 4;
+      if (j >= Cfg::COPIES || pad) continue;
+      const int os = (RPC * j) / 8;
+      const int o = min(8 * k + os, n_child_oct - 1);
+      const int jj = o - ((o >> co_shift) << co_shift);  // child octet of the parent
+      const int par = __builtin_amdgcn_readlane(sel_l, os);
+      const int u = jj * 8 + (RPC * j) % 8;  // the copy's first row among the children
+      if (Ch >= 8) {  // every row of the copy is a child
+        copy_u(cc_bytes + (size_t)(par * Ch + u) * RowB, voff[i], B + Cfg::OFF_C + 1024 * j);
+      } else {
+        const int cc = min(u + lrow, Ch - 1);
+        copy16_to_lds(cc_bytes + (size_t)par * Ch * RowB + ((uint32_t)cc * RowB + (voff[i] - lrow * RowB)),
+                      lds_raw + B + Cfg::OFF_C + 1024 * j);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int j = cwave + MAXW * i;
+      if (j >= Cfg::COPIES) continue;
+      const int os = j / OCPY;
+      const int o = 8 * k + os;
+      const int par = __builtin_amdgcn_readlane(sel_l, os);
+      const int oct = o >= n_child_oct ? ZO : PO + (par << co_shift) + (o - ((o >> co_shift) << co_shift));
+      copy_u(mean_bytes + (size_t)oct * OctB + (j % OCPY) * 1024, moff, B + Cfg::OFF_V + 1024 * j);
+    }
+    if (cwave == MAXW - 1 && lane < 32) {  // count info: lane's octet lane / 4
+      const int o = 8 * k + lane / 4;
+      const int sl = o >> co_shift;
+      const int oct = o >= n_child_oct ? ZO : PO + (lsel[sl] << co_shift) + (o - (sl << co_shift));
+      copy16_to_lds(info_bytes + ((uint32_t)oct * 64u + (uint32_t)(16 * (lane % 4))),
+                    lds_raw + B + Cfg::OFF_I);
+    }
   };
   auto wait_chunk = [&]() {
     __builtin_amdgcn_s_waitcnt(0);
@@ -716,11 +752,11 @@ void attention_kernel(AttnArgs args) {
   // Per chunk: the logits of both tile pairs are issued first, then one max
   // check; the first pair's value MFMAs run while the second pair's weights
   // are computed.
-  issue_parent(0, buffer(0), true);
+  issue_parent(0, 0, true);
   for (int k = 0; k < n_pchunks; ++k) {
     wait_chunk();
     if (tiled_importance && k > 0) importance_flush(k - 1);
-    if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, buffer((k + 1) % 2), true);
+    if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, (k + 1) % 2, true);
     const unsigned char* B = buffer(k % Cfg::NBUF);
     if (has_rows) {
       f32x4 S0[2][QS], S1[2][QS];
@@ -741,7 +777,7 @@ void attention_kernel(AttnArgs args) {
     }
     if (Cfg::NBUF == 1 && k + 1 < n_pchunks) {
       __syncthreads();
-      issue_parent(k + 1, buffer(0), true);
+      issue_parent(k + 1, 0, true);
     }
   }
 
@@ -756,11 +792,11 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
       for (int s = 0; s < QS; ++s) one[s] = 1.f;
       __syncthreads();
-      issue_parent(0, buffer(0), false);
+      issue_parent(0, 0, false);
       for (int k = 0; k < n_pchunks; ++k) {
         wait_chunk();
         if (k > 0) importance_flush(k - 1);
-        if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, buffer((k + 1) % 2), false);
+        if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, (k + 1) % 2, false);
         const unsigned char* B = buffer(k % Cfg::NBUF);
         if (has_rows) {
           f32x4 S0[2][QS], S1[2][QS];
@@ -778,7 +814,7 @@ void attention_kernel(AttnArgs args) {
         }
         if (Cfg::NBUF == 1 && k + 1 < n_pchunks) {
           __syncthreads();
-          issue_parent(k + 1, buffer(0), false);
+          issue_parent(k + 1, 0, false);
         }
       }
       __syncthreads();
@@ -855,10 +891,10 @@ void attention_kernel(AttnArgs args) {
     // recovered parent logit is that child's own logit, so every correcting
     // weight is exactly zero: nothing to do.
     const int n_cchunks = (n_child_oct + 7) / 8;
-    if (n_cchunks > 0) issue_child(0, buffer(0));
+    if (n_cchunks > 0) issue_child(0, 0);
     for (int k = 0; k < n_cchunks; ++k) {
       wait_chunk();
-      if (Cfg::NBUF == 2 && k + 1 < n_cchunks) issue_child(k + 1, buffer((k + 1) % 2));
+      if (Cfg::NBUF == 2 && k + 1 < n_cchunks) issue_child(k + 1, (k + 1) % 2);
       const unsigned char* B = buffer(k % Cfg::NBUF);
       if (has_rows && half_child) {
         child_chunk_half(B);
@@ -878,7 +914,7 @@ void attention_kernel(AttnArgs args) {
       }
       if (Cfg::NBUF == 1 && k + 1 < n_cchunks) {  // one buffer: refill it when all are done
         __syncthreads();
-        issue_child(k + 1, buffer(0));
+        issue_child(k + 1, 0);
       }
     }
   }
