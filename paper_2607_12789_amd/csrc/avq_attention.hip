@@ -833,8 +833,9 @@ void attention_kernel(AttnArgs args) {
   // still missing. The selected parents are listed in index order. With
   // P >= M0 every parent is selected (all keys 1).
   if (P > 0) {
-    if (wave == 0) {
-      constexpr int NV = Cfg::M0MAX / kWave;
+    // NV key registers per lane: the fewest that hold M0 parents
+    auto select_top = [&](auto nv_tag) {
+      constexpr int NV = decltype(nv_tag)::value;
       unsigned key[NV];
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
@@ -870,6 +871,11 @@ void attention_kernel(AttnArgs args) {
         if (sel) lsel[filled + __popcll(ms & below)] = kWave * i + lane;
         filled += __popcll(ms);
       }
+    };
+    if (wave == 0) {
+      if (M0 <= 2 * kWave) select_top(std::integral_constant<int, 2>{});
+      else if (M0 <= 4 * kWave) select_top(std::integral_constant<int, 4>{});
+      else select_top(std::integral_constant<int, Cfg::M0MAX / kWave>{});
     }
     __syncthreads();
     if (args.topp_idx) {  // canonical order (w desc, index asc) for the caller
