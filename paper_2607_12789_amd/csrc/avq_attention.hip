@@ -367,9 +367,12 @@ void attention_kernel(AttnArgs args) {
       }
     }
     const bf16* oct = reinterpret_cast<const bf16*>(B + Cfg::OFF_V) + (4 * b + g) * OCT_ELEMS;
+    // all of the pair's A operands are read before its products, so that the
+    // products wait for the LDS once
     bf16x8 a[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) a[dt] = *reinterpret_cast<const bf16x8*>(oct + 8 * (16 * dt + c));
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -398,6 +401,42 @@ void attention_kernel(AttnArgs args) {
     } else {
       accumulate_f(B, 2 * b, W[0]);
       accumulate_f(B, 2 * b + 1, W[1]);
+    }
+  };
+  // The value product of tile pair b in two steps, so that its A operands
+  // (bf16: octet 4 b + g at the lane's columns) are read from LDS before the
+  // weights they multiply are computed, and their latency is hidden by that
+  // work. bf16 at d = 128 only: at d = 64 the three waves per SIMD leave no
+  // registers for them (they are read where they are used), as for fp32.
+  constexpr bool kValAhead = kB && D == 128;
+  struct ValOps {
+    bf16x8 a[kValAhead ? DT : 1];
+  };
+  auto load_vals = [&](const unsigned char* B, int b) {
+    ValOps v;
+    if constexpr (kValAhead) {
+      const bf16* oct = reinterpret_cast<const bf16*>(B + Cfg::OFF_V) + (4 * b + g) * OCT_ELEMS;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) v.a[dt] = *reinterpret_cast<const bf16x8*>(oct + 8 * (16 * dt + c));
+    }
+    return v;
+  };
+  auto mfma_vals = [&](const unsigned char* B, int b, const ValOps& v, const f32x4 (&W)[2][QS]) {
+    if constexpr (kValAhead) {
+      bf16x8 bw[QS];
+#pragma unroll
+      for (int s = 0; s < QS; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          bw[s][r] = (bf16)W[0][s][r];
+          bw[s][4 + r] = (bf16)W[1][s][r];
+        }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int s = 0; s < QS; ++s) X[dt][s] = mfma_bf16(v.a[dt], bw[s], X[dt][s]);
+    } else {
+      accumulate_pair(B, b, W);
     }
   };
 
@@ -761,11 +800,14 @@ void attention_kernel(AttnArgs args) {
     if (has_rows) {
       f32x4 S0[2][QS], S1[2][QS];
       chunk_logits(B, true, S0, S1);
+      const ValOps v0 = load_vals(B, 0);  // in flight during the max check and weights
+      __builtin_amdgcn_sched_barrier(0);
       check_chunk(S0, S1);
       parent_weights(S0);
-      accumulate_pair(B, 0, S0);
+      mfma_vals(B, 0, v0, S0);
+      const ValOps v1 = load_vals(B, 1);
       parent_weights(S1);
-      accumulate_pair(B, 1, S1);
+      mfma_vals(B, 1, v1, S1);
       if (n_pchunks == 1 && need_importance) {  // max and denominators are final
         set_mz();
         float rz[QS];
@@ -908,15 +950,18 @@ void attention_kernel(AttnArgs args) {
         f32x4 S0[2][QS], S1[2][QS];
         float rs0[2][QS], rs1[2][QS];
         chunk_logits(B, false, S0, S1);
+        const ValOps v0 = load_vals(B, 0);  // in flight during the recovery, bias and weights
+        __builtin_amdgcn_sched_barrier(0);
         child_recover(S0, rs0);
         child_recover(S1, rs1);
         child_bias(B, 0, S0);
         child_bias(B, 1, S1);
         check_chunk(S0, S1);
         child_weights(B, 0, S0, rs0);
-        accumulate_pair(B, 0, S0);
+        mfma_vals(B, 0, v0, S0);
+        const ValOps v1 = load_vals(B, 1);
         child_weights(B, 1, S1, rs1);
-        accumulate_pair(B, 1, S1);
+        mfma_vals(B, 1, v1, S1);
       }
       if (Cfg::NBUF == 1 && k + 1 < n_cchunks) {  // one buffer: refill it when all are done
         __syncthreads();
