@@ -112,11 +112,10 @@ struct AttnArgs {
   int H, N, M0, Ch, P, block_q, n_tiles;
 };
 
-// One wave copies 64 x 16 bytes from global memory to LDS: lane L's 16 bytes
-// land at lds + 16 L (lds must be the same for the whole wave).
-__device__ __forceinline__ void copy16_to_lds(const void* src, void* lds) {
-  __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
-                                   (void __attribute__((address_space(3)))*)lds, 16, 0, 0);
+// A raw buffer resource over bytes [p, p + bytes): stride 0, no format
+// conversion (the gfx9 word-3 setting); loads past the end read 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
 // XOR swizzle of the 16-byte units of a staged codeword row: the 16 rows a
@@ -205,73 +204,74 @@ void attention_kernel(AttnArgs args) {
   }
 
   // ---- chunk staging --------------------------------------------------------
-  // Copy i of this wave is wave copy j = wave + MAXW i of each array. A
-  // codeword copy covers RPC = 64 / U consecutive chunk rows, RPC j + lane / U,
-  // inside one octet. Each source address is a wave-uniform base, formed on
-  // the scalar unit per copy, plus a per-lane offset that is the same for
-  // every chunk and is computed here once; the LDS destination is uniform.
+  // Copies are buffer loads straight into LDS: one buffer resource per array
+  // (base and size in scalar registers, made once per tile), the offset of
+  // the chunk and copy in a scalar register, and a per-lane offset that is the
+  // same for every chunk, computed here once; the LDS destination is uniform.
+  // Copy i of this wave is wave copy j = wave + MAXW i of each array (every j
+  // is below COPIES, a multiple of MAXW). A codeword copy covers RPC = 64 / U
+  // consecutive chunk rows, RPC j + lane / U, inside one octet.
+  static_assert(Cfg::COPIES % MAXW == 0, "copies split evenly over the waves");
   constexpr uint32_t RowB = D * Cfg::ESZ;
   constexpr uint32_t OctB = OCT_ELEMS * Cfg::ESZ;
   constexpr int RPC = 64 / U;
-  const int lrow = lane / U;  // the lane's row inside its codeword copy
-  uint32_t voff[CPW];         // lane offset of codeword copy i: row and swizzled unit
+  const int lrow = lane / U;               // the lane's row inside its codeword copy
+  const uint32_t loff = lrow * RowB;       // ... as a byte offset
+  uint32_t uoff[CPW];                      // the lane's swizzled unit in codeword copy i
 #pragma unroll
   for (int i = 0; i < CPW; ++i) {
     const int r = RPC * (wave + MAXW * i) + lrow;
-    voff[i] = (uint32_t)(lrow * RowB + ((lane % U) ^ row_swizzle<U>(r)) * EPU * Cfg::ESZ);
+    uoff[i] = (uint32_t)(((lane % U) ^ row_swizzle<U>(r)) * EPU * Cfg::ESZ);
   }
-  const uint32_t moff = 16u * lane;  // lane offset of a mean copy
+  const uint32_t moff = 16u * lane;  // lane offset of a mean or count-info copy
   // the wave index in a scalar register: the copy indices derived from it are
   // then computed on the scalar unit
   const int cwave = __builtin_amdgcn_readfirstlane(wave);
   auto buffer = [&](int b) { return lds_raw + b * Cfg::BUF_BYTES; };
-  // a copy from a uniform base: base and LDS offset in scalar registers
-  auto copy_u = [&](const char* base, uint32_t lane_off, uint32_t lds_off) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    const uint64_t ua = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
-                        (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
-    copy16_to_lds(reinterpret_cast<const char*>(ua) + lane_off,
-                  lds_raw + __builtin_amdgcn_readfirstlane(lds_off));
+  const __amdgpu_buffer_rsrc_t r_cp = make_rsrc(cp_head, (uint32_t)M0 * RowB);
+  const __amdgpu_buffer_rsrc_t r_cc = make_rsrc(cc_head, (uint32_t)(M0 * Ch) * RowB);
+  const __amdgpu_buffer_rsrc_t r_pk = make_rsrc(pk, (uint32_t)PL.bytes);
+  // 16 bytes per lane from rsrc at soffset + voffset to LDS at lds_off + 16 lane
+  auto copy = [&](__amdgpu_buffer_rsrc_t rs, uint32_t voffset, uint32_t soffset, uint32_t lds_off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rs, (__attribute__((address_space(3))) void*)(lds_raw + __builtin_amdgcn_readfirstlane(lds_off)),
+        16, voffset, __builtin_amdgcn_readfirstlane(soffset), 0, 0);
   };
-  const char* cp_bytes = reinterpret_cast<const char*>(cp_head);
-  const char* cc_bytes = reinterpret_cast<const char*>(cc_head);
-  const char* mean_bytes = reinterpret_cast<const char*>(means);
-  const char* info_bytes = reinterpret_cast<const char*>(info);
+  const uint32_t info_off = (uint32_t)PL.info_off;
   // parent chunk k into buffer b: rows past M0 - 1 read row M0 - 1 (only the
   // last chunk has such rows; its codeword offsets are clamped per lane)
   auto issue_parent = [&](int k, int b, bool with_values) {
     const uint32_t B = (uint32_t)(b * Cfg::BUF_BYTES);
-    const char* cb = cp_bytes + (size_t)64 * k * RowB;
-    const bool full = 64 * (k + 1) <= M0;
+    const uint32_t kb = (uint32_t)(64 * k) * RowB;
+    if (64 * (k + 1) <= M0) {
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const int j = cwave + MAXW * i;
-      if (j >= Cfg::COPIES) continue;
-      if (full) {
-        copy_u(cb + (size_t)RPC * j * RowB, voff[i], B + Cfg::OFF_C + 1024 * j);
-      } else {
-        const int r = min(RPC * j + lrow, M0 - 1 - 64 * k);
-        copy16_to_lds(cb + ((uint32_t)r * RowB + (voff[i] - lrow * RowB)),
-                      lds_raw + B + Cfg::OFF_C + 1024 * j);
+      for (int i = 0; i < CPW; ++i) {
+        const int j = cwave + MAXW * i;
+        copy(r_cp, loff + uoff[i], kb + (uint32_t)(RPC * j) * RowB, B + Cfg::OFF_C + 1024 * j);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < CPW; ++i) {
+        const int j = cwave + MAXW * i;
+        const uint32_t r = (uint32_t)min(RPC * j + lrow, M0 - 1 - 64 * k);
+        copy(r_cp, r * RowB + uoff[i], kb, B + Cfg::OFF_C + 1024 * j);
       }
     }
     if (with_values) {
 #pragma unroll
       for (int i = 0; i < CPW; ++i) {
         const int j = cwave + MAXW * i;
-        if (j < Cfg::COPIES)
-          copy_u(mean_bytes + (size_t)(8 * k + j / OCPY) * OctB + (j % OCPY) * 1024, moff,
-                 B + Cfg::OFF_V + 1024 * j);
+        copy(r_pk, moff, (uint32_t)(8 * k + j / OCPY) * OctB + (uint32_t)(j % OCPY) * 1024u,
+             B + Cfg::OFF_V + 1024 * j);
       }
     }
     if (cwave == MAXW - 1 && lane < 32)  // 8 octets x 64 bytes of count info
-      copy16_to_lds(info_bytes + ((uint32_t)(8 * k + lane / 4) * 64u + (uint32_t)(16 * (lane % 4))),
-                    lds_raw + B + Cfg::OFF_I);
+      copy(r_pk, moff, info_off + (uint32_t)(8 * k) * 64u, B + Cfg::OFF_I);
   };
   // child chunk k: octet o (o = 8k + os) belongs to selected parent o >> co_shift
   // (CO is 1 or 2); octets past the last read the empty octet (means and
   // counts) and the last octet's rows, rows past Ch - 1 the last child.
-  // skip_pad: with Ch <= 4 the copies that hold only rows 4..7 of their octets
+  // With Ch <= 4 the copies that hold only rows 4..7 of their octets
   // (padding, never read) are not made.
   const int n_child_oct = Ch > 1 ? P * CO : 0;
   const int co_shift = CO == 2 ? 1 : 0;
@@ -281,40 +281,45 @@ void attention_kernel(AttnArgs args) {
     // lane l holds the selected parent of octet 8k + (l mod 8) (clamped to the
     // last octet); a copy takes the one of its octet with a lane read
     const int sel_l = lsel[min(8 * k + (lane & 7), n_child_oct - 1) >> co_shift];
+    if (Ch >= 8) {  // every row of a copy is a child
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const int j = cwave + MAXW * i;
-      const bool pad = RPC <= 4 && half_child && (RPC * j) % 8 >= 4;
-      if (j >= Cfg::COPIES || pad) continue;
-      const int os = (RPC * j) / 8;
-      const int o = min(8 * k + os, n_child_oct - 1);
-      const int jj = o - ((o >> co_shift) << co_shift);  // child octet of the parent
-      const int par = __builtin_amdgcn_readlane(sel_l, os);
-      const int u = jj * 8 + (RPC * j) % 8;  // the copy's first row among the children
-      if (Ch >= 8) {  // every row of the copy is a child
-        copy_u(cc_bytes + (size_t)(par * Ch + u) * RowB, voff[i], B + Cfg::OFF_C + 1024 * j);
-      } else {
-        const int cc = min(u + lrow, Ch - 1);
-        copy16_to_lds(cc_bytes + (size_t)par * Ch * RowB + ((uint32_t)cc * RowB + (voff[i] - lrow * RowB)),
-                      lds_raw + B + Cfg::OFF_C + 1024 * j);
+      for (int i = 0; i < CPW; ++i) {
+        const int j = cwave + MAXW * i;
+        const int os = (RPC * j) / 8;
+        const int o = min(8 * k + os, n_child_oct - 1);
+        const int jj = o - ((o >> co_shift) << co_shift);  // child octet of the parent
+        const int par = __builtin_amdgcn_readlane(sel_l, os);
+        const int u = jj * 8 + (RPC * j) % 8;  // the copy's first row among the children
+        copy(r_cc, loff + uoff[i], (uint32_t)(par * Ch + u) * RowB, B + Cfg::OFF_C + 1024 * j);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < CPW; ++i) {
+        const int j = cwave + MAXW * i;
+        if (RPC <= 4 && half_child && (RPC * j) % 8 >= 4) continue;
+        const int os = (RPC * j) / 8;
+        const int o = min(8 * k + os, n_child_oct - 1);
+        const int jj = o - ((o >> co_shift) << co_shift);
+        const int par = __builtin_amdgcn_readlane(sel_l, os);
+        const int u = jj * 8 + (RPC * j) % 8;
+        const uint32_t cc = (uint32_t)min(u + lrow, Ch - 1);
+        copy(r_cc, cc * RowB + uoff[i], (uint32_t)(par * Ch) * RowB, B + Cfg::OFF_C + 1024 * j);
       }
     }
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int j = cwave + MAXW * i;
-      if (j >= Cfg::COPIES) continue;
       const int os = j / OCPY;
       const int o = 8 * k + os;
       const int par = __builtin_amdgcn_readlane(sel_l, os);
       const int oct = o >= n_child_oct ? ZO : PO + (par << co_shift) + (o - ((o >> co_shift) << co_shift));
-      copy_u(mean_bytes + (size_t)oct * OctB + (j % OCPY) * 1024, moff, B + Cfg::OFF_V + 1024 * j);
+      copy(r_pk, moff, (uint32_t)oct * OctB + (uint32_t)(j % OCPY) * 1024u, B + Cfg::OFF_V + 1024 * j);
     }
     if (cwave == MAXW - 1 && lane < 32) {  // count info: lane's octet lane / 4
       const int o = 8 * k + lane / 4;
       const int sl = o >> co_shift;
       const int oct = o >= n_child_oct ? ZO : PO + (lsel[sl] << co_shift) + (o - (sl << co_shift));
-      copy16_to_lds(info_bytes + ((uint32_t)oct * 64u + (uint32_t)(16 * (lane % 4))),
-                    lds_raw + B + Cfg::OFF_I);
+      copy(r_pk, (uint32_t)oct * 64u + (uint32_t)(16 * (lane % 4)), info_off, B + Cfg::OFF_I);
     }
   };
   auto wait_chunk = [&]() {
