@@ -44,11 +44,12 @@
 // buffer, refilled after each chunk). Phases per tile:
 //   1. parent sweep: logits, running max, weights, fp32 parent denominator,
 //      Xbar += Vmean^T W;
-//   2. importance (Eq. (importance)) with the final max and denominator: a
-//      second sweep recomputes the parent logits (or reuses them when all
-//      parents fit one chunk) and takes exp(t - m - ln Z) directly; sums over
-//      the tile's queries by a reduce-scatter butterfly over lanes, then a
-//      fixed order over waves. TILED instead takes the importance of App. B
+//   2. importance (Eq. (importance)) with the final max and denominator: the
+//      last parent chunk's weights are still in registers when both are
+//      final, and are scaled by 1/Z there; a second sweep recomputes the
+//      logits of the other chunks and takes exp(t - m - ln Z) directly; sums
+//      over the tile's queries by a reduce-scatter butterfly over lanes, then
+//      a fixed order over waves. TILED instead takes the importance of App. B
 //      inside phase 1, chunk by chunk, and skips the second sweep;
 //   3. top-P in one wave: a threshold on the importance bits, built bit by
 //      bit from the top, finds the P-th largest value; ties at it go to the
@@ -813,12 +814,15 @@ void attention_kernel(AttnArgs args) {
       const ValOps v1 = load_vals(B, 1);
       parent_weights(S1);
       mfma_vals(B, 1, v1, S1);
-      if (n_pchunks == 1 && need_importance) {  // max and denominators are final
+      // the last chunk: max and denominators are final, so its normalised
+      // weights are its weights times 1/Z (the other chunks' importance comes
+      // from the second sweep)
+      if (k == n_pchunks - 1 && need_importance && !tiled_importance) {
         set_mz();
         float rz[QS];
 #pragma unroll
         for (int s = 0; s < QS; ++s) rz[s] = exp2_hw(m[s] - mz[s]);
-        importance_partials(S0, S1, rz, 0);
+        importance_partials(S0, S1, rz, k % 2);
       }
       if (tiled_importance) tiled_partials(B, S0, S1, k);
     }
@@ -834,16 +838,19 @@ void attention_kernel(AttnArgs args) {
       __syncthreads();
       importance_flush(n_pchunks - 1);
     } else {
-      if (has_rows) set_mz();
+      // chunks 0 .. n_pchunks - 2 again; the last one's partials (slot
+      // (n_pchunks - 1) % 2) are summed before the sweep writes any slot
+      const int n_sweep = n_pchunks - 1;
       float one[QS];
 #pragma unroll
       for (int s = 0; s < QS; ++s) one[s] = 1.f;
       __syncthreads();
+      importance_flush(n_pchunks - 1);
       issue_parent(0, 0, false);
-      for (int k = 0; k < n_pchunks; ++k) {
+      for (int k = 0; k < n_sweep; ++k) {
         wait_chunk();
         if (k > 0) importance_flush(k - 1);
-        if (Cfg::NBUF == 2 && k + 1 < n_pchunks) issue_parent(k + 1, (k + 1) % 2, false);
+        if (Cfg::NBUF == 2 && k + 1 < n_sweep) issue_parent(k + 1, (k + 1) % 2, false);
         const unsigned char* B = buffer(k % Cfg::NBUF);
         if (has_rows) {
           f32x4 S0[2][QS], S1[2][QS];
@@ -859,13 +866,13 @@ void attention_kernel(AttnArgs args) {
               }
           importance_partials(S0, S1, one, k % 2);
         }
-        if (Cfg::NBUF == 1 && k + 1 < n_pchunks) {
+        if (Cfg::NBUF == 1 && k + 1 < n_sweep) {
           __syncthreads();
           issue_parent(k + 1, 0, false);
         }
       }
       __syncthreads();
-      importance_flush(n_pchunks - 1);
+      importance_flush(n_sweep - 1);
     }
   }
   __syncthreads();
