@@ -525,6 +525,18 @@ void attention_kernel(AttnArgs args) {
       rs[1][s] = fmaf(w2, a01, fmaf(w4, bs, fmaf(w8, ab, w16 * ab16)));
     }
   };
+  // Ch = 8: the lane's octet is the whole family, so the recovered sum is the
+  // sum of the lane's 8 values (the case child_recover keeps for Ch = 8,
+  // without the other cases' arithmetic)
+  auto child_recover8 = [&](const f32x4 (&S)[2][QS], float (&rs)[2][QS]) {
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      const f32x4 v0 = S[0][s], v1 = S[1][s];
+      const float ab = ((v0[0] + v0[1]) + (v0[2] + v0[3])) + ((v1[0] + v1[1]) + (v1[2] + v1[3]));
+      rs[0][s] = ab;
+      rs[1][s] = ab;
+    }
+  };
   // log-count bias of the child logits of tile pair b, in place: T + ln n,
   // -inf for empty children and padding rows (App. D: the running max is
   // taken over non-empty codes only)
@@ -964,8 +976,13 @@ void attention_kernel(AttnArgs args) {
         chunk_logits(B, false, S0, S1);
         const ValOps v0 = load_vals(B, 0);  // in flight during the recovery, bias and weights
         __builtin_amdgcn_sched_barrier(0);
-        child_recover(S0, rs0);
-        child_recover(S1, rs1);
+        if (Ch == 8) {
+          child_recover8(S0, rs0);
+          child_recover8(S1, rs1);
+        } else {
+          child_recover(S0, rs0);
+          child_recover(S1, rs1);
+        }
         child_bias(B, 0, S0);
         child_bias(B, 1, S1);
         check_chunk(S0, S1);
