@@ -1000,23 +1000,72 @@ void attention_kernel(AttnArgs args) {
   }
 
   // ---- phase 5: Y = Xbar / Z (Z: the lane groups' partial sums) --------------
+  // Each wave stages its 32 rows in LDS (the chunk buffers are free by now)
+  // and stores them as whole rows, 16 bytes per lane and 16 B x (row bytes /
+  // 16) lanes per row, instead of 8-byte pieces of 16 rows per instruction.
+  // The 16-byte units of a staged row are XOR-swizzled by row, so the 16
+  // rows a fragment write touches hit different banks.
+  float rinv[QS];
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
     float z = zp[s];
     z += shfl_xor(z, 16);
     z += shfl_xor(z, 32);
-    if (!qvalid[s]) continue;
-    const float rinv = 1.f / z;
-    const int i = token_row(row0 + 16 * s + c);
-    T* yrow = static_cast<T*>(args.Y) + ((size_t)bh * N + i) * D;
+    rinv[s] = 1.f / z;
+  }
+  constexpr int YROW = D * Cfg::ESZ;         // bytes of one Y row
+  constexpr int YU = YROW / 16;              // 16-byte units per row
+  constexpr int RPB = YROW >= 256 ? 1 : 256 / YROW;  // rows per 256 bytes of banks
+  constexpr bool kStageY = (size_t)MAXW * Cfg::RPW * YROW <= (size_t)Cfg::NBUF * Cfg::BUF_BYTES;
+  auto yswz = [](int r) { return (r / RPB) % YU; };
+  if constexpr (kStageY) {
+    __syncthreads();  // every wave is done with the chunk buffers
+    unsigned char* ys = lds_raw + (size_t)wave * Cfg::RPW * YROW;  // this wave's rows
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const f32x4 y = X[dt][s] * rinv;
-      if constexpr (kB) {
-        bf16x4 o = {(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
-        *reinterpret_cast<bf16x4*>(yrow + 16 * dt + 4 * g) = o;
-      } else {
-        *reinterpret_cast<f32x4*>(yrow + 16 * dt + 4 * g) = y;
+    for (int s = 0; s < QS; ++s) {
+      const int r = 16 * s + c;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const f32x4 y = X[dt][s] * rinv[s];
+        const int byte = (16 * dt + 4 * g) * Cfg::ESZ;  // of the lane's 4 values in the row
+        unsigned char* dst = ys + r * YROW + (((byte / 16) ^ yswz(r)) * 16) + byte % 16;
+        if constexpr (kB) {
+          bf16x4 o = {(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
+          *reinterpret_cast<bf16x4*>(dst) = o;
+        } else {
+          *reinterpret_cast<f32x4*>(dst) = y;
+        }
+      }
+    }
+    // the wave reads back only what it wrote: LDS operations of one wave
+    // complete in order
+    constexpr int RPI = 64 / YU;  // rows per instruction
+    const int u = lane % YU;
+#pragma unroll
+    for (int i = 0; i < Cfg::RPW / RPI; ++i) {
+      const int r = RPI * i + lane / YU;
+      const uint4 v = *reinterpret_cast<const uint4*>(ys + r * YROW + ((u ^ yswz(r)) * 16));
+      const int q = row0 + r;
+      const int tok = q < q_end ? token_row(q) : -1;
+      if (tok >= 0)
+        *reinterpret_cast<uint4*>(static_cast<unsigned char*>(args.Y) +
+                                  ((size_t)bh * N + tok) * YROW + u * 16) = v;
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      if (!qvalid[s]) continue;
+      const int i = token_row(row0 + 16 * s + c);
+      T* yrow = static_cast<T*>(args.Y) + ((size_t)bh * N + i) * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const f32x4 y = X[dt][s] * rinv[s];
+        if constexpr (kB) {
+          bf16x4 o = {(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
+          *reinterpret_cast<bf16x4*>(yrow + 16 * dt + 4 * g) = o;
+        } else {
+          *reinterpret_cast<f32x4*>(yrow + 16 * dt + 4 * g) = y;
+        }
       }
     }
   }
