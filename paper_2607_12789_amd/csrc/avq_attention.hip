@@ -1001,10 +1001,10 @@ void attention_kernel(AttnArgs args) {
 
   // ---- phase 5: Y = Xbar / Z (Z: the lane groups' partial sums) --------------
   // Each wave stages its 32 rows in LDS (the chunk buffers are free by now)
-  // and stores them as whole rows, 16 bytes per lane and 16 B x (row bytes /
-  // 16) lanes per row, instead of 8-byte pieces of 16 rows per instruction.
-  // The 16-byte units of a staged row are XOR-swizzled by row, so the 16
-  // rows a fragment write touches hit different banks.
+  // and stores them as whole rows: 16 bytes per lane, a row's 16-byte units
+  // on consecutive lanes, instead of the fragments' 8-byte pieces of 16 rows
+  // per store instruction. The units of a staged row are XOR-swizzled by
+  // row, so the 16 rows a fragment write touches hit different banks.
   float rinv[QS];
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
