@@ -40,7 +40,10 @@
  *   - Logits are exactly Q.C (the paper leaves the 1/sqrt(d) scale out of its
  *     formulas, Eq. (standardattention)); callers fold any scale into Q.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
- *     stream). No call synchronises the device or allocates device memory.
+ *     stream). No call synchronises the device or allocates device memory:
+ *     the device calls enqueue kernels only (no memset or copy), so after one
+ *     call of an entry point on a device (it caches the device's attributes
+ *     and kernel settings) its calls can be captured in a HIP graph.
  *   - Arguments are validated on the host before anything is launched; a
  *     non-OK status means nothing was enqueued (AVQ_ERR_DEVICE: a launch was
  *     rejected). avq_last_error() then returns a message for the calling
