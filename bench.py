@@ -367,6 +367,14 @@ def main():
     # the MFMA peak of the kernel's own type: bf16 2.5 PFLOP/s, fp32 157.3 TFLOP/s
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     traffic = None if (args.tiled_importance or order is not None) else read_traffic()
+    # the precompute against HBM: K and V read once, the codebooks read once per
+    # head, parent indices, codes, counts and packed aggregates written once
+    esz = 2 if w.dtype == "bf16" else 4
+    Mtot = M0 * (1 + Ch)
+    bytes_pre = (2 * qh * d * esz + H * M0 * (1 + Ch) * d * esz
+                 + B * H * (2 * N * 4 + Mtot * 4 + avq.packed_bytes(x["K"].dtype, M0, Ch, d)))
+    t_pre = sum(v for k, v in stage_ms.items() if k != "attention_fwd")
+    pre_gbs = bytes_pre / (t_pre * 1e-3) / 1e9
     line = {
         "metric": METRIC,
         "value": qh / (ms_per_step * 1e-3),
@@ -395,6 +403,10 @@ def main():
                      "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
                      "flops_per_launch": flops_attn},
+        "precompute_roofline": {"kernels": [k for k in stage_ms if k != "attention_fwd"],
+                                "bound": "hbm", "achieved": pre_gbs, "peak": 8000.0,
+                                "unit": "GB/s", "frac": pre_gbs / 8000.0,
+                                "bytes_per_step": bytes_pre},
     }
     if not args.no_cpu_baseline:
         if args.cpu_threads > 0:
