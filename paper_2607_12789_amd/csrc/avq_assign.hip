@@ -441,6 +441,7 @@ constexpr int kChildThreads = 1024;
 constexpr int kChildWaves = kChildThreads / kWave;
 constexpr int kScanPerThread = 8;
 constexpr int kChildRound = kChildThreads * kScanPerThread;  // parent indices per round
+constexpr int kMinChildChunk = 256;  // fewest keys a split of the child compare takes
 constexpr int kMaxFam = 32;
 
 struct ChildLds {
@@ -650,13 +651,21 @@ hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, co
   if (!with_children) return hipSuccess;  // the caller runs the child compare
 
   // child compare: F parents per workgroup, and the keys split into chunks
-  // of one scan round each (the keys are independent: a workgroup scans only
-  // its chunk, so the splits add no scan work; they shorten each wave's
-  // chain of groups and let the grid fill the device in whole rounds)
+  // of at most one scan round each (the keys are independent: a workgroup
+  // scans only its chunk, so the splits add no scan work; they shorten each
+  // wave's chain of groups and let the grid fill the device in whole rounds).
+  // When the family ranges alone would leave CUs idle (few heads, few
+  // parents), the chunks shrink, to no fewer than kMinChildChunk keys, so
+  // that about one workgroup per CU runs.
   const int F = kMaxFam;
   const int ranges = (M0 + F - 1) / F;
   const long long base_grid = (long long)BH * ranges;
-  const int chunk = kChildRound;
+  int chunk = kChildRound;
+  if (base_grid < (long long)dev.cus) {
+    const long long per = ((long long)dev.cus + base_grid - 1) / base_grid;  // splits wanted
+    const long long c = ((long long)N + per - 1) / per;
+    chunk = (int)std::min<long long>(kChildRound, std::max<long long>(kMinChildChunk, (c + 63) / 64 * 64));
+  }
   const int splits = (N + chunk - 1) / chunk;
   grid = base_grid * splits;
   if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
