@@ -635,10 +635,11 @@ hipError_t launch_aggregate_dcs(int BH, int N, int M0, int Ch, const void* V,
 
 // Half waves per family. Each workgroup scans all codes of its head, so
 // splitting a family over more half waves (more, smaller workgroups) costs
-// scanning; it pays only when one half wave per family would walk a long
-// chain of value loads (at least 256 keys per parent) while fewer than half
-// the CUs have a workgroup (few heads, few parents). Then the fewest half
-// waves (2 or 4) that give half the CUs a workgroup.
+// scanning; it pays when fewer than half the CUs have a workgroup (few heads,
+// few parents) and either one half wave per family would walk a long chain
+// of value loads (at least 256 keys per parent) or the head's codes are one
+// scan round (then the extra scanning is that one round). Then the fewest
+// half waves (2 or 4) that give half the CUs a workgroup.
 template <typename T, int D, int CHM, bool FUSED>
 hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
                                const int32_t* code_idx, float* Vbar, int32_t* counts,
@@ -652,7 +653,7 @@ hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
     return (long long)BH * ((M0 + fam - 1) / fam);
   };
   const bool long_chains = (long long)N >= 256LL * M0;
-  if (!long_chains || grid(1) >= half_cus)
+  if ((!long_chains && N > kRound) || grid(1) >= half_cus)
     return launch_aggregate_dcs<T, D, CHM, 1, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
                                                      packed, fa, stream);
   if (grid(2) >= half_cus)
