@@ -635,11 +635,11 @@ hipError_t launch_aggregate_dcs(int BH, int N, int M0, int Ch, const void* V,
 
 // Half waves per family. Each workgroup scans all codes of its head, so
 // splitting a family over more half waves (more, smaller workgroups) costs
-// scanning; it pays when fewer than half the CUs have a workgroup (few heads,
-// few parents) and either one half wave per family would walk a long chain
-// of value loads (at least 256 keys per parent) or the head's codes are one
+// scanning; it pays when some CUs would have no workgroup (few heads, few
+// parents) and either one half wave per family would walk a long chain of
+// value loads (at least 256 keys per parent) or the head's codes are one
 // scan round (then the extra scanning is that one round). Then the fewest
-// half waves (2 or 4) that give half the CUs a workgroup.
+// half waves (2 or 4) that give every CU a workgroup.
 template <typename T, int D, int CHM, bool FUSED>
 hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
                                const int32_t* code_idx, float* Vbar, int32_t* counts,
@@ -647,16 +647,16 @@ hipError_t launch_aggregate_dc(int BH, int N, int M0, int Ch, const void* V,
   DeviceInfo dev;
   hipError_t e = device_info(&dev);
   if (e != hipSuccess) return e;
-  const long long half_cus = dev.cus > 1 ? dev.cus / 2 : 1;
+  const long long cus = dev.cus > 1 ? dev.cus : 1;
   auto grid = [&](int split) {
     const int fam = kFamilies / split;
     return (long long)BH * ((M0 + fam - 1) / fam);
   };
   const bool long_chains = (long long)N >= 256LL * M0;
-  if ((!long_chains && N > kRound) || grid(1) >= half_cus)
+  if ((!long_chains && N > kRound) || grid(1) >= cus)
     return launch_aggregate_dcs<T, D, CHM, 1, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
                                                      packed, fa, stream);
-  if (grid(2) >= half_cus)
+  if (grid(2) >= cus)
     return launch_aggregate_dcs<T, D, CHM, 2, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
                                                      packed, fa, stream);
   return launch_aggregate_dcs<T, D, CHM, 4, FUSED>(BH, N, M0, Ch, V, code_idx, Vbar, counts,
