@@ -257,11 +257,14 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
   //    sum the queue when it would overflow and once the codes are exhausted
   int qlen = 0;
   int next[kCodesPerThread];
+  auto load_round = [&](int b, int (&dst)[kCodesPerThread]) {
 #pragma unroll
-  for (int k = 0; k < kCodesPerThread; ++k) {
-    const int j = k * kAggThreads + tid;
-    next[k] = j < N ? codes[j] : -1;
-  }
+    for (int k = 0; k < kCodesPerThread; ++k) {
+      const int j = b + k * kAggThreads + tid;
+      dst[k] = j < N ? codes[j] : -1;
+    }
+  };
+  load_round(0, next);
   // family-local row of a code (or, FUSED, the family of a parent index);
   // -1 outside this range
   auto row_of = [&](int code) {
@@ -286,11 +289,6 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
 #pragma unroll
       for (int k = 0; k < kCodesPerThread; ++k) cur[k] = next[k];
 #pragma unroll
-      for (int k = 0; k < kCodesPerThread; ++k) {  // prefetch the next round
-        const int j = base + kRound + k * kAggThreads + tid;
-        next[k] = j < N ? codes[j] : -1;
-      }
-#pragma unroll
       for (int k = 0; k < kCodesPerThread; ++k) {
         const unsigned long long mk = __ballot(row_of(cur[k]) >= 0);
         if (lane == 0) L.wave_count[k][wave] = __popcll(mk);
@@ -303,6 +301,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       }
       __syncthreads();
       round_total = L.round_total;
+      load_round(base + kRound, next);  // prefetch the next round
     }
     // uniform across the workgroup
     const bool flush = done ? qlen > 0 : qlen + round_total > kQueueCap;
@@ -398,6 +397,12 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       }
       __syncthreads();
       qlen = 0;
+      // this round's codes and the next round's are loaded again rather than
+      // held in registers through the flush
+      if (!done) {
+        load_round(base, cur);
+        load_round(base + kRound, next);
+      }
     }
     if (done) break;
 #pragma unroll
@@ -406,7 +411,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       const int row = row_of(cur[k]);
       const unsigned long long mk = __ballot(row >= 0);
       if (row >= 0) {
-        const int slot = qlen + L.wave_off[k][wave] + __popcll(mk & ((1ull << lane) - 1ull));
+        const int slot = qlen + L.wave_off[k][wave] + bits_below(mk);
         L.qkey[slot] = base + k * kAggThreads + tid;
         L.qrow[slot] = (uint16_t)row;
       }

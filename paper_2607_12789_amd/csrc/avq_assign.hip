@@ -505,7 +505,7 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
 #pragma unroll
     for (int k = 0; k < kScanPerThread; ++k) {
       if (cur[k] >= 0) {
-        const int slot = L.wave_off[k][wave] + __popcll(mask[k] & ((1ull << lane) - 1ull));
+        const int slot = L.wave_off[k][wave] + bits_below(mask[k]);
         L.qkey[slot] = base + k * kChildThreads + tid;
         L.qfam[slot] = (unsigned char)cur[k];
         atomicAdd(&L.hist[cur[k]], 1);

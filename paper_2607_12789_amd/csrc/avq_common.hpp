@@ -42,6 +42,13 @@ __device__ __forceinline__ f32x4 mfma_f32(float a, float b, const f32x4& c) {
 __device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, kWave); }
 __device__ __forceinline__ int shfl_xor(int v, int mask) { return __shfl_xor(v, mask, kWave); }
 
+// Set bits of a wave-wide mask in the lanes below the calling one (v_mbcnt:
+// no lane mask held in registers).
+__device__ __forceinline__ int bits_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+
 // Data-parallel-primitive lane moves inside each row of 16 lanes (VALU, no
 // LDS). CTRL encodings: quad_perm [1,0,3,2] = 0xB1, [2,3,0,1] = 0x4E,
 // [3,2,1,0] = 0x1B, row_half_mirror = 0x141, row_ror:8 = 0x128.
