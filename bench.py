@@ -4,6 +4,10 @@
     python bench.py --sweep [--steps K] [--warmup W]
     python bench.py --codebook-update [--steps K] [--warmup W]
 
+Without --warmup the untimed warm-up runs whole steps for --warmup-ms of wall
+time (at least 10 steps): from idle the GPU clock takes some tens of
+milliseconds to come up, and steps timed before that measure the ramp.
+
 One step is the whole forward pass over one batch of synthetic inputs
 already resident in HBM: avq_assign_aggregate (the precompute of Alg. 1) ->
 avq_attention_fwd (--unfused-precompute: avq_assign -> avq_aggregate for the
@@ -14,8 +18,9 @@ children each, P=32, query block 128, bf16). Prints one JSON line:
 * value: query-token*heads per second of the whole step, B*H*N / t_step;
 * roofline: the fused attention kernel (the dominant one) against the bf16
   MFMA peak, its algorithmic flops 4 d (M0 + P Ch) per query-head divided by
-  its average launch duration over the timed steps (HIP events bracketing
-  each launch, on the launch stream); traffic is the
+  its average launch duration over the timed steps (HIP events on the launch
+  stream after each entry point, the end of one being the start of the next);
+  traffic is the
   HBM bytes per launch from the committed rocprofv3 counter summary, or null
   if the kernel source changed since those counters were taken;
 * cpu_baseline: the fp64 oracle timed on the host cores, whole passes over
@@ -114,43 +119,73 @@ class Runner:
             ["attention_fwd"]
 
     def step(self, ev=None):
-        # ev: events bracketing the entry points (HIP events on the stream
-        # the kernels are launched on, which is torch's current one)
+        # ev: one event recorded after each entry point (HIP events on the
+        # stream the kernels are launched on, which is torch's current one)
         avq, w, xd = self.avq, self.w, self.xd
-        k = 0
-        if ev: ev[0].record()
         if self.fused:
             avq.assign_aggregate(xd["K"], xd["V"], xd["Cp"], xd["Cc"], self.par, self.code,
                                  self.packed, self.counts)
         else:
             avq.assign(xd["K"], xd["Cp"], xd["Cc"], self.par, self.code)
-            if ev: ev[1].record()
+            if ev: ev[0].record()
             avq.aggregate(xd["V"], self.code, w.M0, w.Ch, self.packed, self.counts)
-        k = len(self.stages) - 1
-        if ev: ev[k].record()
+        if ev: ev[-2].record()
         avq.attention_fwd(xd["Q"], xd["Cp"], xd["Cc"], self.packed, w.P, w.block_q, Y=self.Y,
                           tiled_importance=self.tiled, query_order=self.order)
-        if ev: ev[k + 1].record()
+        if ev: ev[-1].record()
 
-    def timed(self, steps: int, warmup: int, cold: bool = False):
-        """Runs warmup + steps steps; returns (wall ms per step, per-step event
-        durations [steps][len(stages)] in ms). cold: a 1 GiB fill before each
-        step (outside the events) evicts the caches."""
+    def timed(self, steps: int, warmup, cold: bool = False, warmup_ms: float = 200.0):
+        """Runs the warm-up (warmup steps, or None: steps for warmup_ms of wall
+        time) and then steps timed steps; returns (wall ms per step, per-step
+        event durations [steps][len(stages)] in ms, warm-up steps run). Each
+        entry point is timed from the event before it (the previous entry
+        point's, or the start event) to its own. cold: a 1 GiB fill before
+        each step, with its own start event after the fill, evicts the
+        caches."""
         import torch
         flush = torch.empty(1 << 28, dtype=torch.float32, device=self.Y.device) if cold else None
-        for _ in range(warmup):
-            self.step()
+        warmed = warm_up(self.step, warmup, warmup_ms)
         n = len(self.stages)
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(steps)]
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n)] for _ in range(steps)]
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps if cold else 1)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        if not cold:
+            starts[0].record()
         for i in range(steps):
             if flush is not None:
                 flush.fill_(float(i))
+                starts[i].record()
             self.step(evs[i])
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t0) * 1e3 / steps
-        return wall, [[ev[k].elapsed_time(ev[k + 1]) for k in range(n)] for ev in evs]
+        per = []
+        for i in range(steps):
+            prev = starts[i] if cold else (starts[0] if i == 0 else evs[i - 1][-1])
+            row = []
+            for e in evs[i]:
+                row.append(prev.elapsed_time(e))
+                prev = e
+            per.append(row)
+        return wall, per, warmed
+
+
+def warm_up(step, warmup, warmup_ms: float) -> int:
+    """Runs warmup untimed steps, or, with warmup None, whole steps until
+    warmup_ms of wall time have passed (at least 10); returns the count."""
+    import torch
+    if warmup is not None:
+        for _ in range(warmup):
+            step()
+        return warmup
+    n = 0
+    t0 = time.perf_counter()
+    while n < 10 or (time.perf_counter() - t0) * 1e3 < warmup_ms:
+        for _ in range(10):
+            step()
+        n += 10
+        torch.cuda.synchronize()
+    return n
 
 
 def _median(v):
@@ -182,7 +217,7 @@ def sweep(args):
             continue
         x = inputs.generate(w)
         r = Runner(w, x, dev)
-        wall, per = r.timed(args.steps, args.warmup)
+        wall, per, warmed = r.timed(args.steps, args.warmup, warmup_ms=args.warmup_ms)
         step_ms = _median([sum(p) for p in per])
         k = {name: _median([p[i] for p in per]) for i, name in enumerate(r.stages)}
         qh = w.B * w.H * w.N
@@ -191,7 +226,7 @@ def sweep(args):
                "codes_precompute": w.M0 * (1 + w.Ch), "codes_attention": w.M0 + w.P * w.Ch,
                "ms_median": step_ms, "ms_wall_mean": wall, "qh_per_s": qh / (step_ms * 1e-3),
                "kernels_ms_median": k,
-               "steps": args.steps, "warmup": args.warmup}
+               "steps": args.steps, "warmup": warmed}
         rows.append(row)
         print(json.dumps(row), flush=True)
         del r, x
@@ -250,8 +285,7 @@ def codebook_bench(args):
         avq.codebook_update(sums, counts, S, Nm, M0, Ch, 0.99, Cp, Cc)
         if ev: ev[3].record()
 
-    for _ in range(args.warmup):
-        step()
+    warmed = warm_up(step, args.warmup, args.warmup_ms)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -268,7 +302,7 @@ def codebook_bench(args):
     print(json.dumps({
         "metric": "codebook EMA update step (App. A): assign + key aggregates + update",
         "value": B * H * N / (ms * 1e-3), "unit": "keys*heads/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "steps": args.steps, "warmup": warmed, "ms_per_step": ms,
         "higher_is_better": True, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.describe()}", "lambda": 0.99},
         "kernels_ms": {"assign": t[0], "aggregate_keys": t[1], "codebook_update": t[2]},
@@ -281,8 +315,11 @@ def codebook_bench(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default: as many as --warmup-ms takes)")
+    ap.add_argument("--warmup-ms", type=float, default=200.0,
+                    help="wall time of the default warm-up")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="least wall time the oracle baseline runs for")
@@ -347,7 +384,7 @@ def main():
     elif args.query_order == "random":
         order = torch.randperm(w.N, generator=torch.Generator().manual_seed(0)).to(torch.int32)
     runner = Runner(w, x, dev, args.tiled_importance, order, not args.unfused_precompute)
-    ms_per_step, per = runner.timed(args.steps, args.warmup, args.cold)
+    ms_per_step, per, warmed = runner.timed(args.steps, args.warmup, args.cold, args.warmup_ms)
     if args.cold:  # the wall clock includes the fills: the steps are the events
         ms_per_step = sum(sum(p) for p in per) / max(len(per), 1)
     # per-entry-point average duration over the timed steps
@@ -381,7 +418,7 @@ def main():
         "unit": UNIT,
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmed,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",

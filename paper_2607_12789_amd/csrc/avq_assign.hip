@@ -12,14 +12,15 @@
 // kernel) and the MFMA accumulator starts at ||c||^2, so the accumulator holds
 // the distance itself.
 //
-// parent_assign_kernel: one workgroup = 256 keys of one (batch, head): bf16
-// 8 waves of 32 keys (2 subtiles of 16), fp32 4 waves of 64 keys. The norms
-// of the head's parents are summed once per workgroup (one row per thread, in
-// order); the parent codebook streams through LDS in chunks of 64 rows by
-// direct global->LDS copies, double buffered. Every lane keeps a running
-// (distance, index) minimum over its rows in ascending codeword order with a
-// strict <, and the four lane groups merge lexicographically, so exact ties
-// go to the lowest index.
+// parent_stream_kernel (below) when the head's parent codebook fits the LDS
+// (always for bf16); otherwise (fp32 codebooks of more rows)
+// parent_assign_kernel: one workgroup = 256 keys of one (batch, head), 4
+// waves of 64 keys. The norms of the head's parents are summed once per
+// workgroup (one row per thread, in order); the parent codebook streams
+// through LDS in chunks of 64 rows by direct global->LDS copies, double
+// buffered. Every lane keeps a running (distance, index) minimum over its
+// rows in ascending codeword order with a strict <, and the four lane groups
+// merge lexicographically, so exact ties go to the lowest index.
 //
 // child_assign_kernel: one workgroup owns one (batch, head) and a range of F
 // parents. It scans the head's parent indices in rounds, buckets the keys of
@@ -52,50 +53,33 @@ __device__ __forceinline__ void copy16_lds(const void* src, void* lds) {
                                    (void __attribute__((address_space(3)))*)lds, 16, 0, 0);
 }
 
-template <typename T, int D>
+// fp32 only (a bf16 codebook of up to 512 rows always fits the stream kernel)
+template <int D>
 struct AssignCfg {
-  static constexpr bool kB = Elem<T>::kBf16;
-  // bf16: 8 waves of 32 keys (80 VGPRs at d = 128); fp32: 4 waves of 64 keys
-  static constexpr int kWaves = kB ? 8 : 4;
-  static constexpr int KS = kB ? 2 : 4;           // key subtiles (of 16) per wave
+  static constexpr int kWaves = 4;
+  static constexpr int KS = 4;                    // key subtiles (of 16) per wave
   static constexpr int kKeysPerBlock = kWaves * KS * 16;
   static constexpr int CW = 64;                   // codebook rows per chunk
-  static constexpr int KQ = kB ? D / 32 : D / 4;  // MFMA k-steps over d
-  static constexpr int ESZ = sizeof(T);
-  static constexpr int EPU = 16 / ESZ;
-  static constexpr int U = D * ESZ / 16;          // 16-byte units per row
+  static constexpr int KQ = D / 4;                // MFMA k-steps over d
+  static constexpr int EPU = 4;                   // values per 16-byte unit
+  static constexpr int U = D / 4;                 // 16-byte units per row
   static constexpr int COPIES = CW * U / 64;      // wave copies per chunk
   static constexpr int CPW = COPIES / kWaves;
-  static constexpr int CHUNK_BYTES = CW * D * ESZ;
+  static constexpr int CHUNK_BYTES = CW * D * 4;
   static constexpr int BUF_BYTES = CHUNK_BYTES;
   static constexpr int M0MAX = 512;
   static constexpr int LDS_BYTES = 2 * BUF_BYTES + M0MAX * 4;  // two chunks + all norms
   static_assert(COPIES % kWaves == 0, "copies split evenly over the waves");
 };
 
-// ||row||^2 of a codebook row in one fixed order (consecutive pairs of d)
-template <typename T, int D>
-__device__ __forceinline__ float row_norm(const T* row) {
-  float acc = 0.f;
-  if constexpr (Elem<T>::kBf16) {
-#pragma unroll
-    for (int d0 = 0; d0 < D; d0 += 8) acc = frag_sq<T>(*reinterpret_cast<const bf16x8*>(row + d0), acc);
-  } else {
-#pragma unroll 8
-    for (int d0 = 0; d0 < D; ++d0) acc = fmaf(row[d0], row[d0], acc);
-  }
-  return acc;
-}
-
-template <typename T, int D>
-__global__ __launch_bounds__((AssignCfg<T, D>::kWaves * 64)) void parent_assign_kernel(
-    const T* __restrict__ K, const T* __restrict__ Cp, int32_t* __restrict__ parent_idx,
+template <int D>
+__global__ __launch_bounds__((AssignCfg<D>::kWaves * 64)) void parent_assign_kernel(
+    const float* __restrict__ K, const float* __restrict__ Cp, int32_t* __restrict__ parent_idx,
     int32_t* __restrict__ code_idx, int H, int N, int M0, int blocks_per_bh) {
-  using Cfg = AssignCfg<T, D>;
-  constexpr bool kB = Cfg::kB;
+  using Cfg = AssignCfg<D>;
+  using T = float;
   constexpr int KS = Cfg::KS, CW = Cfg::CW, KQ = Cfg::KQ, U = Cfg::U, EPU = Cfg::EPU,
                 CPW = Cfg::CPW;
-  using Frag = typename std::conditional<kB, bf16x8, float>::type;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
 
   const int tid = threadIdx.x;
@@ -122,26 +106,27 @@ __global__ __launch_bounds__((AssignCfg<T, D>::kWaves * 64)) void parent_assign_
   const int n_chunks = (M0 + CW - 1) / CW;
   issue(0);
   float* lnorm = reinterpret_cast<float*>(lds_raw + 2 * Cfg::BUF_BYTES);  // [M0MAX]
-  for (int r = tid; r < n_chunks * CW; r += blockDim.x)
-    lnorm[r] = r < M0 ? row_norm<T, D>(cp_head + (size_t)r * D) : __builtin_inff();
+  // ||row||^2 in one fixed order (ascending d)
+  for (int r = tid; r < n_chunks * CW; r += blockDim.x) {
+    float acc = __builtin_inff();
+    if (r < M0) {
+      const T* row = cp_head + (size_t)r * D;
+      acc = 0.f;
+#pragma unroll 8
+      for (int d0 = 0; d0 < D; ++d0) acc = fmaf(row[d0], row[d0], acc);
+    }
+    lnorm[r] = acc;
+  }
 
   // key fragments: subtile s holds key key0 + 16 s + c; lane group g holds
-  // the d values of k-step kq at 32 kq + 8 g (bf16) or 4 kq + g (fp32)
-  Frag kf[KS][KQ];
+  // the d values of k-step kq at 4 kq + g
+  float kf[KS][KQ];
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     const int j = key0 + 16 * s + c;
     const T* row = K + ((size_t)bh * N + (j < N ? j : 0)) * D;
 #pragma unroll
-    for (int kq = 0; kq < KQ; ++kq) {
-      if constexpr (kB) {
-        bf16x8 v = *reinterpret_cast<const bf16x8*>(row + 32 * kq + 8 * g);
-        kf[s][kq] = times_minus2((j < N) ? v : bf16x8{});
-      } else {
-        float v = row[4 * kq + g];
-        kf[s][kq] = times_minus2((j < N) ? v : 0.f);
-      }
-    }
+    for (int kq = 0; kq < KQ; ++kq) kf[s][kq] = times_minus2((j < N) ? row[4 * kq + g] : 0.f);
   }
 
   float best[KS];
@@ -167,15 +152,9 @@ __global__ __launch_bounds__((AssignCfg<T, D>::kWaves * 64)) void parent_assign_
       f32x4 acc[KS];
 #pragma unroll
       for (int kq = 0; kq < KQ; ++kq) {
-        if constexpr (kB) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
+        const float a = lc[r * D + (kq ^ sw) * EPU + g];
 #pragma unroll
-          for (int s = 0; s < KS; ++s) acc[s] = mfma_bf16(a, kf[s][kq], kq == 0 ? nr : acc[s]);
-        } else {
-          const float a = lc[r * D + (kq ^ sw) * EPU + g];
-#pragma unroll
-          for (int s = 0; s < KS; ++s) acc[s] = mfma_f32(a, kf[s][kq], kq == 0 ? nr : acc[s]);
-        }
+        for (int s = 0; s < KS; ++s) acc[s] = mfma_f32(a, kf[s][kq], kq == 0 ? nr : acc[s]);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -214,19 +193,22 @@ __global__ __launch_bounds__((AssignCfg<T, D>::kWaves * 64)) void parent_assign_
 
 // ---------------------------------------------------------------------------
 // parent_stream_kernel: the same argmin when the head's whole parent codebook
-// fits half the LDS. Two workgroups per CU, each persistent over a run of
-// consecutive 256-key steps (normally of one (batch, head)): the codebook and
-// its norms are staged once per head, and the key fragments of the next step
-// load while the current step runs, so K streams from HBM without the gaps of
-// a one-shot workgroup. It keeps the keys unscaled and maximises
-// k.c - ||c||^2 / 2, which is the distance times -1/2 exactly.
+// fits the LDS (bf16: one 16-wave workgroup per CU, up to 150 KB, every
+// supported codebook; fp32: two 4-wave workgroups per CU, half the LDS
+// each). Each workgroup is persistent over a run of consecutive steps
+// (normally of one (batch, head)): the codebook and its norms are staged once
+// per head, and the key fragments of the next step load while the current
+// step runs, so K streams from HBM without the gaps of a one-shot workgroup.
+// It keeps the keys unscaled and maximises k.c - ||c||^2 / 2, which is the
+// distance times -1/2 exactly.
 template <typename T, int D>
 struct StreamCfg {
   static constexpr bool kB = Elem<T>::kBf16;
-  // bf16: 8 waves of 32 keys (under 128 VGPRs, four waves per SIMD with two
-  // workgroups per CU); fp32: 4 waves of 64 keys (its fragments need the
-  // registers of two waves per SIMD)
-  static constexpr int kWaves = kB ? 8 : 4;
+  // bf16: 16 waves of 32 keys (under 128 VGPRs, four waves per SIMD); fp32:
+  // 4 waves of 64 keys (its fragments need the registers of two waves per
+  // SIMD) and two workgroups per CU
+  static constexpr int kWaves = kB ? 16 : 4;
+  static constexpr int kPerCU = kB ? 1 : 2;       // workgroups per CU
   static constexpr int KS = kB ? 2 : 4;           // key subtiles (of 16) per wave
   static constexpr int kKeysPerStep = kWaves * KS * 16;
   static constexpr int KQ = kB ? D / 32 : D / 4;
@@ -234,10 +216,10 @@ struct StreamCfg {
   static constexpr int EPU = 16 / ESZ;
   static constexpr int U = D * ESZ / 16;
   static constexpr int ROW_BYTES = D * ESZ;
-  static constexpr int LDS_HALF = 80 * 1024;      // two workgroups per CU
+  static constexpr int LDS_CAP = kB ? 150 * 1024 : 80 * 1024;
   // codebook rows padded to whole pairs of 16-row tiles, then the norms
   static int lds_bytes(int M0) { return ((M0 + 31) / 32 * 32) * (ROW_BYTES + 4); }
-  static bool fits(int M0) { return lds_bytes(M0) <= LDS_HALF; }
+  static bool fits(int M0) { return lds_bytes(M0) <= LDS_CAP; }
 };
 
 template <typename T, int D>
@@ -610,40 +592,41 @@ template <typename T, int D>
 hipError_t launch_assign(int BH, int H, int N, int M0, int Ch, const void* K, const void* Cp,
                          const void* Cc, int32_t* parent_idx, int32_t* code_idx,
                          bool with_children, hipStream_t stream) {
-  using Cfg = AssignCfg<T, D>;
   using SCfg = StreamCfg<T, D>;
   long long grid;
   DeviceInfo dev;
   hipError_t e = device_info(&dev);
   if (e != hipSuccess) return e;
   if (SCfg::fits(M0)) {
-    // persistent: two workgroups per CU, each a run of whole steps
+    // persistent: kPerCU workgroups per CU, each a run of whole steps
     const int per_bh = (N + SCfg::kKeysPerStep - 1) / SCfg::kKeysPerStep;
     const long long n_steps = (long long)BH * per_bh;
     if (n_steps > 0x7fffffff) return hipErrorInvalidConfiguration;
-    const long long slots = 2LL * (dev.cus > 0 ? dev.cus : 1);
+    const long long slots = (long long)SCfg::kPerCU * (dev.cus > 0 ? dev.cus : 1);
     const long long per = (n_steps + slots - 1) / slots;
     grid = (n_steps + per - 1) / per;
     const int lds = SCfg::lds_bytes(M0);
     constexpr int slot_s = 32 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
-    e = ensure_dynamic_lds((const void*)parent_stream_kernel<T, D>, SCfg::LDS_HALF, slot_s);
+    e = ensure_dynamic_lds((const void*)parent_stream_kernel<T, D>, SCfg::LDS_CAP, slot_s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((parent_stream_kernel<T, D>), dim3((unsigned)grid),
                        dim3(SCfg::kWaves * kWave), lds, stream,
                        static_cast<const T*>(K), static_cast<const T*>(Cp), parent_idx,
                        Ch == 0 ? code_idx : nullptr, H, N, M0, per_bh, (int)n_steps);
-  } else {
+  } else if constexpr (!Elem<T>::kBf16) {
+    using Cfg = AssignCfg<D>;
     const int per_bh = (N + Cfg::kKeysPerBlock - 1) / Cfg::kKeysPerBlock;
     grid = (long long)BH * per_bh;
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-    constexpr int slot_a = 24 + (Elem<T>::kBf16 ? 0 : 2) + (D == 128 ? 1 : 0);
-    e = ensure_dynamic_lds((const void*)parent_assign_kernel<T, D>, Cfg::LDS_BYTES, slot_a);
+    constexpr int slot_a = 24 + (D == 128 ? 1 : 0);
+    e = ensure_dynamic_lds((const void*)parent_assign_kernel<D>, Cfg::LDS_BYTES, slot_a);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((parent_assign_kernel<T, D>), dim3((unsigned)grid),
-                       dim3(Cfg::kWaves * kWave),
-                       Cfg::LDS_BYTES, stream, static_cast<const T*>(K),
-                       static_cast<const T*>(Cp), parent_idx, Ch == 0 ? code_idx : nullptr, H, N,
-                       M0, per_bh);
+    hipLaunchKernelGGL((parent_assign_kernel<D>), dim3((unsigned)grid),
+                       dim3(Cfg::kWaves * kWave), Cfg::LDS_BYTES, stream,
+                       static_cast<const float*>(K), static_cast<const float*>(Cp), parent_idx,
+                       Ch == 0 ? code_idx : nullptr, H, N, M0, per_bh);
+  } else {
+    return hipErrorInvalidValue;  // not reached: bf16 codebooks of up to 512 rows fit
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;

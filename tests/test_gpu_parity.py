@@ -75,7 +75,7 @@ EDGE = {
     "fp32_d128_bq256_multichunk": small(dtype="f32", d=128, M0=200, Ch=4, P=20, N=600,
                                         block_q=256),
     # an fp32 codebook past the stream kernel's LDS share: the one-shot parent
-    # kernel
+    # kernel (bf16 codebooks of every supported size stream)
     "fp32_m0_320_d64": small(dtype="f32", M0=320, Ch=2, P=24, N=900, B=1, H=2),
     # flat codebook (Ch = 0): VQ attention over the parents alone
     "flat": small(Ch=0, P=0),
