@@ -166,11 +166,16 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
     constexpr bool kPrefetch = D == 64;
     const int h = bh % fa.H;
     const T* kh = static_cast<const T*>(fa.K) + (size_t)bh * N * D;
-    if (tid < kFamilies) L.hist[tid] = 0;
+    // thread and lane index through an empty asm statement: the LDS
+    // addresses below are formed here, not held (or spilled) from the start
+    int tq = tid, lq = lane;
+    asm volatile("" : "+v"(tq), "+v"(lq));
+    if (tq < kFamilies) L.hist[tq] = 0;
     __syncthreads();
-    for (int e = tid; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
+    for (int e = tq; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
     __syncthreads();
     if (wave == 0) {  // family starts and group starts (nfam <= 32 lanes)
+      const int lane = lq;
       const int v = lane < nfam ? L.hist[lane] : 0;
       const int gv = (v + 15) / 16;
       int incl = v, gincl = gv;
@@ -307,11 +312,15 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
     const bool flush = done ? qlen > 0 : qlen + round_total > kQueueCap;
     if (flush) {
       if constexpr (FUSED) child_step(qlen);
-      for (int r = tid; r < rows; r += kAggThreads) L.hist[r] = 0;
+      // as in child_step: indices through an empty asm statement
+      int tq = tid, lq = lane;
+      asm volatile("" : "+v"(tq), "+v"(lq));
+      for (int r = tq; r < rows; r += kAggThreads) L.hist[r] = 0;
       __syncthreads();
-      for (int e = tid; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
+      for (int e = tq; e < qlen; e += kAggThreads) atomicAdd(&L.hist[L.qrow[e]], 1);
       __syncthreads();
       if (wave == 0) {  // exclusive scan of the row histogram
+        const int lane = lq;
         int carry = 0;
         for (int r0 = 0; r0 < rows; r0 += kWave) {
           const int r = r0 + lane;

@@ -94,6 +94,9 @@ struct Elem<bf16> {
 // Exclusive prefix sums of n <= 128 counts (run by one whole wave): off[i] =
 // cnt[0] + ... + cnt[i-1]; returns the total to every lane.
 __device__ __forceinline__ int prefix128(const int* cnt, int* off, int n, int lane) {
+  // the lane index passes an empty asm statement: the addresses below are
+  // computed here, not hoisted out of the caller's loop and held (or spilled)
+  asm volatile("" : "+v"(lane));
   const int a = lane < n ? cnt[lane] : 0;
   const int b = lane + kWave < n ? cnt[lane + kWave] : 0;
   int ia = a, ib = b;
