@@ -197,13 +197,7 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
     for (int kq = 0; kq < KQ; ++kq) {
       if constexpr (kB) {
-        // non-temporal: each query row is read once per launch, and its lines
-        // would otherwise displace the chunks every tile of the head re-reads
-        // and the next pass's keys and values
-        const u32x4 raw = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(qrow + 32 * kq + 8 * g));
-        bf16x8 v;
-        __builtin_memcpy(&v, &raw, sizeof(v));
+        bf16x8 v = *reinterpret_cast<const bf16x8*>(qrow + 32 * kq + 8 * g);
         qf[s][kq] = qvalid[s] ? v : bf16x8{};
       } else {
         float v = qrow[4 * kq + g];
