@@ -113,8 +113,6 @@ struct AttnArgs {
   int H, N, M0, Ch, P, block_q, n_tiles;
 };
 
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 // A raw buffer resource over bytes [p, p + bytes): stride 0, no format
 // conversion (the gfx9 word-3 setting); loads past the end read 0.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -1049,15 +1047,9 @@ void attention_kernel(AttnArgs args) {
       const uint4 v = *reinterpret_cast<const uint4*>(ys + r * YROW + ((u ^ yswz(r)) * 16));
       const int q = row0 + r;
       const int tok = q < q_end ? token_row(q) : -1;
-      // non-temporal: the output is not read again by this kernel, and its
-      // lines would otherwise sit dirty in the caches until the next pass's
-      // reads of K and V force them out
-      if (tok >= 0) {
-        const u32x4 vv = {v.x, v.y, v.z, v.w};
-        __builtin_nontemporal_store(
-            vv, reinterpret_cast<u32x4*>(static_cast<unsigned char*>(args.Y) +
-                                         ((size_t)bh * N + tok) * YROW + u * 16));
-      }
+      if (tok >= 0)
+        *reinterpret_cast<uint4*>(static_cast<unsigned char*>(args.Y) +
+                                  ((size_t)bh * N + tok) * YROW + u * 16) = v;
     }
   } else {
 #pragma unroll
