@@ -96,6 +96,8 @@ EDGE = {
     # every key of a head in one workgroup's range, more than its key queue
     # holds: the queue is bucketed and summed in the middle of the scan
     "agg_queue_overflow": small(M0=8, Ch=8, P=3, N=20000, B=1, H=2, block_q=256),
+    "agg_queue_overflow_d128": small(M0=8, Ch=8, P=3, N=20000, B=1, H=2, block_q=256,
+                                     d=128),
     "agg_queue_overflow_flat": small(Ch=0, P=0, M0=4, N=30000, B=1, H=1, block_q=256),
 }
 
@@ -125,7 +127,8 @@ def test_edge_case_unfused(name):
 
 @pytest.mark.parametrize("name", ["ragged_n", "ch1", "ch2", "ch8_bq200", "m0_512_bq256",
                                   "agg_split2", "agg_split4", "agg_queue_overflow",
-                                  "dirichlet_sparse", "keys_stay", "large_logits"])
+                                  "agg_queue_overflow_d128", "dirichlet_sparse", "keys_stay",
+                                  "large_logits"])
 def test_fused_equals_unfused(name):
     """avq_assign_aggregate gives avq_assign's indices and avq_aggregate's
     counts exactly (the same child compare routine on the same inputs), and
