@@ -4,9 +4,9 @@
     python bench.py --sweep [--steps K] [--warmup W]
     python bench.py --codebook-update [--steps K] [--warmup W]
 
-Without --warmup the untimed warm-up runs whole steps for --warmup-ms of wall
-time (at least 10 steps): from idle the GPU clock takes some tens of
-milliseconds to come up, and steps timed before that measure the ramp.
+Before the W warm-up steps, whole untimed steps run for --warmup-ms of wall
+time (at least 10; reported as "preheat"): from idle the GPU clock takes some
+tens of milliseconds to come up, and steps timed before that measure the ramp.
 
 One step is the whole forward pass over one batch of synthetic inputs
 already resident in HBM: avq_assign_aggregate (the precompute of Alg. 1) ->
@@ -134,17 +134,17 @@ class Runner:
                           tiled_importance=self.tiled, query_order=self.order)
         if ev: ev[-1].record()
 
-    def timed(self, steps: int, warmup, cold: bool = False, warmup_ms: float = 200.0):
-        """Runs the warm-up (warmup steps, or None: steps for warmup_ms of wall
-        time) and then steps timed steps; returns (wall ms per step, per-step
-        event durations [steps][len(stages)] in ms, warm-up steps run). Each
-        entry point is timed from the event before it (the previous entry
-        point's, or the start event) to its own. cold: a 1 GiB fill before
-        each step, with its own start event after the fill, evicts the
-        caches."""
+    def timed(self, steps: int, warmup: int, cold: bool = False, warmup_ms: float = 200.0):
+        """Runs the pre-heat (steps for warmup_ms of wall time), warmup
+        untimed steps, and then steps timed steps; returns (wall ms per step,
+        per-step event durations [steps][len(stages)] in ms, pre-heat steps
+        run). Each entry point is timed from the event before it (the
+        previous entry point's, or the start event) to its own. cold: a 1 GiB
+        fill before each step, with its own start event after the fill,
+        evicts the caches."""
         import torch
         flush = torch.empty(1 << 28, dtype=torch.float32, device=self.Y.device) if cold else None
-        warmed = warm_up(self.step, warmup, warmup_ms)
+        preheat = warm_up(self.step, warmup, warmup_ms)
         n = len(self.stages)
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n)] for _ in range(steps)]
         starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps if cold else 1)]
@@ -167,24 +167,23 @@ class Runner:
                 row.append(prev.elapsed_time(e))
                 prev = e
             per.append(row)
-        return wall, per, warmed
+        return wall, per, preheat
 
 
-def warm_up(step, warmup, warmup_ms: float) -> int:
-    """Runs warmup untimed steps, or, with warmup None, whole steps until
-    warmup_ms of wall time have passed (at least 10); returns the count."""
+def warm_up(step, warmup: int, warmup_ms: float) -> int:
+    """Brings the GPU to its working clock with whole untimed steps for
+    warmup_ms of wall time (at least 10 steps; none with warmup_ms 0), then
+    runs the warmup untimed steps; returns the pre-heat step count."""
     import torch
-    if warmup is not None:
-        for _ in range(warmup):
-            step()
-        return warmup
     n = 0
     t0 = time.perf_counter()
-    while n < 10 or (time.perf_counter() - t0) * 1e3 < warmup_ms:
+    while warmup_ms > 0 and (n < 10 or (time.perf_counter() - t0) * 1e3 < warmup_ms):
         for _ in range(10):
             step()
         n += 10
         torch.cuda.synchronize()
+    for _ in range(warmup):
+        step()
     return n
 
 
@@ -217,7 +216,7 @@ def sweep(args):
             continue
         x = inputs.generate(w)
         r = Runner(w, x, dev)
-        wall, per, warmed = r.timed(args.steps, args.warmup, warmup_ms=args.warmup_ms)
+        wall, per, preheat = r.timed(args.steps, args.warmup, warmup_ms=args.warmup_ms)
         step_ms = _median([sum(p) for p in per])
         k = {name: _median([p[i] for p in per]) for i, name in enumerate(r.stages)}
         qh = w.B * w.H * w.N
@@ -226,7 +225,8 @@ def sweep(args):
                "codes_precompute": w.M0 * (1 + w.Ch), "codes_attention": w.M0 + w.P * w.Ch,
                "ms_median": step_ms, "ms_wall_mean": wall, "qh_per_s": qh / (step_ms * 1e-3),
                "kernels_ms_median": k,
-               "steps": args.steps, "warmup": warmed}
+               "steps": args.steps, "warmup": args.warmup,
+               "preheat": {"steps": preheat, "ms": args.warmup_ms}}
         rows.append(row)
         print(json.dumps(row), flush=True)
         del r, x
@@ -285,7 +285,7 @@ def codebook_bench(args):
         avq.codebook_update(sums, counts, S, Nm, M0, Ch, 0.99, Cp, Cc)
         if ev: ev[3].record()
 
-    warmed = warm_up(step, args.warmup, args.warmup_ms)
+    preheat = warm_up(step, args.warmup, args.warmup_ms)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -302,7 +302,8 @@ def codebook_bench(args):
     print(json.dumps({
         "metric": "codebook EMA update step (App. A): assign + key aggregates + update",
         "value": B * H * N / (ms * 1e-3), "unit": "keys*heads/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": warmed, "ms_per_step": ms,
+        "steps": args.steps, "warmup": args.warmup,
+        "preheat": {"steps": preheat, "ms": args.warmup_ms}, "ms_per_step": ms,
         "higher_is_better": True, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.describe()}", "lambda": 0.99},
         "kernels_ms": {"assign": t[0], "aggregate_keys": t[1], "codebook_update": t[2]},
@@ -316,10 +317,11 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed warm-up steps (default: as many as --warmup-ms takes)")
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="untimed warm-up steps, after the pre-heat")
     ap.add_argument("--warmup-ms", type=float, default=200.0,
-                    help="wall time of the default warm-up")
+                    help="wall time of the pre-heat: untimed steps before the warm-up steps "
+                         "that bring the GPU clock up (0: none)")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="least wall time the oracle baseline runs for")
@@ -384,7 +386,7 @@ def main():
     elif args.query_order == "random":
         order = torch.randperm(w.N, generator=torch.Generator().manual_seed(0)).to(torch.int32)
     runner = Runner(w, x, dev, args.tiled_importance, order, not args.unfused_precompute)
-    ms_per_step, per, warmed = runner.timed(args.steps, args.warmup, args.cold, args.warmup_ms)
+    ms_per_step, per, preheat = runner.timed(args.steps, args.warmup, args.cold, args.warmup_ms)
     if args.cold:  # the wall clock includes the fills: the steps are the events
         ms_per_step = sum(sum(p) for p in per) / max(len(per), 1)
     # per-entry-point average duration over the timed steps
@@ -418,7 +420,8 @@ def main():
         "unit": UNIT,
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": warmed,
+        "warmup": args.warmup,
+        "preheat": {"steps": preheat, "ms": args.warmup_ms},
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",

@@ -28,9 +28,9 @@ def test_bench_line_fields():
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    print("\n[case] bench.py --workload c2 --steps 5 --warmup 3", flush=True)
-    r = run_bench("--workload", "c2", "--steps", "5", "--warmup", "3", "--cpu-seconds", "0.2",
-                  "--cpu-max-passes", "1")
+    print("\n[case] bench.py --workload c2 --steps 5 --warmup 3 --warmup-ms 50", flush=True)
+    r = run_bench("--workload", "c2", "--steps", "5", "--warmup", "3", "--warmup-ms", "50",
+                  "--cpu-seconds", "0.2", "--cpu-max-passes", "1")
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [l for l in r.stdout.splitlines() if l.strip()]
     assert len(lines) == 1, r.stdout
@@ -40,6 +40,8 @@ def test_bench_line_fields():
               "roofline", "cpu_baseline"):
         assert k in j, k
     assert j["n_gpus"] == 1 and j["steps"] == 5 and j["warmup"] == 3
+    # the clock pre-heat before the warm-up steps is reported on its own
+    assert j["preheat"]["ms"] == 50 and j["preheat"]["steps"] >= 10
     assert j["dtype"] == "bf16" and j["data"] == "synthetic"
     c = j["config"]
     qh = c["B"] * c["H"] * c["N"]
