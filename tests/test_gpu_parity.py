@@ -64,6 +64,10 @@ EDGE = {
     "bq1": small(N=50, block_q=1, P=2),
     "m0_512_bq256": small(M0=512, Ch=8, P=64, block_q=256, N=1536, d=128, B=1, H=2),
     "m0_300_bq128": small(M0=300, Ch=4, P=30, block_q=128, N=1024, B=1, H=2),
+    # the largest ragged codebook the parent stream kernel holds (padding rows
+    # in its last 32-row pair), and the smallest codebook
+    "m0_500_d128": small(M0=500, Ch=8, P=40, block_q=128, N=1200, d=128, B=1, H=2),
+    "m0_one": small(M0=1, Ch=2, P=1, N=300, B=1, H=2),
     # few heads: the aggregation splits the parents over several workgroups
     "m0_24_split": small(M0=24, Ch=2, P=5, B=1, H=1, N=700),
     "m0_44_split": small(M0=44, Ch=4, P=5, B=1, H=1, N=700),
