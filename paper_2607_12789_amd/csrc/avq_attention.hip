@@ -554,18 +554,23 @@ void attention_kernel(AttnArgs args) {
   // (biased logits in S, recovered sums in rs), in place. Empty children and
   // padding: exp2(-inf) = 0 and n = 0, so the weight is exactly 0; the
   // recovered term is clamped below 2^64, so 0 times it stays 0.
+  // (full chunks only, Ch = 8 or 16: both tiles of the pair belong to one
+  // parent, whose recovered sums rs[0] and rs[1] are equal, so its term is
+  // computed once)
   auto child_weights = [&](const unsigned char* B, int b, f32x4 (&S)[2][QS],
                            const float (&rs)[2][QS]) {
     const float scale = kLog2e / (float)Ch;
+    float er[QS];
+#pragma unroll
+    for (int s = 0; s < QS; ++s) er[s] = exp2_hw(fminf(fmaf(rs[0][s], scale, -m[s]), 64.f));
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       const f32x4 n4 = info4(B, 2 * b + h2, 0);
 #pragma unroll
       for (int s = 0; s < QS; ++s) {
-        const float er = exp2_hw(fminf(fmaf(rs[h2][s], scale, -m[s]), 64.f));
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float w = fmaf(-n4[r], er, exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])));
+          const float w = fmaf(-n4[r], er[s], exp2_hw(fmaf(S[h2][s][r], kLog2e, -m[s])));
           S[h2][s][r] = w;
           zp[s] += w;
         }
