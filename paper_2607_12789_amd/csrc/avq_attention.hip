@@ -467,11 +467,12 @@ void attention_kernel(AttnArgs args) {
     bool over = false;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
+      // a running three-way max: two new values per instruction
       mx[s] = S0[0][s][0];
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mx[s] = fmaxf(mx[s], fmaxf(S0[h2][s][r], S1[h2][s][r]));
+        for (int r = 0; r < 4; ++r) mx[s] = fmaxf(fmaxf(mx[s], S0[h2][s][r]), S1[h2][s][r]);
       over |= mx[s] > thr[s];
     }
     if (__ballot(over) == 0) return;
