@@ -47,9 +47,11 @@
 //   2. importance (Eq. (importance)) with the final max and denominator: the
 //      last parent chunk's weights are still in registers when both are
 //      final, and are scaled by 1/Z there; a second sweep recomputes the
-//      logits of the other chunks and takes exp(t - m - ln Z) directly; sums
-//      over the tile's queries by a reduce-scatter butterfly over lanes, then
-//      a fixed order over waves. TILED instead takes the importance of App. B
+//      logits of the other chunks, with queries as the MFMA rows, and takes
+//      exp(t - m - ln Z) directly; sums over the tile's queries in registers
+//      and across lanes (a butterfly over the 16 query lanes of a row for the
+//      last chunk, row swaps over the 4 lane groups in the sweep), then a
+//      fixed order over waves. TILED instead takes the importance of App. B
 //      inside phase 1, chunk by chunk, and skips the second sweep;
 //   3. top-P in one wave: a threshold on the importance bits, built bit by
 //      bit from the top, finds the P-th largest value; ties at it go to the
@@ -170,8 +172,6 @@ void attention_kernel(AttnArgs args) {
   const bool has_rows = row0 < q_end;                                 // wave-uniform
   const int n_active = (q_end - q_begin + Cfg::RPW - 1) / Cfg::RPW;  // waves with rows
   const unsigned char* pk = args.packed + (size_t)bh * PL.bytes;
-  const T* means = reinterpret_cast<const T*>(pk);
-  const float* info = reinterpret_cast<const float*>(pk + PL.info_off);
   const T* cp_head = Cp + (size_t)h * M0 * D;
   const T* cc_head = Cc + (size_t)h * M0 * Ch * D;
 
@@ -329,7 +329,12 @@ void attention_kernel(AttnArgs args) {
   };
 
   // ---- S^T tile (16 codewords x 16 queries) for chunk tile tt ----------------
-  auto logits = [&](const unsigned char* B, int tt, f32x4 (&out)[QS], const f32x4& init) {
+  // (qrows: the operands swapped, so the tile is S itself, queries as the D
+  // rows: lane (g, c) holds queries 4 g + r of the codeword in chunk row
+  // 32 (tt/2) + 8 (c/4) + 4 (tt%2) + c % 4; both MFMA operands have the same
+  // lane layout)
+  auto logits = [&](const unsigned char* B, int tt, f32x4 (&out)[QS], const f32x4& init,
+                    bool qrows) {
     const T* lc = reinterpret_cast<const T*>(B + Cfg::OFF_C);
     const int r = 32 * (tt / 2) + 8 * (c / 4) + 4 * (tt % 2) + (c % 4);
     const int sw = row_swizzle<U>(r);
@@ -338,11 +343,15 @@ void attention_kernel(AttnArgs args) {
       if constexpr (kB) {
         const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lc[r * D + ((4 * kq + g) ^ sw) * EPU]);
 #pragma unroll
-        for (int s = 0; s < QS; ++s) out[s] = mfma_bf16(a, qf[s][kq], kq == 0 ? init : out[s]);
+        for (int s = 0; s < QS; ++s)
+          out[s] = qrows ? mfma_bf16(qf[s][kq], a, kq == 0 ? init : out[s])
+                         : mfma_bf16(a, qf[s][kq], kq == 0 ? init : out[s]);
       } else {
         const float a = lc[r * D + (kq ^ sw) * EPU + g];
 #pragma unroll
-        for (int s = 0; s < QS; ++s) out[s] = mfma_f32(a, qf[s][kq], kq == 0 ? init : out[s]);
+        for (int s = 0; s < QS; ++s)
+          out[s] = qrows ? mfma_f32(qf[s][kq], a, kq == 0 ? init : out[s])
+                         : mfma_f32(a, qf[s][kq], kq == 0 ? init : out[s]);
       }
     }
   };
@@ -580,13 +589,23 @@ void attention_kernel(AttnArgs args) {
   };
   // logits of the chunk's two tile pairs; parents start from ln n
   // (bf16: the A fragments of tile tt + 1 are read from LDS while the
-  // products of tile tt run; scheduling barriers keep that order)
+  // products of tile tt run; scheduling barriers keep that order). qrows:
+  // the tiles are S, queries as the D rows (see logits), each lane's column
+  // starting from its codeword's ln n.
   auto chunk_logits = [&](const unsigned char* B, bool with_ln, f32x4 (&S0)[2][QS],
-                          f32x4 (&S1)[2][QS]) {
+                          f32x4 (&S1)[2][QS], bool qrows = false) {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     f32x4 init[TPC];
 #pragma unroll
-    for (int tt = 0; tt < TPC; ++tt) init[tt] = with_ln ? info4(B, tt, 1) : zero;
+    for (int tt = 0; tt < TPC; ++tt) {
+      if (qrows) {
+        const float* li = reinterpret_cast<const float*>(B + Cfg::OFF_I);
+        const float l = li[(4 * (tt / 2) + c / 4) * 16 + 8 + 4 * (tt % 2) + c % 4];
+        init[tt] = f32x4{l, l, l, l};
+      } else {
+        init[tt] = with_ln ? info4(B, tt, 1) : zero;
+      }
+    }
     if constexpr (kB) {
       const T* lc = reinterpret_cast<const T*>(B + Cfg::OFF_C);
       bf16x8 a[2][KQ];
@@ -607,15 +626,16 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
           for (int s = 0; s < QS; ++s) {
             f32x4& o = tt < 2 ? S0[tt][s] : S1[tt - 2][s];
-            o = mfma_bf16(a[tt % 2][kq], qf[s][kq], kq == 0 ? init[tt] : o);
+            o = qrows ? mfma_bf16(qf[s][kq], a[tt % 2][kq], kq == 0 ? init[tt] : o)
+                      : mfma_bf16(a[tt % 2][kq], qf[s][kq], kq == 0 ? init[tt] : o);
           }
         __builtin_amdgcn_sched_barrier(0);
       }
     } else {
-      logits(B, 0, S0[0], init[0]);
-      logits(B, 1, S0[1], init[1]);
-      logits(B, 2, S1[0], init[2]);
-      logits(B, 3, S1[1], init[3]);
+      logits(B, 0, S0[0], init[0], qrows);
+      logits(B, 1, S0[1], init[1], qrows);
+      logits(B, 2, S1[0], init[2], qrows);
+      logits(B, 3, S1[1], init[3], qrows);
     }
   };
 
@@ -648,8 +668,8 @@ void attention_kernel(AttnArgs args) {
           S1[0][s] = mfma_bf16(a[1][kq], qf[s][kq], kq == 0 ? zero : S1[0][s]);
         }
     } else {
-      logits(B, 0, S0[0], zero);
-      logits(B, 2, S1[0], zero);
+      logits(B, 0, S0[0], zero, false);
+      logits(B, 2, S1[0], zero, false);
     }
     // the recovered sums (Ch = 2, 4: only the even tile's rows enter; the odd
     // tile is zero here, as 0 * inf would poison the unused cases), then the
@@ -759,6 +779,46 @@ void attention_kernel(AttnArgs args) {
     const int tt = k / 4, r = k % 4;
     lw[(slot * MAXW + wave) * CW + 32 * (tt / 2) + 8 * g + 4 * (tt % 2) + r] = u[0];
   };
+  // The same from the importance sweep's S tiles (chunk_logits with qrows):
+  // normalised weights exp2(S log2 e - mz) with the shift of query
+  // 16 s + 4 g + r in mzq[s][r]; each lane sums its 8 queries of a tile, then
+  // the four lane groups are reduced by two 32-lane and one 16-lane row swap,
+  // which leave lane group g with the sum of tile g.
+  auto importance_qrows = [&](const f32x4 (&S0)[2][QS], const f32x4 (&S1)[2][QS],
+                              const float (&mzq)[QS][4], int slot) {
+    float u[TPC];
+#pragma unroll
+    for (int tt = 0; tt < TPC; ++tt) {
+      float p[QS][4];
+#pragma unroll
+      for (int s = 0; s < QS; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          p[s][r] = exp2_hw(fmaf(tt < 2 ? S0[tt][s][r] : S1[tt - 2][s][r], kLog2e, -mzq[s][r]));
+      float acc = (p[0][0] + p[0][1]) + (p[0][2] + p[0][3]);
+#pragma unroll
+      for (int s = 1; s < QS; ++s) acc += (p[s][0] + p[s][1]) + (p[s][2] + p[s][3]);
+      u[tt] = acc;
+    }
+    // rows of 32 lanes: (u0, u2) -> lanes 0-31 hold u0 summed over groups
+    // g and g + 2, lanes 32-63 u2; likewise (u1, u3); then rows of 16
+    // (v_permlane32_swap / v_permlane16_swap: the odd rows of x trade places
+    // with the even rows of y; the sum of the two results adds row pairs)
+    auto swap_add = [](float x, float y, auto rows32_tag) {
+      const unsigned ux = __float_as_uint(x), uy = __float_as_uint(y);
+      if constexpr (decltype(rows32_tag)::value) {
+        const auto xy = __builtin_amdgcn_permlane32_swap(ux, uy, false, false);
+        return __uint_as_float(xy[0]) + __uint_as_float(xy[1]);
+      } else {
+        const auto xy = __builtin_amdgcn_permlane16_swap(ux, uy, false, false);
+        return __uint_as_float(xy[0]) + __uint_as_float(xy[1]);
+      }
+    };
+    const float a = swap_add(u[0], u[2], std::true_type{});
+    const float b = swap_add(u[1], u[3], std::true_type{});
+    const float tot = swap_add(a, b, std::false_type{});
+    lw[(slot * MAXW + wave) * CW + 32 * (g / 2) + 8 * (c / 4) + 4 * (g % 2) + c % 4] = tot;
+  };
   // sum the wave partials of chunk k (slot k % 2) in a fixed order
   auto importance_flush = [&](int k) {
     if (tid < CW) {
@@ -859,9 +919,14 @@ void attention_kernel(AttnArgs args) {
       // chunks 0 .. n_pchunks - 2 again; the last one's partials (slot
       // (n_pchunks - 1) % 2) are summed before the sweep writes any slot
       const int n_sweep = n_pchunks - 1;
-      float one[QS];
+      // the shift of query 16 s + 4 g + r, from the lane that holds it
+      float mzq[QS][4];
+      if (has_rows) {
 #pragma unroll
-      for (int s = 0; s < QS; ++s) one[s] = 1.f;
+        for (int s = 0; s < QS; ++s)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mzq[s][r] = __shfl(mz[s], 4 * g + r, kWave);
+      }
       __syncthreads();
       importance_flush(n_pchunks - 1);
       issue_parent(0, 0, false);
@@ -872,17 +937,8 @@ void attention_kernel(AttnArgs args) {
         const unsigned char* B = buffer(k % Cfg::NBUF);
         if (has_rows) {
           f32x4 S0[2][QS], S1[2][QS];
-          chunk_logits(B, true, S0, S1);
-#pragma unroll
-          for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-            for (int s = 0; s < QS; ++s)
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                S0[h2][s][r] = exp2_hw(fmaf(S0[h2][s][r], kLog2e, -mz[s]));
-                S1[h2][s][r] = exp2_hw(fmaf(S1[h2][s][r], kLog2e, -mz[s]));
-              }
-          importance_partials(S0, S1, one, k % 2);
+          chunk_logits(B, true, S0, S1, true);
+          importance_qrows(S0, S1, mzq, k % 2);
         }
         if (Cfg::NBUF == 1 && k + 1 < n_sweep) {
           __syncthreads();
