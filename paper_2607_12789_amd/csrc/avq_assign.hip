@@ -174,15 +174,8 @@ __global__ __launch_bounds__((AssignCfg<D>::kWaves * 64)) void parent_assign_ker
   // merge the four lane groups: lexicographic (distance, index) minimum
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
-#pragma unroll
-    for (int m = 16; m <= 32; m <<= 1) {
-      const float ob = shfl_xor(best[s], m);
-      const int oi = shfl_xor(bidx[s], m);
-      if (ob < best[s] || (ob == best[s] && oi < bidx[s])) {
-        best[s] = ob;
-        bidx[s] = oi;
-      }
-    }
+    merge_xor<16, false>(best[s], bidx[s]);
+    merge_xor<32, false>(best[s], bidx[s]);
     const int j = key0 + 16 * s + c;
     if (g == 0 && j < N) {
       parent_idx[(size_t)bh * N + j] = bidx[s];
@@ -400,15 +393,8 @@ __global__ __launch_bounds__((StreamCfg<T, D>::kWaves * 64)) void parent_stream_
     const int key0 = (st % steps_per_bh) * Cfg::kKeysPerStep + wave * KS * 16;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-#pragma unroll
-      for (int m = 16; m <= 32; m <<= 1) {
-        const float ob = shfl_xor(best[s], m);
-        const int oi = shfl_xor(bidx[s], m);
-        if (ob > best[s] || (ob == best[s] && oi < bidx[s])) {
-          best[s] = ob;
-          bidx[s] = oi;
-        }
-      }
+      merge_xor<16, true>(best[s], bidx[s]);
+      merge_xor<32, true>(best[s], bidx[s]);
       const int j = key0 + 16 * s + c;
       if (g == 0 && j < N) {
         parent_idx[(size_t)bh * N + j] = bidx[s];

@@ -487,8 +487,7 @@ void attention_kernel(AttnArgs args) {
     if (__ballot(over) == 0) return;
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
-      mx[s] = fmaxf(mx[s], shfl_xor(mx[s], 16));
-      mx[s] = fmaxf(mx[s], shfl_xor(mx[s], 32));
+      mx[s] = max_xor<32>(max_xor<16>(mx[s]));
       const float mnew = mx[s] > thr[s] ? mx[s] * kLog2e : m[s];
       const float scs = exp2_hw(m[s] - mnew);
       zp[s] *= scs;
@@ -530,7 +529,7 @@ void attention_kernel(AttnArgs args) {
       const float a = a01 + (v0[2] + v0[3]);
       const float bs = (v1[0] + v1[1]) + (v1[2] + v1[3]);
       const float ab = a + bs;
-      const float ab16 = ab + shfl_xor(ab, 16);
+      const float ab16 = add_xor<16>(ab);
       rs[0][s] = fmaf(w2, a01, fmaf(w4, a, fmaf(w8, ab, w16 * ab16)));
       rs[1][s] = fmaf(w2, a01, fmaf(w4, bs, fmaf(w8, ab, w16 * ab16)));
     }
@@ -837,8 +836,7 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
       float z = zp[s];
-      z += shfl_xor(z, 16);
-      z += shfl_xor(z, 32);
+      z = add_xor<32>(add_xor<16>(z));
       mz[s] = qvalid[s] ? m[s] + log2_hw(z) : __builtin_inff();
     }
   };
@@ -856,16 +854,14 @@ void attention_kernel(AttnArgs args) {
       const f32x4 n4 = info4(B, tt, 0);
       cnt += (n4[0] + n4[1]) + (n4[2] + n4[3]);
     }
-    cnt += shfl_xor(cnt, 16);
-    cnt += shfl_xor(cnt, 32);
+    cnt = add_xor<32>(add_xor<16>(cnt));
     seen += cnt;  // integers below 2^24: exact
     // weight / Ztilde = W * seen / (N * Z), W and Z relative to the same max
     float mul[QS];
 #pragma unroll
     for (int s = 0; s < QS; ++s) {
       float z = zp[s];
-      z += shfl_xor(z, 16);
-      z += shfl_xor(z, 32);
+      z = add_xor<32>(add_xor<16>(z));
       mul[s] = (qvalid[s] && seen > 0.f) ? seen / ((float)N * z) : 0.f;
     }
     importance_partials(W0, W1, mul, k % 2);
@@ -1071,8 +1067,7 @@ void attention_kernel(AttnArgs args) {
 #pragma unroll
   for (int s = 0; s < QS; ++s) {
     float z = zp[s];
-    z += shfl_xor(z, 16);
-    z += shfl_xor(z, 32);
+    z = add_xor<32>(add_xor<16>(z));
     rinv[s] = 1.f / z;
   }
   constexpr int YROW = D * Cfg::ESZ;         // bytes of one Y row

@@ -84,9 +84,8 @@ __device__ __forceinline__ void child_rows(
     float part = 0.f;
 #pragma unroll
     for (int kq = 0; kq < KQ; ++kq) part = frag_sq<T>(cf[t2][kq], part);
-    const float p01 = part + shfl_xor(part, 16);
-    const float p23 = shfl_xor(p01, 32);
-    const float nrm = (g < 2) ? p01 + p23 : p23 + p01;
+    // (lane groups 0 + 1, then + (2 + 3), the same order in every lane)
+    const float nrm = add_xor<32>(add_xor<16>(part));
 #pragma unroll
     for (int r = 0; r < 4; ++r) cn[t2][r] = __shfl(nrm, 4 * g + r, kWave);
 #pragma unroll
@@ -141,15 +140,8 @@ __device__ __forceinline__ int child_pick(
   // parent distance from lane group 0; children by the lexicographic
   // (distance, child) minimum over the lane groups
   dpar = __shfl(dpar, c, kWave);
-#pragma unroll
-  for (int m = 16; m <= 32; m <<= 1) {
-    const float ob = shfl_xor(dch, m);
-    const int oi = shfl_xor(cbest, m);
-    if (ob < dch || (ob == dch && oi < cbest)) {
-      dch = ob;
-      cbest = oi;
-    }
-  }
+  merge_xor<16, false>(dch, cbest);
+  merge_xor<32, false>(dch, cbest);
   return dch < dpar ? 1 + cbest : 0;
 }
 

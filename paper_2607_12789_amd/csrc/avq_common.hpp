@@ -39,8 +39,50 @@ __device__ __forceinline__ f32x4 mfma_f32(float a, float b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, kWave); }
-__device__ __forceinline__ int shfl_xor(int v, int mask) { return __shfl_xor(v, mask, kWave); }
+// Row swaps of gfx950 (v_permlane16_swap / v_permlane32_swap of a register
+// with itself: VALU, no LDS round trip): every lane receives the value of the
+// even and of the odd row of its pair of 16-lane (ROW = 16) or 32-lane rows,
+// i.e. its own value and that of lane l ^ ROW, in row order.
+template <int ROW>
+__device__ __forceinline__ void row_pair(unsigned x, unsigned& even, unsigned& odd) {
+  static_assert(ROW == 16 || ROW == 32, "rows of 16 or 32 lanes");
+  if constexpr (ROW == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    even = r[0];
+    odd = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    even = r[0];
+    odd = r[1];
+  }
+}
+// x + (x of lane l ^ ROW) in every lane: the same sum as with a shuffle, as
+// the addition commutes
+template <int ROW>
+__device__ __forceinline__ float add_xor(float x) {
+  unsigned e, o;
+  row_pair<ROW>(__float_as_uint(x), e, o);
+  return __uint_as_float(e) + __uint_as_float(o);
+}
+template <int ROW>
+__device__ __forceinline__ float max_xor(float x) {
+  unsigned e, o;
+  row_pair<ROW>(__float_as_uint(x), e, o);
+  return fmaxf(__uint_as_float(e), __uint_as_float(o));
+}
+// (value, index) of lanes l and l ^ ROW merged in both: the larger value
+// (kMax) or the smaller one, the lower index on ties
+template <int ROW, bool kMax>
+__device__ __forceinline__ void merge_xor(float& v, int& i) {
+  unsigned ve, vo, ie, io;
+  row_pair<ROW>(__float_as_uint(v), ve, vo);
+  row_pair<ROW>((unsigned)i, ie, io);
+  const float a = __uint_as_float(ve), b = __uint_as_float(vo);
+  const int ia = (int)ie, ib = (int)io;
+  const bool take_b = (kMax ? b > a : b < a) || (b == a && ib < ia);
+  v = take_b ? b : a;
+  i = take_b ? ib : ia;
+}
 
 // Set bits of a wave-wide mask in the lanes below the calling one (v_mbcnt:
 // no lane mask held in registers).
