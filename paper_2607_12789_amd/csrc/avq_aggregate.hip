@@ -178,16 +178,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       const int lane = lq;
       const int v = lane < nfam ? L.hist[lane] : 0;
       const int gv = (v + 15) / 16;
-      int incl = v, gincl = gv;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off, kWave);
-        const int gy = __shfl_up(gincl, off, kWave);
-        if (lane >= off) {
-          incl += y;
-          gincl += gy;
-        }
-      }
+      const int incl = wave_incl_scan(v), gincl = wave_incl_scan(gv);
       if (lane < nfam) {
         L.fstart[lane] = incl - v;
         L.fcursor[lane] = incl - v;
@@ -325,18 +316,13 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
         for (int r0 = 0; r0 < rows; r0 += kWave) {
           const int r = r0 + lane;
           const int v = r < rows ? L.hist[r] : 0;
-          int incl = v;
-#pragma unroll
-          for (int off = 1; off < kWave; off <<= 1) {
-            const int y = __shfl_up(incl, off, kWave);
-            if (lane >= off) incl += y;
-          }
+          const int incl = wave_incl_scan(v);
           if (r < rows) {
             L.start[r] = carry + incl - v;
             L.cursor[r] = carry + incl - v;
             L.total[r] += v;
           }
-          carry += __shfl(incl, kWave - 1, kWave);
+          carry += last_lane(incl);
         }
         if (lane == 0) L.start[rows] = carry;
       }

@@ -504,16 +504,7 @@ __global__ __launch_bounds__(kChildThreads) void child_assign_kernel(
     if (wave == 0) {
       const int v = lane < nfam ? L.hist[lane] : 0;
       const int gv = (v + 15) / 16;
-      int incl = v, gincl = gv;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off, kWave);
-        const int gy = __shfl_up(gincl, off, kWave);
-        if (lane >= off) {
-          incl += y;
-          gincl += gy;
-        }
-      }
+      const int incl = wave_incl_scan(v), gincl = wave_incl_scan(gv);
       if (lane < nfam) {
         L.start[lane] = incl - v;
         L.cursor[lane] = incl - v;

@@ -139,7 +139,7 @@ __device__ __forceinline__ int child_pick(
   }
   // parent distance from lane group 0; children by the lexicographic
   // (distance, child) minimum over the lane groups
-  dpar = __shfl(dpar, c, kWave);
+  dpar = from_row0(dpar);
   merge_xor<16, false>(dch, cbest);
   merge_xor<32, false>(dch, cbest);
   return dch < dpar ? 1 + cbest : 0;

@@ -70,6 +70,15 @@ __device__ __forceinline__ float max_xor(float x) {
   row_pair<ROW>(__float_as_uint(x), e, o);
   return fmaxf(__uint_as_float(e), __uint_as_float(o));
 }
+// The value of lane l % 16 (row 0) in every lane: row 0 into row 1 and row 2
+// into row 3 (the even rows of the 16-lane swap), then the lower half into
+// the upper one (the even row of the 32-lane swap).
+__device__ __forceinline__ float from_row0(float x) {
+  unsigned e, o, e2, o2;
+  row_pair<16>(__float_as_uint(x), e, o);
+  row_pair<32>(e, e2, o2);
+  return __uint_as_float(e2);
+}
 // (value, index) of lanes l and l ^ ROW merged in both: the larger value
 // (kMax) or the smaller one, the lower index on ties
 template <int ROW, bool kMax>
@@ -83,6 +92,23 @@ __device__ __forceinline__ void merge_xor(float& v, int& i) {
   v = take_b ? b : a;
   i = take_b ? ib : ia;
 }
+
+// Inclusive prefix sum over the 64 lanes of a wave with data-parallel-primitive
+// adds (no LDS): a Hillis-Steele scan inside each row of 16 lanes (row_shr
+// 1, 2, 4, 8; lanes whose source lies before the row start add 0), then the
+// last lane of row 0 into row 1 and of row 2 into row 3 (row_bcast:15), and
+// the last lane of row 1 into rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15, rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31, rows 2 and 3
+  return x;
+}
+// The value of the wave's last lane, in a scalar register.
+__device__ __forceinline__ int last_lane(int x) { return __builtin_amdgcn_readlane(x, kWave - 1); }
 
 // Set bits of a wave-wide mask in the lanes below the calling one (v_mbcnt:
 // no lane mask held in registers).
@@ -141,20 +167,11 @@ __device__ __forceinline__ int prefix128(const int* cnt, int* off, int n, int la
   asm volatile("" : "+v"(lane));
   const int a = lane < n ? cnt[lane] : 0;
   const int b = lane + kWave < n ? cnt[lane + kWave] : 0;
-  int ia = a, ib = b;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int ya = __shfl_up(ia, o, kWave);
-    const int yb = __shfl_up(ib, o, kWave);
-    if (lane >= o) {
-      ia += ya;
-      ib += yb;
-    }
-  }
-  const int ta = __shfl(ia, kWave - 1, kWave);
+  const int ia = wave_incl_scan(a), ib = wave_incl_scan(b);
+  const int ta = last_lane(ia);
   if (lane < n) off[lane] = ia - a;
   if (lane + kWave < n) off[lane + kWave] = ta + ib - b;
-  return ta + __shfl(ib, kWave - 1, kWave);
+  return ta + last_lane(ib);
 }
 
 // Maps a linear workgroup index to a tile index so that consecutive tiles run
