@@ -310,7 +310,7 @@ __global__ __launch_bounds__((StreamCfg<T, D>::kWaves * 64)) void parent_stream_
 
     // per key subtile: the largest value so far, its 16-row tile, and that
     // tile's 4 values of the lane (the row within the tile is found once at
-    // the end): 9 VALU per tile and subtile instead of 12 for a running
+    // the end): 8 VALU per tile and subtile instead of 12 for a running
     // (value, row) pair
     float best[KS];
     int btile[KS];
@@ -359,9 +359,12 @@ __global__ __launch_bounds__((StreamCfg<T, D>::kWaves * 64)) void parent_stream_
         for (int s = 0; s < KS; ++s) {
           const f32x4 v = acc[h2][s];
           if constexpr (kB) {
-            const float tmax = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-            const bool gt = tmax > best[s];  // strict: the earlier tile keeps a tie
-            best[s] = gt ? tmax : best[s];
+            // the new best is a max of the tile's values and the old best
+            // (two three-way maxima); it exceeds the old one only if the tile
+            // holds a larger value (strict: the earlier tile keeps a tie)
+            const float nb = fmaxf(fmaxf(fmaxf(fmaxf(v[0], v[1]), v[2]), v[3]), best[s]);
+            const bool gt = nb > best[s];
+            best[s] = nb;
             btile[s] = gt ? tt + h2 : btile[s];
 #pragma unroll
             for (int q = 0; q < 4; ++q) bv[s][q] = gt ? v[q] : bv[s][q];
