@@ -332,8 +332,12 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const T* __restr
       __syncthreads();
       if (fam < nfam) {
         // the family's keys, bucketed by row, in kInFlight<CHM, T> batches; the
-        // running row sum goes into the table when its row ends
-        const int r_begin = fam * (1 + Ch);
+        // running row sum goes into the table when its row ends. The family
+        // index passes an empty asm statement: its row addresses are formed
+        // here, not held (or spilled) from the kernel start.
+        int fq = fam;
+        asm volatile("" : "+v"(fq));
+        const int r_begin = fq * (1 + Ch);
         const int fb = L.start[r_begin], fe = L.start[r_begin + 1 + Ch];
         // this half wave's share of the family's keys
         const int kb = fb + (fe - fb) * part / SPLIT, ke = fb + (fe - fb) * (part + 1) / SPLIT;
