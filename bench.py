@@ -35,6 +35,7 @@ against the effective codebook size (linear scaling is slope 1).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -344,6 +345,10 @@ def main():
     ap.add_argument("--query-order", choices=["token", "gilbert", "random"], default="token",
                     help="order of the queries: token order, or the tokens as a square grid "
                          "along a Gilbert curve, or a random permutation")
+    ap.add_argument("--top-p", type=int, default=None,
+                    help="run the workload with this P instead of its own (a diagnostic of the "
+                         "attention's phases: 0 leaves the parent sweep and the output alone); "
+                         "the line then names the override and carries no traffic figure")
     ap.add_argument("--codebook-update", action="store_true",
                     help="time the codebook EMA step (App. A) instead")
     ap.add_argument("--sweep", action="store_true",
@@ -373,6 +378,13 @@ def main():
         return
     w = inputs.WORKLOADS[args.workload]
     x = inputs.generate(w)
+    name = w.name
+    if args.top_p is not None:  # the same inputs, another number of selected parents
+        if not 0 <= args.top_p <= w.M0:
+            print(f"--top-p must lie in [0, M0 = {w.M0}]", file=sys.stderr)
+            sys.exit(2)
+        w = dataclasses.replace(w, P=args.top_p)
+        name = f"{w.name} with P overridden to {w.P}"
     dev = torch.device("cuda:0")
     B, H, N, d, M0, Ch, P = w.B, w.H, w.N, w.d, w.M0, w.Ch, w.P
     order = None
@@ -405,7 +417,8 @@ def main():
     achieved = flops_attn / (t_attn * 1e-3) / 1e12
     # the MFMA peak of the kernel's own type: bf16 2.5 PFLOP/s, fp32 157.3 TFLOP/s
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    traffic = None if (args.tiled_importance or order is not None) else read_traffic()
+    traffic = (None if (args.tiled_importance or order is not None or args.top_p is not None)
+               else read_traffic())
     # the precompute against HBM: K and V read once, the codebooks read once per
     # head, parent indices, codes, counts and packed aggregates written once
     esz = 2 if w.dtype == "bf16" else 4
@@ -428,7 +441,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: {w.describe()}", "B": B, "H": H, "N": N, "d": d,
+        "config": {"workload": f"{name}: {w.describe()}", "B": B, "H": H, "N": N, "d": d,
                    "M0": M0, "Ch": Ch, "P": P, "block_q": w.block_q,
                    "importance": "tiled (App. B, 64-parent tiles)" if args.tiled_importance
                    else "exact", "query_order": args.query_order,
